@@ -1,0 +1,300 @@
+"""Pins for the fp64 CPU oracle: each test checks it against something other
+than itself -- a closed form, a library routine on a special case, brute-force
+finite differences, a construction from the paper's proofs, or a number the
+paper prints.  CPU only."""
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+import scipy.special
+import torch
+
+import oracle
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def rng(seed):
+    return np.random.Generator(np.random.PCG64(seed))
+
+
+def rand_layer(seed, T, d_in, d_out, r, scale_a=None, scale_b=None):
+    g = rng(seed)
+    X = g.standard_normal((T, d_in))
+    A = g.standard_normal((r, d_in)) * (scale_a if scale_a else 1 / math.sqrt(d_in))
+    B = g.standard_normal((d_out, r)) * (scale_b if scale_b else 1 / math.sqrt(r))
+    dY = g.standard_normal((T, d_out))
+    return X, A, B, dY
+
+
+def relerr(a, b):
+    nb = np.linalg.norm(b)
+    return np.linalg.norm(a - b) / (nb if nb > 0 else 1.0)
+
+
+# --------------------------------------------------------------------------
+# sigma: SiLU special values and identities (Prop. 1 needs sigma(0)=0, sigma'(0)!=0)
+# --------------------------------------------------------------------------
+
+def test_silu_special_values():
+    assert oracle.sigma("silu", 0.0) == 0.0
+    assert oracle.sigma_prime("silu", 0.0) == 0.5
+    e = math.e
+    # SiLU(1) = 1 * e/(1+e), SiLU(-1) = -1/(1+e)
+    assert oracle.sigma("silu", 1.0) == pytest.approx(e / (1 + e), rel=1e-15)
+    assert oracle.sigma("silu", -1.0) == pytest.approx(-1 / (1 + e), rel=1e-15)
+    # large |z|: no overflow, SiLU(z) -> z for z -> +inf, -> 0 for z -> -inf
+    assert oracle.sigma("silu", 800.0) == 800.0
+    assert oracle.sigma("silu", -800.0) == 0.0 or abs(oracle.sigma("silu", -800.0)) < 1e-300
+    assert math.isfinite(oracle.sigma_prime("silu", -800.0))
+    assert oracle.sigma("identity", -3.25) == -3.25
+    assert oracle.sigma_prime("identity", 7.0) == 1.0
+
+
+@pytest.mark.parametrize("z", [-6.0, -1.2784645, -1.0, -0.3, 0.0, 0.25, 1.0, 4.5])
+def test_silu_derivative_by_central_difference(z):
+    h = 1e-5
+    fd = (oracle.sigma("silu", z + h) - oracle.sigma("silu", z - h)) / (2 * h)
+    assert oracle.sigma_prime("silu", z) == pytest.approx(fd, abs=1e-9)
+
+
+@pytest.mark.parametrize("z", [-5.0, -0.7, 0.3, 2.0, 9.0])
+def test_silu_odd_part_identities(z):
+    # z s(z) - (-z) s(-z) = z (s(z) + s(-z)) = z, and its derivative: sigma'(z) + sigma'(-z) = 1
+    assert oracle.sigma("silu", z) - oracle.sigma("silu", -z) == pytest.approx(z, rel=1e-14)
+    assert oracle.sigma_prime("silu", z) + oracle.sigma_prime("silu", -z) == pytest.approx(1.0, rel=1e-14)
+
+
+def test_silu_against_scipy_expit():
+    zs = np.linspace(-30, 30, 601)
+    ours = np.array([oracle.sigma("silu", z) for z in zs])
+    np.testing.assert_allclose(ours, zs * scipy.special.expit(zs), rtol=1e-14, atol=1e-300)
+
+
+# --------------------------------------------------------------------------
+# identity sigma: the layer is the conventional low-rank product B A X (Sec. 3.3)
+# --------------------------------------------------------------------------
+
+@pytest.mark.parametrize("shape", [(1, 1, 1, 1), (7, 5, 4, 3), (33, 40, 24, 8), (64, 17, 29, 5)])
+def test_identity_sigma_is_low_rank_product(shape):
+    T, d_in, d_out, r = shape
+    X, A, B, dY = rand_layer(11, T, d_in, d_out, r)
+    Z, H, Y = oracle.cola_fwd(X, A, B, act="identity")
+    W = B @ A                                  # d_out x d_in, merged weight
+    assert relerr(Y, X @ W.T) < 1e-13
+    assert relerr(Z, H) == 0.0
+    dZ, dX, dA, dB = oracle.cola_bwd(X, Z, A, B, dY, act="identity")
+    G = dY.T @ X                               # dense weight gradient d_out x d_in
+    assert relerr(dX, dY @ W) < 1e-13
+    assert relerr(dA, B.T @ G) < 1e-13
+    assert relerr(dB, G @ A.T) < 1e-13
+    assert relerr(dZ, dY @ B) < 1e-13
+
+
+def test_dense_oracle_against_numpy_and_merged_cola():
+    T, d_in, d_out, r = 19, 23, 11, 6
+    X, A, B, dY = rand_layer(12, T, d_in, d_out, r)
+    W = rng(13).standard_normal((d_out, d_in))
+    Y = oracle.dense_fwd(X, W)
+    dX, dW = oracle.dense_bwd(X, W, dY)
+    assert relerr(Y, X @ W.T) < 1e-14
+    assert relerr(dX, dY @ W) < 1e-14
+    assert relerr(dW, dY.T @ X) < 1e-14
+    # CoLA with identity sigma equals the dense layer with W = B A
+    _, _, Yc = oracle.cola_fwd(X, A, B, act="identity")
+    assert relerr(Yc, oracle.dense_fwd(X, B @ A)) < 1e-13
+
+
+# --------------------------------------------------------------------------
+# SiLU gradients: brute-force central differences of L = <dY, Y(X, A, B)>
+# --------------------------------------------------------------------------
+
+@pytest.mark.parametrize("shape", [(1, 1, 1, 1), (3, 5, 4, 2), (7, 1, 4, 3), (7, 5, 1, 3)])
+def test_gradients_by_central_differences(shape):
+    T, d_in, d_out, r = shape
+    X, A, B, dY = rand_layer(21 + T, T, d_in, d_out, r, scale_a=0.9, scale_b=0.8)
+
+    def loss(X_, A_, B_):
+        return float(np.sum(dY * oracle.cola_fwd(X_, A_, B_, act="silu")[2]))
+
+    Z, _, _ = oracle.cola_fwd(X, A, B, act="silu")
+    _, dX, dA, dB = oracle.cola_bwd(X, Z, A, B, dY, act="silu")
+    h = 1e-5
+    for name, arr, grad in (("X", X, dX), ("A", A, dA), ("B", B, dB)):
+        fd = np.zeros_like(arr)
+        for idx in np.ndindex(arr.shape):
+            p = arr.copy(); p[idx] += h
+            m = arr.copy(); m[idx] -= h
+            args_p = {"X": X, "A": A, "B": B}; args_p[name] = p
+            args_m = {"X": X, "A": A, "B": B}; args_m[name] = m
+            fd[idx] = (loss(args_p["X"], args_p["A"], args_p["B"]) -
+                       loss(args_m["X"], args_m["A"], args_m["B"])) / (2 * h)
+        assert relerr(grad, fd) < 1e-7, name
+
+
+# --------------------------------------------------------------------------
+# library cross-check: torch fp64 autograd on the CPU
+# --------------------------------------------------------------------------
+
+@pytest.mark.parametrize("shape", [(16, 32, 24, 8), (37, 13, 29, 5), (64, 64, 64, 16)])
+def test_against_torch_fp64_autograd(shape):
+    T, d_in, d_out, r = shape
+    X, A, B, dY = rand_layer(31, T, d_in, d_out, r)
+    tX = torch.tensor(X, requires_grad=True)
+    tA = torch.tensor(A, requires_grad=True)
+    tB = torch.tensor(B, requires_grad=True)
+    tZ = tX @ tA.T
+    tZ.retain_grad()
+    tH = torch.nn.functional.silu(tZ)
+    tY = tH @ tB.T
+    tY.backward(torch.tensor(dY))
+    Z, H, Y = oracle.cola_fwd(X, A, B, act="silu")
+    dZ, dX, dA, dB = oracle.cola_bwd(X, Z, A, B, dY, act="silu")
+    for ours, ref in ((Z, tZ), (H, tH), (Y, tY), (dZ, tZ.grad), (dX, tX.grad),
+                      (dA, tA.grad), (dB, tB.grad)):
+        assert relerr(ours, ref.detach().numpy()) < 1e-13
+
+
+# --------------------------------------------------------------------------
+# constructions from the paper's proofs
+# --------------------------------------------------------------------------
+
+def test_prop1_limit_construction():
+    """Proof of Prop. 1: with A_tau = tau A and B_tau = B / (sigma'(0) tau),
+    B_tau sigma(A_tau X) -> B A X as tau -> 0.  For SiLU (sigma''(0) = 1/2,
+    sigma'''(0) = 0) the error is tau/2 * B (A X)^2 + O(tau^3): first order,
+    so it halves with tau, and error/tau tends to ||(1/2) (Z*Z) B^T||."""
+    T, d_in, d_out, r = 24, 12, 10, 4
+    X, A, B, _ = rand_layer(41, T, d_in, d_out, r)
+    sp0 = oracle.sigma_prime("silu", 0.0)
+    Ylin = X @ (B @ A).T
+    Zlin = X @ A.T
+    coef = np.linalg.norm(0.5 * (Zlin * Zlin) @ B.T)
+    errs = []
+    for tau in (1e-2, 5e-3, 2.5e-3):
+        _, _, Yt = oracle.cola_fwd(X, tau * A, B / (sp0 * tau), act="silu")
+        errs.append(np.linalg.norm(Yt - Ylin))
+        assert errs[-1] / tau == pytest.approx(coef, rel=5e-4)
+    assert errs[0] / errs[1] == pytest.approx(2.0, rel=1e-3)
+    assert errs[1] / errs[2] == pytest.approx(2.0, rel=1e-3)
+
+
+def test_lemma_esigma_zero_construction():
+    """Lemma (E_sigma = 0): if every row of A is u^T and B = [w, 0, ..., 0],
+    then B sigma(A X) = w sigma(u^T X), token-major: Y = sigma(X u) w^T."""
+    T, d_in, d_out, r = 31, 9, 7, 5
+    g = rng(51)
+    X = g.standard_normal((T, d_in))
+    u = g.standard_normal(d_in)
+    w = g.standard_normal(d_out)
+    A = np.tile(u, (r, 1))
+    B = np.zeros((d_out, r)); B[:, 0] = w
+    _, _, Y = oracle.cola_fwd(X, A, B, act="silu")
+    xu = X @ u
+    expect = np.outer(xu * scipy.special.expit(xu), w)
+    assert relerr(Y, expect) < 1e-14
+
+
+# --------------------------------------------------------------------------
+# sampled evaluation paths agree with the full oracle
+# --------------------------------------------------------------------------
+
+def test_sampled_rows_and_columns_match_full():
+    T, d_in, d_out, r = 40, 21, 13, 6
+    X, A, B, dY = rand_layer(61, T, d_in, d_out, r)
+    Z, H, Y = oracle.cola_fwd(X, A, B)
+    dZ, dX, dA, dB = oracle.cola_bwd(X, Z, A, B, dY)
+    rows = [0, 5, 39, 17]
+    s = oracle.cola_rows(X, A, B, dY, rows)
+    for k, full in (("Z", Z), ("H", H), ("Y", Y), ("dZ", dZ), ("dX", dX)):
+        assert relerr(s[k], full[rows]) < 1e-14, k
+    cols = [0, 5, 2]
+    dA_rows, dB_cols = oracle.cola_wgrad_cols(X, A, B, dY, cols)
+    assert relerr(dA_rows, dA[cols]) < 1e-13
+    assert relerr(dB_cols, dB[:, cols].T) < 1e-13
+    with pytest.raises(ValueError):
+        oracle.cola_rows(X, A, B, dY, [T])
+    with pytest.raises(ValueError):
+        oracle.cola_wgrad_cols(X, A, B, dY, [r])
+
+
+# --------------------------------------------------------------------------
+# FLOP counts (Sec. 3.4: 2MNK per GEMM; Table 'compute all methods'; App. B)
+# --------------------------------------------------------------------------
+
+def counted_flops_layer(T, d_in, d_out, r):
+    X, A, B, dY = rand_layer(71, T, d_in, d_out, r)
+    oracle.reset_macs()
+    Z, _, _ = oracle.cola_fwd(X, A, B)
+    fwd = 2 * oracle.macs()
+    oracle.reset_macs()
+    oracle.cola_bwd(X, Z, A, B, dY)
+    bwd = 2 * oracle.macs()
+    return fwd, bwd
+
+
+def counted_flops_dense(T, d_in, d_out):
+    g = rng(72)
+    X = g.standard_normal((T, d_in)); W = g.standard_normal((d_out, d_in))
+    dY = g.standard_normal((T, d_out))
+    oracle.reset_macs()
+    oracle.dense_fwd(X, W)
+    oracle.dense_bwd(X, W, dY)
+    return 2 * oracle.macs()
+
+
+@pytest.mark.parametrize("shape", [(3, 8, 5, 2), (16, 64, 40, 16)])
+def test_layer_flop_count(shape):
+    T, d_in, d_out, r = shape
+    fwd, bwd = counted_flops_layer(T, d_in, d_out, r)
+    assert fwd == 2 * T * r * (d_in + d_out)
+    assert bwd == 4 * T * r * (d_in + d_out)
+
+
+def block_flops(n, d, dff, r):
+    """Counted by running the oracle over the seven projections of a block."""
+    shapes = [(d, d)] * 4 + [(d, dff)] * 2 + [(dff, d)]
+    cola = sum(sum(counted_flops_layer(n, a, b, r)) for a, b in shapes)
+    dense = sum(counted_flops_dense(n, a, b) for a, b in shapes)
+    return cola, dense
+
+
+def test_block_flops_match_paper_formulas():
+    gold = json.load(open(os.path.join(GOLDEN, "paper_numbers.json")))
+    n, d, dff, r = 2, 24, 60, 6
+    cola, dense = block_flops(n, d, dff, r)
+    c = gold["cola_block_flops"]
+    f = gold["full_rank_block_flops"]
+    # Table 'compute all methods' minus the attention SDP term (12 n^2 d), which
+    # is not a linear projection
+    assert cola == c["coeff_ndr"] * n * d * r + c["coeff_nr_d_plus_dff"] * n * r * (d + dff)
+    assert dense == f["coeff_nd2"] * n * d * d + f["coeff_nd_dff"] * n * d * dff
+
+
+def test_break_even_rank():
+    """Sec. 3.4: CoLA is cheaper than full rank iff r < 0.62 d (d_ff = 2.5 d)."""
+    gold = json.load(open(os.path.join(GOLDEN, "paper_numbers.json")))
+    d = 100
+    dff = 250
+    cheaper = [r for r in range(1, d + 1) if block_flops(1, d, dff, r)[0] < block_flops(1, d, dff, r)[1]]
+    r_max = max(cheaper)
+    assert cheaper == list(range(1, r_max + 1))
+    assert round(r_max / d, 2) == gold["break_even_rank_over_d"]["value"]   # 62 / 100
+
+
+@pytest.mark.parametrize("size,dff", [("1B", 5461), ("7B", 11008)])
+def test_flop_ratio_at_paper_shapes(size, dff):
+    """Sec. 5.3 table prints CoLA at 0.40x the full-rank FLOPs for 1B and 7B.
+    Counted at the paper's r/d and a 256-token sequence, adding the SDP term
+    12 n^2 d that both methods share."""
+    gold = json.load(open(os.path.join(GOLDEN, "paper_numbers.json")))
+    shape = gold["llama_" + size]
+    d, r = shape["d"], shape["r"]
+    n = gold["seq_len"]["value"]
+    # per-token counts scale linearly in n: count at n = 1 and scale
+    cola1, dense1 = block_flops(1, d, dff, r)
+    sdp = 12 * n * n * d
+    ratio = (n * cola1 + sdp) / (n * dense1 + sdp)
+    assert abs(ratio - gold["flop_ratio_cola_vs_full_" + size]["value"]) <= 0.01
