@@ -1,0 +1,170 @@
+/*
+ * cola.h -- C ABI of libcola.so, the MI355X (gfx950) CoLA layer.
+ *
+ * The CoLA layer replaces a full-size linear projection h = W x by the
+ * low-rank auto-encoder h = B sigma(A x), with A in R^{r x d_in},
+ * B in R^{d_out x r} and sigma a pointwise nonlinearity
+ * (arXiv 2502.10940, Sec. 3.2, Eq. main-fwd; the same layer replaces the
+ * attention projections, Eq. full-rank-linear).  Its gradients follow the
+ * paper's 2x rule, two GEMMs per forward GEMM (Sec. 3.4):
+ *   dH = dY B,  dZ = dH (.) sigma'(Z),  dX = dZ A,  dA = dZ^T X,  dB = dY^T H.
+ * CoLA-M (Sec. 4.2, App. C) saves only the r-wide pre-activation Z = A x and
+ * recomputes H = sigma(Z) in backward; its outputs are bitwise those of CoLA.
+ *
+ * Layout.  Every tensor is row-major and token-major (one token per row; the
+ * paper's X in R^{d_in x n} is stored transposed):
+ *   X, dX  [T][ldx]  (d_in used per row)      A   [r][d_in]   contiguous
+ *   Y, dY  [T][ldy]  (d_out used per row)     B   [d_out][r]  contiguous
+ *   Z, H   [T][ldz]  (r used per row)         dA  [r][d_in]   fp32, contiguous
+ *                                             dB  [d_out][r]  fp32, contiguous
+ * A leading dimension of 0 means "contiguous" (ld = width).  Row padding
+ * (ld > width) is never read or written.
+ *
+ * Precision.  COLA_BF16: activations and weights are bf16, every product is
+ * accumulated in fp32, Z/H/dZ are rounded to bf16 (round to nearest even)
+ * when stored, and H = bf16(sigma(Z_bf16)) in both modes; dA, dB are fp32.
+ * COLA_F32: fp32 storage, fp32 arithmetic throughout (no reduced-precision
+ * shortcut).
+ *
+ * Ownership and streams.  The caller allocates every buffer, including the
+ * workspace sized by cola_workspace_bytes().  The library never allocates
+ * device memory, never frees, never synchronises: all work is enqueued on the
+ * given stream (a hipStream_t; NULL = the null stream), and the call returns
+ * once it is enqueued.  Buffers must stay valid until that work completes.
+ * Calls that share a workspace must be ordered on one stream.
+ *
+ * Errors.  Every entry point validates all of its arguments before it
+ * enqueues anything; on any error nothing is enqueued and the outputs are
+ * untouched.  No C++ exception crosses this boundary.
+ *
+ * Alignment.  Base pointers that are 16-byte aligned with ld a multiple of
+ * 16 bytes take the vector path; anything else is accepted and takes a
+ * per-element path (same results, slower).
+ *
+ * Determinism.  Results are bitwise reproducible run to run: the T-long
+ * weight-gradient sums are split into a fixed number of chunks whose fp32
+ * partials are added in a fixed order.
+ */
+#ifndef COLA_H
+#define COLA_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define COLA_ABI_VERSION 1
+
+/* A hipStream_t, kept opaque so this header needs no HIP headers. */
+typedef void* cola_stream_t;
+
+typedef enum { COLA_F32 = 0, COLA_BF16 = 1 } cola_dtype;
+
+/* sigma: identity (the conventional low-rank product B A x, Sec. 3.3) or
+ * SiLU z * logistic(z) (Swish, the activation of the paper's LLaMA runs). */
+typedef enum { COLA_ACT_IDENTITY = 0, COLA_ACT_SILU = 1 } cola_act;
+
+typedef enum {
+    COLA_OK = 0,
+    COLA_ERR_INVALID_ARG = 1,      /* NULL desc/pointer, bad enum, H vs recompute mismatch */
+    COLA_ERR_BAD_SHAPE = 2,        /* d_in, d_out or r < 1, T < 0, ld < width, size overflow */
+    COLA_ERR_WORKSPACE = 3,        /* ws_bytes below the size cola_workspace_bytes() returns */
+    COLA_ERR_HIP = 4,              /* a launch failed; cola_strerror() returns HIP's text */
+    COLA_ERR_UNSUPPORTED = 5       /* combination not compiled in */
+} cola_status;
+
+typedef struct {
+    int64_t T;          /* tokens (rows); T = 0 is an empty batch */
+    int64_t d_in;       /* input width  (>= 1) */
+    int64_t d_out;      /* output width (>= 1) */
+    int64_t r;          /* rank (>= 1); r >= min(d_in, d_out) is accepted */
+    int64_t ldx;        /* row pitch of X and dX in elements, 0 = d_in  */
+    int64_t ldy;        /* row pitch of Y and dY in elements, 0 = d_out */
+    int64_t ldz;        /* row pitch of Z and H in elements, 0 = r      */
+    int32_t dtype;      /* cola_dtype */
+    int32_t act;        /* cola_act */
+    int32_t recompute;  /* 0 = CoLA (H stored), 1 = CoLA-M (only Z stored) */
+} cola_desc;
+
+int cola_abi_version(void);
+
+/* Text for a status code; for COLA_ERR_HIP the text of the last failure. */
+const char* cola_strerror(int status);
+
+/* Workspace bytes for phase 0 (cola_fwd) or 1 (cola_bwd); 0 on an invalid
+ * descriptor.  Forward needs T*r elements when recompute = 1 (H lives only
+ * there), else nothing.  Backward needs dZ (T*r elements), H again when
+ * recompute = 1, and the fp32 partial sums of dA and dB. */
+size_t cola_workspace_bytes(const cola_desc* desc, int phase);
+
+/* Forward (Eq. main-fwd): Z = X A^T, H = sigma(Z), Y = H B^T.
+ * Writes Z and Y; writes H when recompute = 0 (H must then be non-NULL) and
+ * keeps H in the workspace when recompute = 1 (H must then be NULL). */
+int cola_fwd(const cola_desc* desc,
+             const void* X, const void* A, const void* B,
+             void* Y, void* Z, void* H,
+             void* ws, size_t ws_bytes, cola_stream_t stream);
+
+/* Backward (Sec. 3.4, 2x rule; CoLA-M recompute per Sec. 4.2):
+ *   dZ = (dY B) (.) sigma'(Z)   [and H = sigma(Z) into the workspace if recompute = 1]
+ *   dX = dZ A,  dA = dZ^T X,  dB = dY^T H.
+ * Reads the saved Z (and H when recompute = 0; H must be NULL when
+ * recompute = 1).  dX is overwritten in the storage dtype; dA and dB are
+ * overwritten in fp32 (not accumulated).  T = 0 writes dA = dB = 0. */
+int cola_bwd(const cola_desc* desc,
+             const void* dY, const void* X, const void* Z, const void* H,
+             const void* A, const void* B,
+             void* dX, float* dA, float* dB,
+             void* ws, size_t ws_bytes, cola_stream_t stream);
+
+/* Dense full-rank baseline on the same kernels (Eq. full-rank-linear and
+ * the 2x rule of Sec. 3.4): Y = X W^T, dX = dY W, dW = dY^T X, with
+ * W [d_out][d_in] contiguous and dW fp32 contiguous. */
+typedef struct {
+    int64_t T, d_in, d_out;
+    int64_t ldx, ldy;   /* 0 = contiguous */
+    int32_t dtype;      /* cola_dtype */
+} dense_desc;
+
+size_t dense_workspace_bytes(const dense_desc* desc, int phase);
+int dense_fwd(const dense_desc* desc, const void* X, const void* W, void* Y,
+              void* ws, size_t ws_bytes, cola_stream_t stream);
+int dense_bwd(const dense_desc* desc, const void* dY, const void* X, const void* W,
+              void* dX, float* dW, void* ws, size_t ws_bytes, cola_stream_t stream);
+
+/* Kernel timing (profiling aid).  While enabled, every kernel the library
+ * launches is bracketed by two HIP events on its stream; reading sums the
+ * elapsed times per kernel class and waits for the recorded events.
+ * Kernel classes: */
+typedef enum {
+    COLA_KC_FWD_Z = 0,     /* Z = X A^T with the sigma epilogue        */
+    COLA_KC_FWD_Y = 1,     /* Y = H B^T                                */
+    COLA_KC_BWD_DZ = 2,    /* dZ = (dY B) (.) sigma'(Z) [+ H recompute] */
+    COLA_KC_BWD_DX = 3,    /* dX = dZ A                                */
+    COLA_KC_BWD_DA = 4,    /* dA = dZ^T X (split over tokens)          */
+    COLA_KC_BWD_DB = 5,    /* dB = dY^T H (split over tokens)          */
+    COLA_KC_REDUCE = 6,    /* fixed-order sum of the dA/dB partials    */
+    COLA_KC_DENSE_FWD = 7, /* Y = X W^T                                */
+    COLA_KC_DENSE_DX = 8,  /* dX = dY W                                */
+    COLA_KC_DENSE_DW = 9,  /* dW = dY^T X                              */
+    COLA_KC_FILL = 10,     /* zero fill (empty batches)                */
+    COLA_KC_COUNT = 11
+} cola_kernel_class;
+
+/* Per-class totals since the last reset: launches, elapsed milliseconds,
+ * algorithmic flops (2 M N K per GEMM) and algorithmic bytes (each operand
+ * read once, each output written once).  Returns COLA_ERR_INVALID_ARG for a
+ * bad class or NULL pointers, COLA_ERR_HIP if an event failed. */
+int cola_timing_enable(int on);
+int cola_timing_reset(void);
+int cola_timing_read(int kernel_class, int64_t* launches, double* ms,
+                     double* flops, double* bytes);
+const char* cola_kernel_name(int kernel_class);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* COLA_H */

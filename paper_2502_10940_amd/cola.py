@@ -1,0 +1,174 @@
+"""Thin ctypes binding of libcola.so (include/cola.h).
+
+Argument marshalling only: every step of the layer runs in the library's HIP
+kernels.  Tensors are passed as device pointers (``tensor.data_ptr()``), the
+stream is torch's current stream unless one is given.  There is no fallback:
+if ``libcola.so`` is missing or fails to load, every call raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG, "libcola.so")
+
+F32, BF16 = 0, 1
+ACT_IDENTITY, ACT_SILU = 0, 1
+DTYPES = {"f32": F32, "bf16": BF16}
+ACTS = {"identity": ACT_IDENTITY, "silu": ACT_SILU}
+
+OK, ERR_INVALID_ARG, ERR_BAD_SHAPE, ERR_WORKSPACE, ERR_HIP, ERR_UNSUPPORTED = range(6)
+
+KERNEL_CLASSES = ("fwd_z_sigma", "fwd_y", "bwd_dz", "bwd_dx", "bwd_da", "bwd_db",
+                  "reduce_splits", "dense_fwd", "dense_dx", "dense_dw", "fill_zero")
+
+
+class ColaError(RuntimeError):
+    def __init__(self, status: int, text: str):
+        super().__init__(f"libcola status {status}: {text}")
+        self.status = status
+
+
+class ColaDesc(ctypes.Structure):
+    _fields_ = [("T", ctypes.c_int64), ("d_in", ctypes.c_int64), ("d_out", ctypes.c_int64),
+                ("r", ctypes.c_int64), ("ldx", ctypes.c_int64), ("ldy", ctypes.c_int64),
+                ("ldz", ctypes.c_int64), ("dtype", ctypes.c_int32), ("act", ctypes.c_int32),
+                ("recompute", ctypes.c_int32)]
+
+
+class DenseDesc(ctypes.Structure):
+    _fields_ = [("T", ctypes.c_int64), ("d_in", ctypes.c_int64), ("d_out", ctypes.c_int64),
+                ("ldx", ctypes.c_int64), ("ldy", ctypes.c_int64), ("dtype", ctypes.c_int32)]
+
+
+_lib = None
+
+_P = ctypes.c_void_p
+_SZ = ctypes.c_size_t
+
+EXPORTS = {
+    "cola_abi_version": ([], ctypes.c_int),
+    "cola_strerror": ([ctypes.c_int], ctypes.c_char_p),
+    "cola_workspace_bytes": ([ctypes.POINTER(ColaDesc), ctypes.c_int], _SZ),
+    "cola_fwd": ([ctypes.POINTER(ColaDesc), _P, _P, _P, _P, _P, _P, _P, _SZ, _P], ctypes.c_int),
+    "cola_bwd": ([ctypes.POINTER(ColaDesc), _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _SZ, _P],
+                 ctypes.c_int),
+    "dense_workspace_bytes": ([ctypes.POINTER(DenseDesc), ctypes.c_int], _SZ),
+    "dense_fwd": ([ctypes.POINTER(DenseDesc), _P, _P, _P, _P, _SZ, _P], ctypes.c_int),
+    "dense_bwd": ([ctypes.POINTER(DenseDesc), _P, _P, _P, _P, _P, _P, _SZ, _P], ctypes.c_int),
+    "cola_timing_enable": ([ctypes.c_int], ctypes.c_int),
+    "cola_timing_reset": ([], ctypes.c_int),
+    "cola_timing_read": ([ctypes.c_int, ctypes.POINTER(ctypes.c_int64), ctypes.POINTER(ctypes.c_double),
+                          ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double)], ctypes.c_int),
+    "cola_kernel_name": ([ctypes.c_int], ctypes.c_char_p),
+}
+
+
+def lib():
+    """Load libcola.so (built by ``paper_2502_10940_amd.build``); raises if absent."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with "
+                               "`python -m paper_2502_10940_amd.build` (no fallback exists)")
+        L = ctypes.CDLL(LIB_PATH)
+        for name, (args, res) in EXPORTS.items():
+            fn = getattr(L, name)
+            fn.argtypes = args
+            fn.restype = res
+        _lib = L
+    return _lib
+
+
+def _check(status: int):
+    if status != OK:
+        raise ColaError(status, lib().cola_strerror(status).decode())
+
+
+def _ptr(x):
+    if x is None:
+        return None
+    if isinstance(x, int):
+        return x
+    return x.data_ptr()
+
+
+def _stream(stream):
+    if stream is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+def desc(T, d_in, d_out, r, dtype="bf16", act="silu", recompute=False, ldx=0, ldy=0, ldz=0):
+    return ColaDesc(T, d_in, d_out, r, ldx, ldy, ldz,
+                    DTYPES[dtype] if isinstance(dtype, str) else int(dtype),
+                    ACTS[act] if isinstance(act, str) else int(act), int(bool(recompute)))
+
+
+def dense_desc(T, d_in, d_out, dtype="bf16", ldx=0, ldy=0):
+    return DenseDesc(T, d_in, d_out, ldx, ldy, DTYPES[dtype] if isinstance(dtype, str) else int(dtype))
+
+
+def workspace_bytes(d: ColaDesc, phase: int) -> int:
+    return int(lib().cola_workspace_bytes(ctypes.byref(d), phase))
+
+
+def dense_workspace_bytes(d: DenseDesc, phase: int) -> int:
+    return int(lib().dense_workspace_bytes(ctypes.byref(d), phase))
+
+
+def fwd(d: ColaDesc, X, A, B, Y, Z, H, ws=None, ws_bytes=None, stream=None):
+    """Z = X A^T, H = sigma(Z), Y = H B^T (H is None in CoLA-M mode)."""
+    if ws_bytes is None:
+        ws_bytes = ws.numel() * ws.element_size() if ws is not None else 0
+    _check(lib().cola_fwd(ctypes.byref(d), _ptr(X), _ptr(A), _ptr(B), _ptr(Y), _ptr(Z), _ptr(H),
+                          _ptr(ws), ws_bytes, _stream(stream)))
+
+
+def bwd(d: ColaDesc, dY, X, Z, H, A, B, dX, dA, dB, ws=None, ws_bytes=None, stream=None):
+    """dZ = (dY B) * sigma'(Z), dX = dZ A, dA = dZ^T X, dB = dY^T H (H None in CoLA-M)."""
+    if ws_bytes is None:
+        ws_bytes = ws.numel() * ws.element_size() if ws is not None else 0
+    _check(lib().cola_bwd(ctypes.byref(d), _ptr(dY), _ptr(X), _ptr(Z), _ptr(H), _ptr(A), _ptr(B),
+                          _ptr(dX), _ptr(dA), _ptr(dB), _ptr(ws), ws_bytes, _stream(stream)))
+
+
+def dense_fwd(d: DenseDesc, X, W, Y, ws=None, ws_bytes=None, stream=None):
+    if ws_bytes is None:
+        ws_bytes = ws.numel() * ws.element_size() if ws is not None else 0
+    _check(lib().dense_fwd(ctypes.byref(d), _ptr(X), _ptr(W), _ptr(Y), _ptr(ws), ws_bytes,
+                           _stream(stream)))
+
+
+def dense_bwd(d: DenseDesc, dY, X, W, dX, dW, ws=None, ws_bytes=None, stream=None):
+    if ws_bytes is None:
+        ws_bytes = ws.numel() * ws.element_size() if ws is not None else 0
+    _check(lib().dense_bwd(ctypes.byref(d), _ptr(dY), _ptr(X), _ptr(W), _ptr(dX), _ptr(dW),
+                           _ptr(ws), ws_bytes, _stream(stream)))
+
+
+def timing_enable(on: bool = True):
+    _check(lib().cola_timing_enable(int(on)))
+
+
+def timing_reset():
+    _check(lib().cola_timing_reset())
+
+
+def timing_read(kernel_class: int):
+    """(launches, ms, flops, bytes) summed since the last reset."""
+    n = ctypes.c_int64()
+    ms = ctypes.c_double()
+    fl = ctypes.c_double()
+    by = ctypes.c_double()
+    _check(lib().cola_timing_read(kernel_class, ctypes.byref(n), ctypes.byref(ms), ctypes.byref(fl),
+                                  ctypes.byref(by)))
+    return n.value, ms.value, fl.value, by.value
+
+
+def kernel_name(kernel_class: int) -> str:
+    return lib().cola_kernel_name(kernel_class).decode()

@@ -1,0 +1,501 @@
+// cola_abi.hip -- the C ABI of libcola.so (include/cola.h): argument
+// validation, workspace planning, the launch sequence of each call, and the
+// optional per-kernel event timing.
+//
+// Launch sequences (one stream, no host synchronisation):
+//   cola_fwd : K1  Z = X A^T, H = sigma(Z)          (epilogue writes Z and H)
+//              K2  Y = H B^T
+//   cola_bwd : K3  dZ = (dY B) (.) sigma'(Z)        (CoLA-M: also H = sigma(Z))
+//              K4  dX = dZ A
+//              K5  dA partials = dZ^T X             (split over tokens)
+//              K6  dB partials = dY^T H             (split over tokens)
+//              K7  dA, dB = fixed-order sums of the partials
+//   dense    : Y = X W^T ; dX = dY W ; dW = dY^T X (split over tokens + K7)
+#include <mutex>
+#include <new>
+#include <stdio.h>
+#include <string.h>
+#include <vector>
+
+#include "../../include/cola.h"
+#include "internal.hpp"
+
+using namespace cola;
+
+namespace {
+
+thread_local char g_err[256] = "";
+
+int hip_fail(hipError_t e, const char* where) {
+    snprintf(g_err, sizeof(g_err), "%s: %s", where, hipGetErrorString(e));
+    return COLA_ERR_HIP;
+}
+
+// ---------------------------------------------------------------------------
+// timing
+// ---------------------------------------------------------------------------
+struct Timed {
+    hipEvent_t start, stop;
+    int kc;
+    double flops, bytes;
+};
+
+struct TimingState {
+    std::mutex mu;
+    bool on = false;
+    std::vector<Timed> pending;
+    std::vector<hipEvent_t> free_events;
+    int64_t launches[COLA_KC_COUNT] = {};
+    double ms[COLA_KC_COUNT] = {};
+    double flops[COLA_KC_COUNT] = {};
+    double bytes[COLA_KC_COUNT] = {};
+};
+
+TimingState& timing() {
+    static TimingState* t = new TimingState();   // never destroyed: events may outlive static dtors
+    return *t;
+}
+
+hipError_t get_event(TimingState& t, hipEvent_t* e) {
+    if (!t.free_events.empty()) {
+        *e = t.free_events.back();
+        t.free_events.pop_back();
+        return hipSuccess;
+    }
+    return hipEventCreate(e);
+}
+
+// Drain recorded events into the totals (waits for them).
+hipError_t drain(TimingState& t) {
+    for (const Timed& x : t.pending) {
+        hipError_t e = hipEventSynchronize(x.stop);
+        if (e != hipSuccess) return e;
+        float ms = 0.f;
+        e = hipEventElapsedTime(&ms, x.start, x.stop);
+        if (e != hipSuccess) return e;
+        t.launches[x.kc] += 1;
+        t.ms[x.kc] += ms;
+        t.flops[x.kc] += x.flops;
+        t.bytes[x.kc] += x.bytes;
+        t.free_events.push_back(x.start);
+        t.free_events.push_back(x.stop);
+    }
+    t.pending.clear();
+    return hipSuccess;
+}
+
+// Run one launch, bracketed by events when timing is on.
+template <class F>
+hipError_t timed(int kc, double flops, double bytes, hipStream_t s, F&& launch) {
+    TimingState& t = timing();
+    if (!t.on) return launch();
+    std::lock_guard<std::mutex> lock(t.mu);
+    if (t.pending.size() >= 8192) {
+        hipError_t e = drain(t);
+        if (e != hipSuccess) return e;
+    }
+    Timed x{};
+    x.kc = kc; x.flops = flops; x.bytes = bytes;
+    hipError_t e = get_event(t, &x.start);
+    if (e == hipSuccess) e = get_event(t, &x.stop);
+    if (e == hipSuccess) e = hipEventRecord(x.start, s);
+    if (e != hipSuccess) return e;
+    e = launch();
+    if (e != hipSuccess) return e;
+    e = hipEventRecord(x.stop, s);
+    if (e != hipSuccess) return e;
+    t.pending.push_back(x);
+    return hipSuccess;
+}
+
+// ---------------------------------------------------------------------------
+// shapes and plans
+// ---------------------------------------------------------------------------
+constexpr int64_t kMaxDim = int64_t(1) << 40;   // keeps every byte count far from overflow
+
+struct Dims {
+    int64_t T, d_in, d_out, r, ldx, ldy, ldz;
+    bool bf16;
+    size_t esize;
+};
+
+int check_desc(const cola_desc* d, Dims* out) {
+    if (!d) return COLA_ERR_INVALID_ARG;
+    if (d->dtype != COLA_F32 && d->dtype != COLA_BF16) return COLA_ERR_INVALID_ARG;
+    if (d->act != COLA_ACT_IDENTITY && d->act != COLA_ACT_SILU) return COLA_ERR_INVALID_ARG;
+    if (d->recompute != 0 && d->recompute != 1) return COLA_ERR_INVALID_ARG;
+    if (d->T < 0 || d->d_in < 1 || d->d_out < 1 || d->r < 1) return COLA_ERR_BAD_SHAPE;
+    if (d->T > kMaxDim || d->d_in > kMaxDim || d->d_out > kMaxDim || d->r > kMaxDim)
+        return COLA_ERR_BAD_SHAPE;
+    Dims x;
+    x.T = d->T; x.d_in = d->d_in; x.d_out = d->d_out; x.r = d->r;
+    x.ldx = d->ldx ? d->ldx : d->d_in;
+    x.ldy = d->ldy ? d->ldy : d->d_out;
+    x.ldz = d->ldz ? d->ldz : d->r;
+    if (x.ldx < x.d_in || x.ldy < x.d_out || x.ldz < x.r) return COLA_ERR_BAD_SHAPE;
+    if (x.ldx > kMaxDim || x.ldy > kMaxDim || x.ldz > kMaxDim) return COLA_ERR_BAD_SHAPE;
+    // element counts of the largest operands must stay below 2^62
+    const double big = (double)x.T * (double)(x.ldx > x.ldy ? x.ldx : x.ldy);
+    if (big > 4.0e18 || (double)x.r * (double)(x.d_in > x.d_out ? x.d_in : x.d_out) > 4.0e18)
+        return COLA_ERR_BAD_SHAPE;
+    x.bf16 = d->dtype == COLA_BF16;
+    x.esize = x.bf16 ? 2 : 4;
+    *out = x;
+    return COLA_OK;
+}
+
+size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+// Split of a token-long (K = T) weight-gradient GEMM: enough workgroups to
+// cover the chip twice, each split at least four K tiles long.  Depends only
+// on the shape, so results are reproducible run to run.
+struct Split {
+    int splits;
+    int64_t k_chunk;
+};
+
+Split plan_split(bool bf16, int64_t M, int64_t N, int64_t K) {
+    const int64_t bk = bf16 ? BF16_BK : F32_BK;
+    const int64_t tiles = gemm_tiles(bf16, M, N);
+    const int64_t target = 512;
+    int64_t want = (target + tiles - 1) / tiles;
+    const int64_t ktiles = (K + bk - 1) / bk;
+    int64_t maxs = ktiles / 4;
+    if (maxs < 1) maxs = 1;
+    if (want > maxs) want = maxs;
+    if (want > 64) want = 64;
+    if (want < 1) want = 1;
+    int64_t chunk_tiles = (ktiles + want - 1) / want;
+    if (chunk_tiles < 1) chunk_tiles = 1;
+    Split s;
+    s.k_chunk = chunk_tiles * bk;
+    s.splits = (int)((K + s.k_chunk - 1) / s.k_chunk);
+    if (s.splits < 1) s.splits = 1;
+    return s;
+}
+
+struct BwdPlan {
+    int64_t ldw;          // pitch of dZ (and recomputed H) in the workspace
+    size_t off_dz, off_h, off_pa, off_pb, total;
+    Split sa, sb;
+};
+
+BwdPlan plan_bwd(const Dims& x, bool recompute) {
+    BwdPlan p;
+    p.ldw = x.bf16 ? (x.r + 7) / 8 * 8 : (x.r + 3) / 4 * 4;
+    const size_t zbytes = align256((size_t)x.T * (size_t)p.ldw * x.esize);
+    p.sa = plan_split(x.bf16, x.r, x.d_in, x.T);
+    p.sb = plan_split(x.bf16, x.d_out, x.r, x.T);
+    p.off_dz = 0;
+    p.off_h = zbytes;
+    p.off_pa = p.off_h + (recompute ? zbytes : 0);
+    const size_t pa = p.sa.splits > 1 ? align256((size_t)p.sa.splits * (size_t)(x.r * x.d_in) * 4) : 0;
+    p.off_pb = p.off_pa + pa;
+    const size_t pb = p.sb.splits > 1 ? align256((size_t)p.sb.splits * (size_t)(x.d_out * x.r) * 4) : 0;
+    p.total = p.off_pb + pb;
+    if (x.T == 0) p.total = 0;
+    return p;
+}
+
+size_t fwd_ws(const Dims& x, bool recompute) {
+    if (!recompute || x.T == 0) return 0;
+    const int64_t ldw = x.bf16 ? (x.r + 7) / 8 * 8 : (x.r + 3) / 4 * 4;
+    return align256((size_t)x.T * (size_t)ldw * x.esize);
+}
+
+hipError_t gemm(const GemmArgs& a, bool bf16, hipStream_t s) {
+    return bf16 ? launch_gemm_bf16(a, s) : launch_gemm_f32(a, s);
+}
+
+GemmArgs make_args(int64_t M, int64_t N, int64_t K, const void* p, int64_t ldp, int pl,
+                   const void* q, int64_t ldq, int ql, void* c, int64_t ldc, int epi, int act) {
+    GemmArgs a{};
+    a.M = M; a.N = N; a.K = K;
+    a.p = p; a.ldp = ldp; a.p_layout = pl;
+    a.q = q; a.ldq = ldq; a.q_layout = ql;
+    a.c = c; a.ldc = ldc;
+    a.epi = epi; a.act = act;
+    a.splits = 1;
+    a.k_chunk = K > 0 ? K : 1;
+    a.split_stride = 0;
+    return a;
+}
+
+double gemm_flops(int64_t M, int64_t N, int64_t K) { return 2.0 * (double)M * (double)N * (double)K; }
+
+// Weight gradient C[M][N] = sum_t P[t][m] Q[t][n] with K = T split into
+// chunks whose partials are summed in a fixed order.
+int wgrad(bool bf16, int64_t M, int64_t N, int64_t T, const void* P, int64_t ldp, const void* Q,
+          int64_t ldq, float* C, const Split& sp, float* partials, int kc, double bytes_in,
+          hipStream_t s) {
+    GemmArgs a = make_args(M, N, T, P, ldp, MNMAJ, Q, ldq, MNMAJ, C, N, EPI_STORE_F32, 0);
+    a.splits = sp.splits;
+    a.k_chunk = sp.k_chunk;
+    if (sp.splits > 1) {
+        a.c = partials;
+        a.split_stride = M * N;
+    }
+    const double out_bytes = (double)M * (double)N * 4.0 * (sp.splits > 1 ? sp.splits : 1);
+    hipError_t e = timed(kc, gemm_flops(M, N, T), bytes_in + out_bytes, s, [&] { return gemm(a, bf16, s); });
+    if (e != hipSuccess) return hip_fail(e, cola_kernel_name(kc));
+    if (sp.splits > 1) {
+        const double rb = (double)M * (double)N * 4.0 * (sp.splits + 1);
+        e = timed(COLA_KC_REDUCE, 0.0, rb, s,
+                  [&] { return launch_reduce_splits(partials, sp.splits, M * N, C, M * N, s); });
+        if (e != hipSuccess) return hip_fail(e, "reduce");
+    }
+    return COLA_OK;
+}
+
+template <class F>
+int guarded(F&& f) {
+    try {
+        return f();
+    } catch (const std::bad_alloc&) {
+        snprintf(g_err, sizeof(g_err), "host allocation failed");
+        return COLA_ERR_HIP;
+    } catch (...) {
+        snprintf(g_err, sizeof(g_err), "unexpected host exception");
+        return COLA_ERR_HIP;
+    }
+}
+
+}  // namespace
+
+extern "C" {
+
+int cola_abi_version(void) { return COLA_ABI_VERSION; }
+
+const char* cola_strerror(int status) {
+    switch (status) {
+        case COLA_OK: return "success";
+        case COLA_ERR_INVALID_ARG: return "invalid argument (NULL pointer, bad enum, or H/recompute mismatch)";
+        case COLA_ERR_BAD_SHAPE: return "bad shape (dimension < 1, T < 0, ld < width, or size overflow)";
+        case COLA_ERR_WORKSPACE: return "workspace too small";
+        case COLA_ERR_HIP: return g_err[0] ? g_err : "HIP error";
+        case COLA_ERR_UNSUPPORTED: return "unsupported combination";
+        default: return "unknown status";
+    }
+}
+
+const char* cola_kernel_name(int kc) {
+    static const char* names[COLA_KC_COUNT] = {
+        "fwd_z_sigma", "fwd_y", "bwd_dz", "bwd_dx", "bwd_da", "bwd_db",
+        "reduce_splits", "dense_fwd", "dense_dx", "dense_dw", "fill_zero"};
+    if (kc < 0 || kc >= COLA_KC_COUNT) return "invalid";
+    return names[kc];
+}
+
+size_t cola_workspace_bytes(const cola_desc* desc, int phase) {
+    Dims x;
+    if (check_desc(desc, &x) != COLA_OK) return 0;
+    if (phase == 0) return fwd_ws(x, desc->recompute == 1);
+    if (phase == 1) return plan_bwd(x, desc->recompute == 1).total;
+    return 0;
+}
+
+int cola_fwd(const cola_desc* desc, const void* X, const void* A, const void* B, void* Y, void* Z,
+             void* H, void* ws, size_t ws_bytes, cola_stream_t stream) {
+    return guarded([&]() -> int {
+        Dims x;
+        int st = check_desc(desc, &x);
+        if (st != COLA_OK) return st;
+        const bool recompute = desc->recompute == 1;
+        if (recompute ? (H != nullptr) : (H == nullptr)) return COLA_ERR_INVALID_ARG;
+        if (x.T == 0) return COLA_OK;
+        if (!X || !A || !B || !Y || !Z) return COLA_ERR_INVALID_ARG;
+        const size_t need = fwd_ws(x, recompute);
+        if (need > 0 && (!ws || ws_bytes < need)) return COLA_ERR_WORKSPACE;
+        hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+
+        void* Hbuf = recompute ? ws : H;
+        const int64_t ldh = recompute ? (x.bf16 ? (x.r + 7) / 8 * 8 : (x.r + 3) / 4 * 4) : x.ldz;
+        const double es = (double)x.esize;
+
+        // K1: Z = X A^T, H = sigma(Z)
+        GemmArgs k1 = make_args(x.T, x.r, x.d_in, X, x.ldx, KMAJ, A, x.d_in, KMAJ, Z, x.ldz, EPI_Z_H,
+                                desc->act);
+        k1.aux = Hbuf;
+        k1.ldaux = ldh;
+        const double b1 = es * ((double)x.T * x.d_in + (double)x.r * x.d_in + 2.0 * x.T * x.r);
+        hipError_t e = timed(COLA_KC_FWD_Z, gemm_flops(x.T, x.r, x.d_in), b1, s,
+                             [&] { return gemm(k1, x.bf16, s); });
+        if (e != hipSuccess) return hip_fail(e, "fwd_z_sigma");
+
+        // K2: Y = H B^T
+        GemmArgs k2 = make_args(x.T, x.d_out, x.r, Hbuf, ldh, KMAJ, B, x.r, KMAJ, Y, x.ldy, EPI_STORE,
+                                desc->act);
+        const double b2 = es * ((double)x.T * x.r + (double)x.d_out * x.r + (double)x.T * x.d_out);
+        e = timed(COLA_KC_FWD_Y, gemm_flops(x.T, x.d_out, x.r), b2, s, [&] { return gemm(k2, x.bf16, s); });
+        if (e != hipSuccess) return hip_fail(e, "fwd_y");
+        return COLA_OK;
+    });
+}
+
+int cola_bwd(const cola_desc* desc, const void* dY, const void* X, const void* Z, const void* H,
+             const void* A, const void* B, void* dX, float* dA, float* dB, void* ws, size_t ws_bytes,
+             cola_stream_t stream) {
+    return guarded([&]() -> int {
+        Dims x;
+        int st = check_desc(desc, &x);
+        if (st != COLA_OK) return st;
+        const bool recompute = desc->recompute == 1;
+        if (recompute ? (H != nullptr) : (H == nullptr && x.T > 0)) return COLA_ERR_INVALID_ARG;
+        if (!dA || !dB) return COLA_ERR_INVALID_ARG;
+        hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+        if (x.T == 0) {
+            // empty batch: the token sums are empty, dA = dB = 0
+            hipError_t e = timed(COLA_KC_FILL, 0.0, 4.0 * x.r * x.d_in, s,
+                                 [&] { return launch_fill_zero(dA, x.r * x.d_in, s); });
+            if (e == hipSuccess)
+                e = timed(COLA_KC_FILL, 0.0, 4.0 * x.d_out * x.r, s,
+                          [&] { return launch_fill_zero(dB, x.d_out * x.r, s); });
+            return e == hipSuccess ? COLA_OK : hip_fail(e, "fill_zero");
+        }
+        if (!dY || !X || !Z || !A || !B || !dX) return COLA_ERR_INVALID_ARG;
+        const BwdPlan p = plan_bwd(x, recompute);
+        if (!ws || ws_bytes < p.total) return COLA_ERR_WORKSPACE;
+
+        char* w = reinterpret_cast<char*>(ws);
+        void* dZ = w + p.off_dz;
+        const void* Hbuf = recompute ? (const void*)(w + p.off_h) : H;
+        const int64_t ldh = recompute ? p.ldw : x.ldz;
+        const double es = (double)x.esize;
+
+        // K3: dZ = (dY B) (.) sigma'(Z); CoLA-M regenerates H = sigma(Z) here
+        GemmArgs k3 = make_args(x.T, x.r, x.d_out, dY, x.ldy, KMAJ, B, x.r, MNMAJ, dZ, p.ldw, EPI_DZ,
+                                desc->act);
+        k3.zin = Z;
+        k3.ldzin = x.ldz;
+        k3.aux = recompute ? (void*)(w + p.off_h) : nullptr;
+        k3.ldaux = p.ldw;
+        const double b3 = es * ((double)x.T * x.d_out + (double)x.d_out * x.r +
+                                (double)x.T * x.r * (recompute ? 3.0 : 2.0));
+        hipError_t e = timed(COLA_KC_BWD_DZ, gemm_flops(x.T, x.r, x.d_out), b3, s,
+                             [&] { return gemm(k3, x.bf16, s); });
+        if (e != hipSuccess) return hip_fail(e, "bwd_dz");
+
+        // K4: dX = dZ A
+        GemmArgs k4 = make_args(x.T, x.d_in, x.r, dZ, p.ldw, KMAJ, A, x.d_in, MNMAJ, dX, x.ldx, EPI_STORE,
+                                desc->act);
+        const double b4 = es * ((double)x.T * x.r + (double)x.r * x.d_in + (double)x.T * x.d_in);
+        e = timed(COLA_KC_BWD_DX, gemm_flops(x.T, x.d_in, x.r), b4, s, [&] { return gemm(k4, x.bf16, s); });
+        if (e != hipSuccess) return hip_fail(e, "bwd_dx");
+
+        // K5: dA = dZ^T X ; K6: dB = dY^T H  (+ K7 fixed-order reductions)
+        st = wgrad(x.bf16, x.r, x.d_in, x.T, dZ, p.ldw, X, x.ldx, dA, p.sa,
+                   reinterpret_cast<float*>(w + p.off_pa), COLA_KC_BWD_DA,
+                   es * ((double)x.T * x.r + (double)x.T * x.d_in), s);
+        if (st != COLA_OK) return st;
+        st = wgrad(x.bf16, x.d_out, x.r, x.T, dY, x.ldy, Hbuf, ldh, dB, p.sb,
+                   reinterpret_cast<float*>(w + p.off_pb), COLA_KC_BWD_DB,
+                   es * ((double)x.T * x.d_out + (double)x.T * x.r), s);
+        return st;
+    });
+}
+
+// ---------------------------------------------------------------------------
+// dense baseline
+// ---------------------------------------------------------------------------
+static int check_dense(const dense_desc* d, Dims* out) {
+    if (!d) return COLA_ERR_INVALID_ARG;
+    cola_desc c{};
+    c.T = d->T; c.d_in = d->d_in; c.d_out = d->d_out; c.r = 1;
+    c.ldx = d->ldx; c.ldy = d->ldy; c.ldz = 0;
+    c.dtype = d->dtype; c.act = COLA_ACT_IDENTITY; c.recompute = 0;
+    return check_desc(&c, out);
+}
+
+size_t dense_workspace_bytes(const dense_desc* desc, int phase) {
+    Dims x;
+    if (check_dense(desc, &x) != COLA_OK) return 0;
+    if (phase != 1 || x.T == 0) return 0;
+    const Split sp = plan_split(x.bf16, x.d_out, x.d_in, x.T);
+    return sp.splits > 1 ? align256((size_t)sp.splits * (size_t)(x.d_out * x.d_in) * 4) : 0;
+}
+
+int dense_fwd(const dense_desc* desc, const void* X, const void* W, void* Y, void* ws, size_t ws_bytes,
+              cola_stream_t stream) {
+    (void)ws; (void)ws_bytes;
+    return guarded([&]() -> int {
+        Dims x;
+        int st = check_dense(desc, &x);
+        if (st != COLA_OK) return st;
+        if (x.T == 0) return COLA_OK;
+        if (!X || !W || !Y) return COLA_ERR_INVALID_ARG;
+        hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+        GemmArgs a = make_args(x.T, x.d_out, x.d_in, X, x.ldx, KMAJ, W, x.d_in, KMAJ, Y, x.ldy, EPI_STORE, 0);
+        const double b = (double)x.esize * ((double)x.T * x.d_in + (double)x.d_out * x.d_in + (double)x.T * x.d_out);
+        hipError_t e = timed(COLA_KC_DENSE_FWD, gemm_flops(x.T, x.d_out, x.d_in), b, s,
+                             [&] { return gemm(a, x.bf16, s); });
+        return e == hipSuccess ? COLA_OK : hip_fail(e, "dense_fwd");
+    });
+}
+
+int dense_bwd(const dense_desc* desc, const void* dY, const void* X, const void* W, void* dX, float* dW,
+              void* ws, size_t ws_bytes, cola_stream_t stream) {
+    return guarded([&]() -> int {
+        Dims x;
+        int st = check_dense(desc, &x);
+        if (st != COLA_OK) return st;
+        if (!dW) return COLA_ERR_INVALID_ARG;
+        hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+        if (x.T == 0) {
+            hipError_t e = timed(COLA_KC_FILL, 0.0, 4.0 * x.d_out * x.d_in, s,
+                                 [&] { return launch_fill_zero(dW, x.d_out * x.d_in, s); });
+            return e == hipSuccess ? COLA_OK : hip_fail(e, "fill_zero");
+        }
+        if (!dY || !X || !W || !dX) return COLA_ERR_INVALID_ARG;
+        const Split sp = plan_split(x.bf16, x.d_out, x.d_in, x.T);
+        const size_t need = dense_workspace_bytes(desc, 1);
+        if (need > 0 && (!ws || ws_bytes < need)) return COLA_ERR_WORKSPACE;
+        GemmArgs a = make_args(x.T, x.d_in, x.d_out, dY, x.ldy, KMAJ, W, x.d_in, MNMAJ, dX, x.ldx, EPI_STORE, 0);
+        const double b = (double)x.esize * ((double)x.T * x.d_out + (double)x.d_out * x.d_in + (double)x.T * x.d_in);
+        hipError_t e = timed(COLA_KC_DENSE_DX, gemm_flops(x.T, x.d_in, x.d_out), b, s,
+                             [&] { return gemm(a, x.bf16, s); });
+        if (e != hipSuccess) return hip_fail(e, "dense_dx");
+        return wgrad(x.bf16, x.d_out, x.d_in, x.T, dY, x.ldy, X, x.ldx, dW, sp, reinterpret_cast<float*>(ws),
+                     COLA_KC_DENSE_DW, (double)x.esize * ((double)x.T * x.d_out + (double)x.T * x.d_in), s);
+    });
+}
+
+// ---------------------------------------------------------------------------
+// timing API
+// ---------------------------------------------------------------------------
+int cola_timing_enable(int on) {
+    return guarded([&]() -> int {
+        TimingState& t = timing();
+        std::lock_guard<std::mutex> lock(t.mu);
+        t.on = on != 0;
+        return COLA_OK;
+    });
+}
+
+int cola_timing_reset(void) {
+    return guarded([&]() -> int {
+        TimingState& t = timing();
+        std::lock_guard<std::mutex> lock(t.mu);
+        hipError_t e = drain(t);
+        for (int k = 0; k < COLA_KC_COUNT; ++k) {
+            t.launches[k] = 0; t.ms[k] = 0; t.flops[k] = 0; t.bytes[k] = 0;
+        }
+        return e == hipSuccess ? COLA_OK : hip_fail(e, "timing_reset");
+    });
+}
+
+int cola_timing_read(int kc, int64_t* launches, double* ms, double* flops, double* bytes) {
+    if (kc < 0 || kc >= COLA_KC_COUNT || !launches || !ms || !flops || !bytes) return COLA_ERR_INVALID_ARG;
+    return guarded([&]() -> int {
+        TimingState& t = timing();
+        std::lock_guard<std::mutex> lock(t.mu);
+        hipError_t e = drain(t);
+        if (e != hipSuccess) return hip_fail(e, "timing_read");
+        *launches = t.launches[kc];
+        *ms = t.ms[kc];
+        *flops = t.flops[kc];
+        *bytes = t.bytes[kc];
+        return COLA_OK;
+    });
+}
+
+}  // extern "C"

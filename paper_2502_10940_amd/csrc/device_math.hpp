@@ -1,0 +1,53 @@
+// device_math.hpp -- pointwise helpers for the gfx950 kernels: bf16 rounding
+// and the CoLA nonlinearity sigma with its derivative.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace cola {
+
+// bf16 bits -> float (exact).
+__device__ __forceinline__ float bf16_to_f32(uint32_t bits16) {
+    return __uint_as_float(bits16 << 16);
+}
+
+// float -> bf16 bits, round to nearest, ties to even; NaN stays a quiet NaN.
+__device__ __forceinline__ uint32_t f32_to_bf16(float f) {
+    uint32_t u = __float_as_uint(f);
+    if ((u & 0x7fffffffu) > 0x7f800000u) return ((u >> 16) | 0x40u) & 0xffffu;
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return u >> 16;
+}
+
+// Two floats -> packed bf16 pair (lo in bits 15:0).
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+    return f32_to_bf16(lo) | (f32_to_bf16(hi) << 16);
+}
+
+// logistic sigmoid s(z) = 1 / (1 + e^{-z}); e^{-z} = inf for very negative z
+// gives s = 0 exactly, never NaN.
+__device__ __forceinline__ float logistic_fast(float z) {
+    return 1.0f / (1.0f + __expf(-z));
+}
+__device__ __forceinline__ float logistic_exact(float z) {
+    return 1.0f / (1.0f + expf(-z));
+}
+
+// sigma(z) and sigma'(z) for act 0 (identity) and 1 (SiLU = z s(z),
+// SiLU' = s (1 + z (1 - s))).  FAST selects the hardware exp (bf16 path).
+template <bool FAST>
+__device__ __forceinline__ float act_sigma(int act, float z) {
+    if (act == 0) return z;
+    float s = FAST ? logistic_fast(z) : logistic_exact(z);
+    return z * s;
+}
+
+template <bool FAST>
+__device__ __forceinline__ float act_sigma_prime(int act, float z) {
+    if (act == 0) return 1.0f;
+    float s = FAST ? logistic_fast(z) : logistic_exact(z);
+    return s * (1.0f + z * (1.0f - s));
+}
+
+}  // namespace cola

@@ -1,0 +1,439 @@
+// gemm_bf16.hip -- the bf16 MFMA GEMM behind every CoLA and dense step on
+// gfx950:  C[M][N] = sum_k P(m, k) Q(n, k), fp32 accumulation, with a fused
+// epilogue (plain store, Z/H with sigma, dZ with sigma', fp32 partials).
+//
+// Design (CDNA4, wave64):
+//  * 256 threads = 4 waves in a 2 x 2 grid; each wave owns a (BM/2) x (BN/2)
+//    block of C, computed with v_mfma_f32_32x32x16_bf16 tiles (acc in fp32).
+//  * K advances in tiles of 64.  Both operand tiles live in LDS as [row][k]
+//    with 128-byte rows; the eight 16-byte chunks of a row are XOR-swizzled
+//    by (row ^ row >> 3) & 7, so the MFMA fragment reads (16 B per lane) and
+//    the tile writes are free of bank conflicts.
+//  * Operands with contiguous k (KMAJ) are copied global -> registers -> LDS
+//    unchanged.  Operands with k strided (MNMAJ: the weight-gradient GEMMs,
+//    whose reduction runs over tokens, and products with the small weight
+//    matrices) are loaded as 16-byte runs along m and transposed in registers
+//    (8 x 8 blocks of bf16, pure permutes) on their way into LDS, so the MFMA
+//    core only ever sees k-contiguous fragments.
+//  * Double-buffered LDS: the next tile's global loads are issued before the
+//    current tile's MFMAs, with one barrier per K tile.
+//  * Workgroups are renumbered so that each XCD (blockIdx % 8 on MI355X)
+//    receives a contiguous run of output tiles: tiles sharing an operand row
+//    block share that XCD's L2.
+//  * The epilogue stages each wave's accumulators through LDS so that every
+//    global access is a coalesced 16-byte vector (ragged edges and unaligned
+//    pitches fall back to guarded per-element accesses).
+#include "internal.hpp"
+#include "device_math.hpp"
+
+namespace cola {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+constexpr int BK = BF16_BK;   // 64
+constexpr int NT = 256;
+
+__device__ __forceinline__ int swz(int row) { return (row ^ (row >> 3)) & 7; }
+__device__ __forceinline__ int lds_off(int row, int chunk) {
+    return row * 128 + ((chunk ^ swz(row)) << 4);
+}
+
+__device__ __forceinline__ bool aligned16(const void* p, int64_t ld) {
+    return ((reinterpret_cast<uintptr_t>(p) & 15u) == 0) && ((ld & 7) == 0);
+}
+
+// ---------------------------------------------------------------------------
+// operand tile loaders: global -> registers -> LDS tile [R rows][64 k]
+// ---------------------------------------------------------------------------
+template <int R, int LAYOUT>
+struct Loader;
+
+// k contiguous: thread t moves chunks (row t/8 + 32 i, chunk t%8).
+template <int R>
+struct Loader<R, KMAJ> {
+    static constexpr int NV = R / 32;
+    uint4 v[NV];
+
+    __device__ __forceinline__ void load(const uint16_t* base, int64_t ld, int64_t row0,
+                                         int64_t rows, int64_t k0, int64_t kend, bool fast) {
+        const int t = threadIdx.x;
+        const int c = t & 7;
+        const int r = t >> 3;
+        if (fast) {
+            const uint16_t* p = base + (row0 + r) * ld + k0 + c * 8;
+#pragma unroll
+            for (int i = 0; i < NV; ++i)
+                v[i] = *reinterpret_cast<const uint4*>(p + (int64_t)(32 * i) * ld);
+        } else {
+#pragma unroll
+            for (int i = 0; i < NV; ++i) {
+                const int64_t row = row0 + r + 32 * i;
+                const int64_t k = k0 + c * 8;
+                uint32_t w[4];
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    uint32_t lo = 0, hi = 0;
+                    if (row < rows && k + 2 * e < kend) lo = base[row * ld + k + 2 * e];
+                    if (row < rows && k + 2 * e + 1 < kend) hi = base[row * ld + k + 2 * e + 1];
+                    w[e] = lo | (hi << 16);
+                }
+                v[i] = make_uint4(w[0], w[1], w[2], w[3]);
+            }
+        }
+    }
+
+    __device__ __forceinline__ void store(char* lds) const {
+        const int t = threadIdx.x;
+        const int c = t & 7;
+        const int r = t >> 3;
+#pragma unroll
+        for (int i = 0; i < NV; ++i)
+            *reinterpret_cast<uint4*>(lds + lds_off(r + 32 * i, c)) = v[i];
+    }
+};
+
+// k strided: thread covers KR consecutive k rows x 8 consecutive m (one
+// 16-byte load per k row), transposes the block in registers, and writes
+// KR k-values per m row into the [m][k] LDS tile.
+template <int R>
+struct Loader<R, MNMAJ> {
+    static constexpr int MB = R / 8;        // m blocks per tile
+    static constexpr int KB = NT / MB;      // k blocks per tile
+    static constexpr int KR = BK / KB;      // k rows per thread: 8 (R=256) or 4 (R=128)
+    static_assert(KR == 8 || KR == 4, "unsupported tile");
+    uint4 v[KR];
+
+    __device__ __forceinline__ void load(const uint16_t* base, int64_t ld, int64_t row0,
+                                         int64_t rows, int64_t k0, int64_t kend, bool fast) {
+        const int t = threadIdx.x;
+        const int mb = t % MB;
+        const int kb = t / MB;
+        const int64_t m = row0 + mb * 8;
+        const int64_t k = k0 + kb * KR;
+        if (fast) {
+            const uint16_t* p = base + k * ld + m;
+#pragma unroll
+            for (int kk = 0; kk < KR; ++kk)
+                v[kk] = *reinterpret_cast<const uint4*>(p + (int64_t)kk * ld);
+        } else {
+#pragma unroll
+            for (int kk = 0; kk < KR; ++kk) {
+                uint32_t w[4];
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    uint32_t lo = 0, hi = 0;
+                    if (k + kk < kend && m + 2 * e < rows) lo = base[(k + kk) * ld + m + 2 * e];
+                    if (k + kk < kend && m + 2 * e + 1 < rows) hi = base[(k + kk) * ld + m + 2 * e + 1];
+                    w[e] = lo | (hi << 16);
+                }
+                v[kk] = make_uint4(w[0], w[1], w[2], w[3]);
+            }
+        }
+    }
+
+    __device__ __forceinline__ void store(char* lds) const {
+        const int t = threadIdx.x;
+        const int mb = t % MB;
+        const int kb = t / MB;
+        const int kofs = kb * KR;              // first k of this thread within the tile
+        const int chunk = kofs >> 3;
+        const int inchunk = (kofs & 7) * 2;    // byte offset inside the chunk (0 or 8)
+        uint32_t src[KR][4];
+#pragma unroll
+        for (int kk = 0; kk < KR; ++kk) {
+            src[kk][0] = v[kk].x; src[kk][1] = v[kk].y; src[kk][2] = v[kk].z; src[kk][3] = v[kk].w;
+        }
+#pragma unroll
+        for (int mm = 0; mm < 8; ++mm) {
+            const int row = mb * 8 + mm;
+            uint32_t d[KR / 2];
+#pragma unroll
+            for (int pp = 0; pp < KR / 2; ++pp) {
+                const uint32_t a = src[2 * pp][mm >> 1];
+                const uint32_t b = src[2 * pp + 1][mm >> 1];
+                d[pp] = (mm & 1) ? ((a >> 16) | (b & 0xffff0000u)) : ((a & 0xffffu) | (b << 16));
+            }
+            char* dst = lds + lds_off(row, chunk) + inchunk;
+            if constexpr (KR == 8) {
+                *reinterpret_cast<uint4*>(dst) = make_uint4(d[0], d[1], d[2], d[3]);
+            } else {
+                *reinterpret_cast<uint2*>(dst) = make_uint2(d[0], d[1]);
+            }
+        }
+    }
+};
+
+// ---------------------------------------------------------------------------
+// epilogue: 8 consecutive columns of one output row
+// ---------------------------------------------------------------------------
+template <int EPI>
+__device__ __forceinline__ void epilogue8(const GemmArgs& a, int64_t gm, int64_t gn,
+                                          const float* acc, int split) {
+    if (gm >= a.M || gn >= a.N) return;
+    const bool full = gn + 8 <= a.N;
+    if constexpr (EPI == EPI_STORE_F32) {
+        float* c = reinterpret_cast<float*>(a.c) + (int64_t)split * a.split_stride + gm * a.ldc + gn;
+        const bool vec = full && ((reinterpret_cast<uintptr_t>(c) & 15u) == 0);
+        if (vec) {
+            reinterpret_cast<float4*>(c)[0] = make_float4(acc[0], acc[1], acc[2], acc[3]);
+            reinterpret_cast<float4*>(c)[1] = make_float4(acc[4], acc[5], acc[6], acc[7]);
+        } else {
+            #pragma unroll
+            for (int e = 0; e < 8; ++e)
+                if (gn + e < a.N) c[e] = acc[e];
+        }
+        return;
+    } else {
+        uint16_t* c = reinterpret_cast<uint16_t*>(a.c) + gm * a.ldc + gn;
+        float out[8];
+        float h[8];
+        if constexpr (EPI == EPI_STORE) {
+#pragma unroll
+            for (int e = 0; e < 8; ++e) out[e] = acc[e];
+        } else if constexpr (EPI == EPI_Z_H) {
+            // Z is stored rounded to bf16; H = sigma of that rounded Z
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                out[e] = bf16_to_f32(f32_to_bf16(acc[e]));
+                h[e] = act_sigma<true>(a.act, out[e]);
+            }
+        } else if constexpr (EPI == EPI_DZ) {
+            const uint16_t* zp = reinterpret_cast<const uint16_t*>(a.zin) + gm * a.ldzin + gn;
+            float z[8];
+            if (full && ((reinterpret_cast<uintptr_t>(zp) & 15u) == 0)) {
+                const uint4 zz = *reinterpret_cast<const uint4*>(zp);
+                const uint32_t w[4] = {zz.x, zz.y, zz.z, zz.w};
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    z[2 * e] = bf16_to_f32(w[e] & 0xffffu);
+                    z[2 * e + 1] = bf16_to_f32(w[e] >> 16);
+                }
+            } else {
+                #pragma unroll
+                for (int e = 0; e < 8; ++e) z[e] = (gn + e < a.N) ? bf16_to_f32(zp[e]) : 0.0f;
+            }
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                if (a.act == 0) {
+                    out[e] = acc[e];
+                    h[e] = z[e];
+                } else {
+                    const float s = logistic_fast(z[e]);
+                    out[e] = acc[e] * (s * (1.0f + z[e] * (1.0f - s)));
+                    h[e] = z[e] * s;
+                }
+            }
+        }
+        const bool vec = full && ((reinterpret_cast<uintptr_t>(c) & 15u) == 0);
+        if (vec) {
+            *reinterpret_cast<uint4*>(c) = make_uint4(pack_bf16x2(out[0], out[1]), pack_bf16x2(out[2], out[3]),
+                                                      pack_bf16x2(out[4], out[5]), pack_bf16x2(out[6], out[7]));
+        } else {
+            #pragma unroll
+            for (int e = 0; e < 8; ++e)
+                if (gn + e < a.N) c[e] = (uint16_t)f32_to_bf16(out[e]);
+        }
+        if constexpr (EPI == EPI_Z_H || EPI == EPI_DZ) {
+            if (a.aux) {
+                uint16_t* hp = reinterpret_cast<uint16_t*>(a.aux) + gm * a.ldaux + gn;
+                if (full && ((reinterpret_cast<uintptr_t>(hp) & 15u) == 0)) {
+                    *reinterpret_cast<uint4*>(hp) = make_uint4(pack_bf16x2(h[0], h[1]), pack_bf16x2(h[2], h[3]),
+                                                               pack_bf16x2(h[4], h[5]), pack_bf16x2(h[6], h[7]));
+                } else {
+                    #pragma unroll
+                    for (int e = 0; e < 8; ++e)
+                        if (gn + e < a.N) hp[e] = (uint16_t)f32_to_bf16(h[e]);
+                }
+            }
+        }
+    }
+}
+
+// One 32-row slab (MFMA row tile I) of a wave's accumulators: stage through
+// LDS as fp32 in [row][col] order, then each lane handles 8 consecutive
+// columns of a row, so global accesses are 16-byte vectors.
+template <int I, int BM, int BN, int EPI, int TM, int TN>
+__device__ __forceinline__ void epi_slab(const GemmArgs& a, const f32x16 (&acc)[TM][TN], float* stg,
+                                         int64_t m0, int64_t n0, int wm, int wn, int lane, int split) {
+    constexpr int WC = BN / 2;            // wave columns
+    constexpr int SP = WC + 4;            // staging pitch (floats)
+    constexpr int LPR = WC / 8;           // lanes per row in the read-back
+    constexpr int RPP = 64 / LPR;         // rows per pass
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+            const int row = 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
+            const int col = 32 * j + (lane & 31);
+            stg[row * SP + col] = acc[I][j][v];
+        }
+    __syncthreads();
+    const int cc = lane % LPR;
+    const int rr = lane / LPR;
+#pragma unroll
+    for (int pass = 0; pass < 32 / RPP; ++pass) {
+        const int lr = pass * RPP + rr;
+        const float4 x0 = *reinterpret_cast<const float4*>(stg + lr * SP + cc * 8);
+        const float4 x1 = *reinterpret_cast<const float4*>(stg + lr * SP + cc * 8 + 4);
+        const float vals[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
+        const int64_t gm = m0 + wm * (BM / 2) + 32 * I + lr;
+        const int64_t gn = n0 + wn * WC + cc * 8;
+        epilogue8<EPI>(a, gm, gn, vals, split);
+    }
+    __syncthreads();
+}
+
+// ---------------------------------------------------------------------------
+// the kernel
+// ---------------------------------------------------------------------------
+template <int BM, int BN, int PL, int QL, int EPI>
+__global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmArgs a) {
+    constexpr int TM = BM / 64;   // 32x32 MFMA tiles per wave along m
+    constexpr int TN = BN / 64;   // ... along n
+    constexpr int STAGE = (BM + BN) * 128;
+    static_assert(4 * 32 * (BN / 2 + 4) * 4 <= 2 * STAGE, "epilogue staging does not fit");
+    __shared__ __attribute__((aligned(16))) char smem[2 * STAGE];
+
+    // XCD-aware renumbering: hardware hands block b to XCD b % 8
+    const int64_t nb = gridDim.x;
+    int64_t b = blockIdx.x;
+    if ((nb & 7) == 0) b = (b & 7) * (nb >> 3) + (b >> 3);
+    const int64_t tiles_n = (a.N + BN - 1) / BN;
+    const int64_t tiles_m = (a.M + BM - 1) / BM;
+    const int64_t per_split = tiles_m * tiles_n;
+    const int split = (int)(b / per_split);
+    const int64_t rem = b - (int64_t)split * per_split;
+    const int64_t m0 = (rem / tiles_n) * BM;
+    const int64_t n0 = (rem % tiles_n) * BN;
+    const int64_t kbeg = (int64_t)split * a.k_chunk;
+    const int64_t kend = min(a.K, kbeg + a.k_chunk);
+    const int nk = (int)((kend - kbeg + BK - 1) / BK);
+
+    const uint16_t* P = reinterpret_cast<const uint16_t*>(a.p);
+    const uint16_t* Q = reinterpret_cast<const uint16_t*>(a.q);
+    const bool p_al = aligned16(a.p, a.ldp);
+    const bool q_al = aligned16(a.q, a.ldq);
+    const bool p_rows_full = m0 + BM <= a.M;
+    const bool q_rows_full = n0 + BN <= a.N;
+
+    const int tid = threadIdx.x;
+    const int wave = tid >> 6;
+    const int lane = tid & 63;
+    const int wm = wave >> 1;
+    const int wn = wave & 1;
+
+    f32x16 acc[TM][TN];
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.0f;
+
+    Loader<BM, PL> lp;
+    Loader<BN, QL> lq;
+
+    if (nk > 0) {
+        {
+            const bool kfull = kbeg + BK <= kend;
+            lp.load(P, a.ldp, m0, a.M, kbeg, kend, p_al && p_rows_full && kfull);
+            lq.load(Q, a.ldq, n0, a.N, kbeg, kend, q_al && q_rows_full && kfull);
+            lp.store(smem);
+            lq.store(smem + BM * 128);
+        }
+        __syncthreads();
+
+        for (int kt = 0; kt < nk; ++kt) {
+            const int cur = kt & 1;
+            const bool more = kt + 1 < nk;
+            if (more) {
+                const int64_t k0 = kbeg + (int64_t)(kt + 1) * BK;
+                const bool kfull = k0 + BK <= kend;
+                lp.load(P, a.ldp, m0, a.M, k0, kend, p_al && p_rows_full && kfull);
+                lq.load(Q, a.ldq, n0, a.N, k0, kend, q_al && q_rows_full && kfull);
+            }
+            const char* As = smem + cur * STAGE;
+            const char* Bs = As + BM * 128;
+#pragma unroll
+            for (int s = 0; s < BK / 16; ++s) {
+                bf16x8 fa[TM], fb[TN];
+                const int chunk = 2 * s + (lane >> 5);
+#pragma unroll
+                for (int i = 0; i < TM; ++i)
+                    fa[i] = *reinterpret_cast<const bf16x8*>(
+                        As + lds_off(wm * (BM / 2) + 32 * i + (lane & 31), chunk));
+#pragma unroll
+                for (int j = 0; j < TN; ++j)
+                    fb[j] = *reinterpret_cast<const bf16x8*>(
+                        Bs + lds_off(wn * (BN / 2) + 32 * j + (lane & 31), chunk));
+#pragma unroll
+                for (int i = 0; i < TM; ++i)
+#pragma unroll
+                    for (int j = 0; j < TN; ++j)
+                        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
+            }
+            if (more) {
+                char* nxt = smem + (cur ^ 1) * STAGE;
+                lp.store(nxt);
+                lq.store(nxt + BM * 128);
+            }
+            __syncthreads();
+        }
+    }
+
+    // ---- epilogue: per wave, 32-row slabs staged through LDS as fp32 ----
+    // (one instantiation per slab keeps every accumulator index a constant,
+    // so the accumulators stay in registers)
+    float* stg = reinterpret_cast<float*>(smem) + wave * 32 * (BN / 2 + 4);
+    epi_slab<0, BM, BN, EPI>(a, acc, stg, m0, n0, wm, wn, lane, split);
+    if constexpr (TM > 1) epi_slab<1, BM, BN, EPI>(a, acc, stg, m0, n0, wm, wn, lane, split);
+    if constexpr (TM > 2) epi_slab<2, BM, BN, EPI>(a, acc, stg, m0, n0, wm, wn, lane, split);
+    if constexpr (TM > 3) epi_slab<3, BM, BN, EPI>(a, acc, stg, m0, n0, wm, wn, lane, split);
+}
+
+template <int BM, int BN, int PL, int QL, int EPI>
+hipError_t launch_t(const GemmArgs& a, hipStream_t s) {
+    const int64_t tiles = ((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN) * (int64_t)a.splits;
+    if (tiles <= 0) return hipSuccess;
+    if (tiles > 0x7fffffffLL) return hipErrorInvalidConfiguration;
+    hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, PL, QL, EPI>), dim3((unsigned)tiles), dim3(NT), 0, s, a);
+    return hipGetLastError();
+}
+
+template <int PL, int QL, int EPI>
+hipError_t launch_layout(const GemmArgs& a, hipStream_t s) {
+    const bool bm256 = a.M > 128;
+    const bool bn256 = a.N > 128;
+    if (bm256 && bn256) return launch_t<256, 256, PL, QL, EPI>(a, s);
+    if (bm256) return launch_t<256, 128, PL, QL, EPI>(a, s);
+    if (bn256) return launch_t<128, 256, PL, QL, EPI>(a, s);
+    return launch_t<128, 128, PL, QL, EPI>(a, s);
+}
+
+}  // namespace
+
+hipError_t launch_gemm_bf16(const GemmArgs& a, hipStream_t s) {
+    const int pl = a.p_layout, ql = a.q_layout;
+    switch (a.epi) {
+        case EPI_Z_H:
+            if (pl == KMAJ && ql == KMAJ) return launch_layout<KMAJ, KMAJ, EPI_Z_H>(a, s);
+            break;
+        case EPI_STORE:
+            if (pl == KMAJ && ql == KMAJ) return launch_layout<KMAJ, KMAJ, EPI_STORE>(a, s);
+            if (pl == KMAJ && ql == MNMAJ) return launch_layout<KMAJ, MNMAJ, EPI_STORE>(a, s);
+            break;
+        case EPI_DZ:
+            if (pl == KMAJ && ql == MNMAJ) return launch_layout<KMAJ, MNMAJ, EPI_DZ>(a, s);
+            break;
+        case EPI_STORE_F32:
+            if (pl == MNMAJ && ql == MNMAJ) return launch_layout<MNMAJ, MNMAJ, EPI_STORE_F32>(a, s);
+            break;
+        default:
+            break;
+    }
+    return hipErrorNotSupported;
+}
+
+}  // namespace cola

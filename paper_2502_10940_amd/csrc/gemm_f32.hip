@@ -1,0 +1,192 @@
+// gemm_f32.hip -- fp32 storage path: C[M][N] = sum_k P(m, k) Q(n, k) with
+// true fp32 fused multiply-adds on the vector ALUs (no reduced-precision
+// matrix shortcut), the same operand layouts and epilogues as the bf16 MFMA
+// kernel.  Tiles of 64 x 64 outputs, K tiles of 16, 256 threads each owning a
+// 4 x 4 block; every access is guarded, so any shape and pitch is accepted.
+#include "internal.hpp"
+#include "device_math.hpp"
+
+namespace cola {
+namespace {
+
+constexpr int TB = 64;
+constexpr int KT = 16;
+
+template <int LAYOUT>
+__device__ __forceinline__ float load_op(const float* base, int64_t ld, int64_t row, int64_t rows,
+                                         int64_t k, int64_t kend) {
+    if (row >= rows || k >= kend) return 0.0f;
+    return LAYOUT == KMAJ ? base[row * ld + k] : base[k * ld + row];
+}
+
+template <int PL, int QL, int EPI>
+__global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a) {
+    __shared__ float Ps[KT][TB + 4];
+    __shared__ float Qs[KT][TB + 4];
+    const int64_t tiles_n = (a.N + TB - 1) / TB;
+    const int64_t tiles_m = (a.M + TB - 1) / TB;
+    const int64_t per_split = tiles_m * tiles_n;
+    const int64_t b = blockIdx.x;
+    const int split = (int)(b / per_split);
+    const int64_t rem = b - (int64_t)split * per_split;
+    const int64_t m0 = (rem / tiles_n) * TB;
+    const int64_t n0 = (rem % tiles_n) * TB;
+    const int64_t kbeg = (int64_t)split * a.k_chunk;
+    const int64_t kend = min(a.K, kbeg + a.k_chunk);
+    const float* P = reinterpret_cast<const float*>(a.p);
+    const float* Q = reinterpret_cast<const float*>(a.q);
+    const int tid = threadIdx.x;
+    const int tx = tid & 15;
+    const int ty = tid >> 4;
+
+    float acc[4][4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = 0.0f;
+
+    for (int64_t k0 = kbeg; k0 < kend; k0 += KT) {
+        // 64 rows x 16 k per operand = 1024 values, 4 per thread; the index
+        // order follows the contiguous dimension so loads coalesce.
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const int idx = tid + 256 * e;
+            int rp, kp, rq, kq;
+            if (PL == KMAJ) { rp = idx >> 4; kp = idx & 15; } else { kp = idx >> 6; rp = idx & 63; }
+            if (QL == KMAJ) { rq = idx >> 4; kq = idx & 15; } else { kq = idx >> 6; rq = idx & 63; }
+            Ps[kp][rp] = load_op<PL>(P, a.ldp, m0 + rp, a.M, k0 + kp, kend);
+            Qs[kq][rq] = load_op<QL>(Q, a.ldq, n0 + rq, a.N, k0 + kq, kend);
+        }
+        __syncthreads();
+#pragma unroll
+        for (int kk = 0; kk < KT; ++kk) {
+            float pv[4], qv[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) pv[i] = Ps[kk][ty * 4 + i];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) qv[j] = Qs[kk][tx * 4 + j];
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+                for (int j = 0; j < 4; ++j) acc[i][j] = fmaf(pv[i], qv[j], acc[i][j]);
+        }
+        __syncthreads();
+    }
+
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int64_t gm = m0 + ty * 4 + i;
+        if (gm >= a.M) continue;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int64_t gn = n0 + tx * 4 + j;
+            if (gn >= a.N) continue;
+            const float v = acc[i][j];
+            if constexpr (EPI == EPI_STORE || EPI == EPI_STORE_F32) {
+                reinterpret_cast<float*>(a.c)[(int64_t)split * a.split_stride + gm * a.ldc + gn] = v;
+            } else if constexpr (EPI == EPI_Z_H) {
+                reinterpret_cast<float*>(a.c)[gm * a.ldc + gn] = v;
+                if (a.aux) reinterpret_cast<float*>(a.aux)[gm * a.ldaux + gn] = act_sigma<false>(a.act, v);
+            } else if constexpr (EPI == EPI_DZ) {
+                const float z = reinterpret_cast<const float*>(a.zin)[gm * a.ldzin + gn];
+                reinterpret_cast<float*>(a.c)[gm * a.ldc + gn] = v * act_sigma_prime<false>(a.act, z);
+                if (a.aux) reinterpret_cast<float*>(a.aux)[gm * a.ldaux + gn] = act_sigma<false>(a.act, z);
+            }
+        }
+    }
+}
+
+template <int PL, int QL, int EPI>
+hipError_t launch_t(const GemmArgs& a, hipStream_t s) {
+    const int64_t tiles = ((a.M + TB - 1) / TB) * ((a.N + TB - 1) / TB) * (int64_t)a.splits;
+    if (tiles <= 0) return hipSuccess;
+    if (tiles > 0x7fffffffLL) return hipErrorInvalidConfiguration;
+    hipLaunchKernelGGL((gemm_f32_kernel<PL, QL, EPI>), dim3((unsigned)tiles), dim3(256), 0, s, a);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_gemm_f32(const GemmArgs& a, hipStream_t s) {
+    const int pl = a.p_layout, ql = a.q_layout;
+    switch (a.epi) {
+        case EPI_Z_H:
+            if (pl == KMAJ && ql == KMAJ) return launch_t<KMAJ, KMAJ, EPI_Z_H>(a, s);
+            break;
+        case EPI_STORE:
+            if (pl == KMAJ && ql == KMAJ) return launch_t<KMAJ, KMAJ, EPI_STORE>(a, s);
+            if (pl == KMAJ && ql == MNMAJ) return launch_t<KMAJ, MNMAJ, EPI_STORE>(a, s);
+            break;
+        case EPI_DZ:
+            if (pl == KMAJ && ql == MNMAJ) return launch_t<KMAJ, MNMAJ, EPI_DZ>(a, s);
+            break;
+        case EPI_STORE_F32:
+            if (pl == MNMAJ && ql == MNMAJ) return launch_t<MNMAJ, MNMAJ, EPI_STORE_F32>(a, s);
+            break;
+        default:
+            break;
+    }
+    return hipErrorNotSupported;
+}
+
+// ---------------------------------------------------------------------------
+// split-K reduction and zero fill
+// ---------------------------------------------------------------------------
+namespace {
+
+__global__ __launch_bounds__(256) void reduce_splits_kernel(const float* __restrict__ part, int splits,
+                                                            int64_t stride, float* __restrict__ out,
+                                                            int64_t n) {
+    const int64_t n4 = n >> 2;
+    const bool vec = ((stride & 3) == 0) && ((reinterpret_cast<uintptr_t>(part) & 15u) == 0) &&
+                     ((reinterpret_cast<uintptr_t>(out) & 15u) == 0);
+    const int64_t step = (int64_t)gridDim.x * blockDim.x;
+    int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (vec) {
+        for (; i < n4; i += step) {
+            float4 s = reinterpret_cast<const float4*>(part)[i];
+            for (int k = 1; k < splits; ++k) {
+                const float4 v = reinterpret_cast<const float4*>(part + (int64_t)k * stride)[i];
+                s.x += v.x; s.y += v.y; s.z += v.z; s.w += v.w;
+            }
+            reinterpret_cast<float4*>(out)[i] = s;
+        }
+        // scalar tail
+        i = n4 * 4 + (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    }
+    for (; i < n; i += step) {
+        float s = part[i];
+        for (int k = 1; k < splits; ++k) s += part[(int64_t)k * stride + i];
+        out[i] = s;
+    }
+}
+
+__global__ __launch_bounds__(256) void fill_zero_kernel(float* __restrict__ out, int64_t n) {
+    const int64_t step = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += step) out[i] = 0.0f;
+}
+
+unsigned grid_for(int64_t work) {
+    int64_t g = (work + 255) / 256;
+    if (g < 1) g = 1;
+    if (g > 4096) g = 4096;
+    return (unsigned)g;
+}
+
+}  // namespace
+
+hipError_t launch_reduce_splits(const float* part, int splits, int64_t stride, float* out, int64_t n,
+                                hipStream_t s) {
+    if (n <= 0) return hipSuccess;
+    hipLaunchKernelGGL(reduce_splits_kernel, dim3(grid_for((n + 3) / 4)), dim3(256), 0, s, part, splits,
+                       stride, out, n);
+    return hipGetLastError();
+}
+
+hipError_t launch_fill_zero(float* out, int64_t n, hipStream_t s) {
+    if (n <= 0) return hipSuccess;
+    hipLaunchKernelGGL(fill_zero_kernel, dim3(grid_for(n)), dim3(256), 0, s, out, n);
+    return hipGetLastError();
+}
+
+}  // namespace cola

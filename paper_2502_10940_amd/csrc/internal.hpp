@@ -1,0 +1,62 @@
+// internal.hpp -- declarations shared by the translation units of libcola.so.
+// Not part of the public ABI (that is include/cola.h).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace cola {
+
+// Operand layout of a GEMM C[M][N] = sum_k P(m, k) Q(n, k):
+//   KMAJ : element (m, k) at ptr[m * ld + k]   (k contiguous)
+//   MNMAJ: element (m, k) at ptr[k * ld + m]   (m contiguous, k strided)
+enum Layout : int { KMAJ = 0, MNMAJ = 1 };
+
+// Epilogue applied to the fp32 accumulator tile.
+enum Epilogue : int {
+    EPI_STORE = 0,     // c = acc, in the output dtype (bf16 / fp32 for GEMMs in fp32 storage)
+    EPI_STORE_F32 = 1, // c = acc as fp32 (weight gradients, split-K partials)
+    EPI_Z_H = 2,       // c = Z = round(acc); aux = H = round(sigma(Z))
+    EPI_DZ = 3,        // c = dZ = round(acc * sigma'(Z)), Z read from zin; aux = H if non-NULL
+};
+
+struct GemmArgs {
+    int64_t M, N, K;
+    const void* p; int64_t ldp; int p_layout;    // left operand P
+    const void* q; int64_t ldq; int q_layout;    // right operand Q (C = P Q^T)
+    void* c; int64_t ldc;                        // output
+    void* aux; int64_t ldaux;                    // second output (H) or NULL
+    const void* zin; int64_t ldzin;              // Z read by EPI_DZ
+    int epi;
+    int act;                                     // 0 identity, 1 SiLU
+    int splits;                                  // split-K count (>= 1)
+    int64_t k_chunk;                             // K range per split (multiple of the K tile)
+    int64_t split_stride;                        // elements between partial slices of c
+};
+
+// Enqueue one GEMM.  Return hipSuccess or the launch error.
+hipError_t launch_gemm_bf16(const GemmArgs& a, hipStream_t s);
+hipError_t launch_gemm_f32(const GemmArgs& a, hipStream_t s);
+
+// out[i] = sum_{s < splits} part[s * stride + i], s in increasing order (fp32).
+hipError_t launch_reduce_splits(const float* part, int splits, int64_t stride,
+                                float* out, int64_t n, hipStream_t s);
+// out[i] = 0 for i < n (fp32 words).
+hipError_t launch_fill_zero(float* out, int64_t n, hipStream_t s);
+
+// K tile of the bf16 kernel: split-K chunks are multiples of it.
+constexpr int BF16_BK = 64;
+// K tile of the fp32 kernel.
+constexpr int F32_BK = 16;
+
+// Output tiles one launch covers (before split-K), mirroring the launchers'
+// tile choice: bf16 uses 256 (or 128 when the dimension is <= 128) per side,
+// fp32 uses 64 x 64.
+inline int64_t bf16_tile(int64_t dim) { return dim > 128 ? 256 : 128; }
+inline int64_t gemm_tiles(bool bf16, int64_t M, int64_t N) {
+    const int64_t tm = bf16 ? bf16_tile(M) : 64;
+    const int64_t tn = bf16 ? bf16_tile(N) : 64;
+    return ((M + tm - 1) / tm) * ((N + tn - 1) / tn);
+}
+
+}  // namespace cola

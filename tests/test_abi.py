@@ -1,0 +1,174 @@
+"""The C ABI on the CPU: libcola.so loads without a GPU, exports every function
+include/cola.h declares, and rejects every invalid argument with its documented
+status before touching the GPU (only failing calls are made here)."""
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+
+from paper_2502_10940_amd import cola
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "cola.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    names = re.findall(r"^\s*(?:const\s+)?[A-Za-z_][\w\s]*?[\s\*]+([a-z_][a-z0-9_]*)\s*\(",
+                       text, flags=re.M)
+    return sorted(set(n for n in names if not n.startswith("typedef")))
+
+
+def test_header_declares_expected_calls():
+    names = declared_functions()
+    for n in ("cola_fwd", "cola_bwd", "cola_workspace_bytes", "cola_strerror", "cola_abi_version",
+              "dense_fwd", "dense_bwd", "dense_workspace_bytes", "cola_timing_enable",
+              "cola_timing_read", "cola_timing_reset", "cola_kernel_name"):
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol():
+    L = cola.lib()
+    for n in declared_functions():
+        assert hasattr(L, n), n
+    out = subprocess.run(["nm", "-D", "--defined-only", cola.LIB_PATH], capture_output=True,
+                         text=True, check=True).stdout
+    exported = set(line.split()[-1] for line in out.splitlines() if line.strip())
+    for n in declared_functions():
+        assert n in exported, n
+    assert set(declared_functions()) == set(cola.EXPORTS)
+
+
+def test_abi_version_and_strerror():
+    L = cola.lib()
+    assert L.cola_abi_version() == 1
+    for s in range(6):
+        assert L.cola_strerror(s)
+    assert L.cola_strerror(99) == b"unknown status"
+    for k in range(len(cola.KERNEL_CLASSES)):
+        assert cola.kernel_name(k) == cola.KERNEL_CLASSES[k]
+    assert cola.kernel_name(-1) == "invalid"
+
+
+FAKE = 0x1000  # never dereferenced: every call below fails validation first
+
+
+def fwd_status(d, X=FAKE, A=FAKE, B=FAKE, Y=FAKE, Z=FAKE, H=FAKE, ws=None, ws_bytes=0):
+    p = ctypes.byref(d) if d is not None else None
+    return cola.lib().cola_fwd(p, X, A, B, Y, Z, H, ws, ws_bytes, None)
+
+
+def bwd_status(d, dY=FAKE, X=FAKE, Z=FAKE, H=FAKE, A=FAKE, B=FAKE, dX=FAKE, dA=FAKE, dB=FAKE,
+               ws=None, ws_bytes=0):
+    p = ctypes.byref(d) if d is not None else None
+    return cola.lib().cola_bwd(p, dY, X, Z, H, A, B, dX, dA, dB, ws, ws_bytes, None)
+
+
+def test_invalid_descriptors():
+    assert fwd_status(None) == cola.ERR_INVALID_ARG
+    assert bwd_status(None) == cola.ERR_INVALID_ARG
+    for kw, code in ((dict(dtype=7), cola.ERR_INVALID_ARG), (dict(act=5), cola.ERR_INVALID_ARG),
+                     (dict(recompute=True), None)):
+        d = cola.desc(16, 32, 32, 8, **{k: v for k, v in kw.items() if k != "recompute"})
+        if "recompute" in kw:
+            d.recompute = 2
+            code = cola.ERR_INVALID_ARG
+        assert fwd_status(d) == code
+        assert bwd_status(d) == code
+    for shape in ((16, 0, 32, 8), (16, 32, 0, 8), (16, 32, 32, 0), (-1, 32, 32, 8)):
+        d = cola.desc(*shape)
+        assert fwd_status(d) == cola.ERR_BAD_SHAPE
+        assert bwd_status(d) == cola.ERR_BAD_SHAPE
+        assert cola.workspace_bytes(d, 0) == 0 and cola.workspace_bytes(d, 1) == 0
+    for ld in (dict(ldx=31), dict(ldy=30), dict(ldz=7)):
+        d = cola.desc(16, 32, 32, 8, **ld)
+        assert fwd_status(d) == cola.ERR_BAD_SHAPE
+        assert bwd_status(d) == cola.ERR_BAD_SHAPE
+    d = cola.desc(1 << 41, 32, 32, 8)
+    assert fwd_status(d) == cola.ERR_BAD_SHAPE
+
+
+def test_h_must_match_recompute():
+    d = cola.desc(16, 32, 32, 8, recompute=False)
+    assert fwd_status(d, H=None) == cola.ERR_INVALID_ARG
+    assert bwd_status(d, H=None) == cola.ERR_INVALID_ARG
+    d = cola.desc(16, 32, 32, 8, recompute=True)
+    assert fwd_status(d, H=FAKE) == cola.ERR_INVALID_ARG
+    assert bwd_status(d, H=FAKE) == cola.ERR_INVALID_ARG
+
+
+@pytest.mark.parametrize("name", ["X", "A", "B", "Y", "Z"])
+def test_null_forward_pointers(name):
+    d = cola.desc(16, 32, 32, 8)
+    assert fwd_status(d, **{name: None}) == cola.ERR_INVALID_ARG
+
+
+@pytest.mark.parametrize("name", ["dY", "X", "Z", "A", "B", "dX", "dA", "dB"])
+def test_null_backward_pointers(name):
+    d = cola.desc(16, 32, 32, 8)
+    need = cola.workspace_bytes(d, 1)
+    assert bwd_status(d, ws=FAKE, ws_bytes=need, **{name: None}) == cola.ERR_INVALID_ARG
+
+
+def test_workspace_too_small():
+    d = cola.desc(64, 32, 48, 8, recompute=True)
+    need = cola.workspace_bytes(d, 0)
+    assert need >= 64 * 8 * 2
+    assert fwd_status(d, H=None, ws=FAKE, ws_bytes=need - 1) == cola.ERR_WORKSPACE
+    assert fwd_status(d, H=None, ws=None, ws_bytes=need) == cola.ERR_WORKSPACE
+    need_b = cola.workspace_bytes(d, 1)
+    assert need_b >= 2 * 64 * 8 * 2          # dZ and the recomputed H
+    assert bwd_status(d, H=None, ws=FAKE, ws_bytes=need_b - 1) == cola.ERR_WORKSPACE
+
+
+def test_workspace_sizes():
+    for dtype, es in (("bf16", 2), ("f32", 4)):
+        d = cola.desc(1000, 96, 80, 24, dtype=dtype)
+        assert cola.workspace_bytes(d, 0) == 0                       # CoLA: H is an output
+        dm = cola.desc(1000, 96, 80, 24, dtype=dtype, recompute=True)
+        assert cola.workspace_bytes(dm, 0) >= 1000 * 24 * es         # CoLA-M keeps H here
+        assert cola.workspace_bytes(dm, 1) >= cola.workspace_bytes(d, 1) + 1000 * 24 * es
+        assert cola.workspace_bytes(d, 2) == 0
+    empty = cola.desc(0, 96, 80, 24)
+    assert cola.workspace_bytes(empty, 0) == 0 and cola.workspace_bytes(empty, 1) == 0
+
+
+def test_empty_forward_is_a_noop():
+    # T = 0 is an empty batch: nothing to compute, nothing enqueued
+    d = cola.desc(0, 32, 32, 8)
+    assert fwd_status(d, X=None, A=None, B=None, Y=None, Z=None) == cola.OK
+
+
+def test_dense_validation():
+    L = cola.lib()
+    d = cola.dense_desc(16, 0, 8)
+    assert L.dense_fwd(ctypes.byref(d), FAKE, FAKE, FAKE, None, 0, None) == cola.ERR_BAD_SHAPE
+    d = cola.dense_desc(16, 32, 8, dtype=3)
+    assert L.dense_fwd(ctypes.byref(d), FAKE, FAKE, FAKE, None, 0, None) == cola.ERR_INVALID_ARG
+    d = cola.dense_desc(16, 32, 8)
+    assert L.dense_fwd(ctypes.byref(d), None, FAKE, FAKE, None, 0, None) == cola.ERR_INVALID_ARG
+    assert L.dense_bwd(ctypes.byref(d), FAKE, FAKE, FAKE, FAKE, None, None, 0, None) == cola.ERR_INVALID_ARG
+    big = cola.dense_desc(100000, 512, 512)
+    need = cola.dense_workspace_bytes(big, 1)
+    assert need > 0
+    assert L.dense_bwd(ctypes.byref(big), FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, need - 1, None) == cola.ERR_WORKSPACE
+
+
+def test_timing_api_validation():
+    L = cola.lib()
+    n = ctypes.c_int64(); x = ctypes.c_double()
+    assert L.cola_timing_read(99, ctypes.byref(n), ctypes.byref(x), ctypes.byref(x),
+                              ctypes.byref(x)) == cola.ERR_INVALID_ARG
+    assert L.cola_timing_read(0, None, ctypes.byref(x), ctypes.byref(x), ctypes.byref(x)) == cola.ERR_INVALID_ARG
+    # enable/disable touch no GPU state
+    assert L.cola_timing_enable(0) == cola.OK
+
+
+def test_binding_raises_on_error():
+    d = cola.desc(16, 0, 32, 8)
+    with pytest.raises(cola.ColaError) as e:
+        cola.fwd(d, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, stream=0)
+    assert e.value.status == cola.ERR_BAD_SHAPE
