@@ -1,0 +1,317 @@
+"""Benchmark: one step = forward + backward of every CoLA projection of a
+LLaMA-shaped decoder block (q, k, v, o, gate, up, down), all through the
+C ABI of libcola.so on one MI355X.
+
+Default workload: the LLaMA-1B-shaped block (d = 2048, ffn = 5461, r = 512,
+T = 128 x 256 = 32768 tokens), bf16 storage with fp32 accumulation, SiLU.
+Reported value: algorithmic TFLOP/s = sum over projections of
+6 T r (d_in + d_out) per step (Sec. 3.4: 2MNK per GEMM, sigma excluded),
+divided by the measured step time.  Inputs are resident in HBM before the
+timed region.  Also measured on the same harness: the CoLA-M step and the
+dense full-rank step (6 T d_in d_out), for tokens/s and the speedup.
+
+Prints ONE JSON line.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+import numpy as np  # noqa: E402
+
+BF16_PEAK_TFLOPS = 2516.6     # MI355X dense bf16 MFMA: 256 CU x 4096 flop/clk x 2.4 GHz
+FP32_PEAK_TFLOPS = 157.3
+HBM_PEAK_GBS = 8000.0
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", type=int, default=4, help="1..5 (default 4: LLaMA-1B-shaped block)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-dense", action="store_true")
+    ap.add_argument("--no-cola-m", action="store_true")
+    ap.add_argument("--cpu-tokens", type=int, default=1024,
+                    help="tokens per projection in the oracle's CPU sample")
+    ap.add_argument("--only", choices=["cola", "cola_m", "dense"], default=None,
+                    help="run only one mode (profiling)")
+    return ap.parse_args()
+
+
+def algo_flops_cola(T, d_in, d_out, r):
+    """fwd + bwd of one CoLA layer: 6 GEMMs of 2 T r d each (Sec. 3.4)."""
+    return 6.0 * T * r * (d_in + d_out)
+
+
+def algo_flops_dense(T, d_in, d_out):
+    return 6.0 * T * d_in * d_out
+
+
+class Projection:
+    def __init__(self, cfg, name, idx, d_in, d_out, r, T, dtype, dense: bool, recompute_too: bool):
+        import torch
+        from paper_2502_10940_amd import cola
+        from paper_2502_10940_amd import inputs as I
+        self.name, self.T, self.d_in, self.d_out, self.r = name, T, d_in, d_out, r
+        self.dtype = dtype
+        tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+        dev = "cuda:0"
+        self.ldx = I.padded_ld(d_in, dtype)
+        self.ldy = I.padded_ld(d_out, dtype)
+        self.ldz = I.padded_ld(r, dtype)
+        ins = I.layer_inputs(cfg, idx, d_in, d_out, r, T, dtype, with_dense=dense)
+        self.host = ins
+
+        def put(t, ld=None):
+            a = t.store
+            if ld is not None and ld != a.shape[1]:
+                a = I.with_pitch(a, ld, 0)
+            if dtype == "bf16":
+                x = torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).to(dev).view(torch.bfloat16)
+            else:
+                x = torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+            return x
+
+        self.X = put(ins["X"], self.ldx)
+        self.A = put(ins["A"])
+        self.B = put(ins["B"])
+        self.dY = put(ins["dY"], self.ldy)
+        self.W = put(ins["W"]) if dense else None
+        self.Y = torch.empty((T, self.ldy), dtype=tdt, device=dev)
+        self.Z = torch.empty((T, self.ldz), dtype=tdt, device=dev)
+        self.H = torch.empty((T, self.ldz), dtype=tdt, device=dev)
+        self.dX = torch.empty((T, self.ldx), dtype=tdt, device=dev)
+        self.dA = torch.empty((r, d_in), dtype=torch.float32, device=dev)
+        self.dB = torch.empty((d_out, r), dtype=torch.float32, device=dev)
+        self.dW = torch.empty((d_out, d_in), dtype=torch.float32, device=dev) if dense else None
+        self.desc = cola.desc(T, d_in, d_out, r, dtype, "silu", False, self.ldx, self.ldy, self.ldz)
+        self.desc_m = cola.desc(T, d_in, d_out, r, dtype, "silu", True, self.ldx, self.ldy, self.ldz)
+        self.ddesc = cola.dense_desc(T, d_in, d_out, dtype, self.ldx, self.ldy)
+        self.ws_need = max(cola.workspace_bytes(self.desc, 0), cola.workspace_bytes(self.desc, 1),
+                           cola.workspace_bytes(self.desc_m, 0) if recompute_too else 0,
+                           cola.workspace_bytes(self.desc_m, 1) if recompute_too else 0,
+                           cola.dense_workspace_bytes(self.ddesc, 1) if dense else 0)
+
+    def fwd(self, ws, recompute=False):
+        from paper_2502_10940_amd import cola
+        if recompute:
+            cola.fwd(self.desc_m, self.X, self.A, self.B, self.Y, self.Z, None, ws)
+        else:
+            cola.fwd(self.desc, self.X, self.A, self.B, self.Y, self.Z, self.H, ws)
+
+    def bwd(self, ws, recompute=False):
+        from paper_2502_10940_amd import cola
+        if recompute:
+            cola.bwd(self.desc_m, self.dY, self.X, self.Z, None, self.A, self.B, self.dX, self.dA,
+                     self.dB, ws)
+        else:
+            cola.bwd(self.desc, self.dY, self.X, self.Z, self.H, self.A, self.B, self.dX, self.dA,
+                     self.dB, ws)
+
+    def dense_step(self, ws):
+        from paper_2502_10940_amd import cola
+        cola.dense_fwd(self.ddesc, self.X, self.W, self.Y)
+        cola.dense_bwd(self.ddesc, self.dY, self.X, self.W, self.dX, self.dW, ws)
+
+
+def timed_steps(step, steps, warmup):
+    import torch
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    s = torch.cuda.Event(enable_timing=True)
+    e = torch.cuda.Event(enable_timing=True)
+    s.record()
+    for _ in range(steps):
+        step()
+    e.record()
+    torch.cuda.synchronize()
+    return s.elapsed_time(e) / steps
+
+
+def kernel_table(cola):
+    out = {}
+    for k, name in enumerate(cola.KERNEL_CLASSES):
+        n, ms, fl, by = cola.timing_read(k)
+        if n == 0:
+            continue
+        out[name] = {"launches": n, "avg_us": 1000.0 * ms / n, "total_ms": ms,
+                     "tflops": fl / (ms * 1e9) if ms > 0 else 0.0,
+                     "gbs": by / (ms * 1e6) if ms > 0 else 0.0,
+                     "flops_per_launch": fl / n, "bytes_per_launch": by / n}
+    return out
+
+
+def load_traffic(kernel):
+    """HBM bytes per launch measured by rocprofv3 counters (profiles/traffic.json),
+    or None when absent or taken on a different kernel source."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(path):
+        return None
+    try:
+        rec = json.load(open(path))
+    except (OSError, ValueError):
+        return None
+    ent = rec.get(kernel)
+    if not ent:
+        return None
+    import hashlib
+    src = os.path.join(ROOT, "paper_2502_10940_amd", "csrc", "gemm_bf16.hip")
+    h = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
+    if ent.get("source_sha256_16") != h:
+        return None
+    return ent.get("bytes_per_launch")
+
+
+def cpu_baseline(projs, cfg_T, tokens):
+    """The fp64 oracle (test infrastructure, untuned) on a bounded sample: the
+    first ``tokens`` tokens of each projection, forward + backward."""
+    import oracle
+    from paper_2502_10940_amd import inputs as I
+    t_total = 0.0
+    flops = 0.0
+    for p in projs:
+        X = I.Tensor(p.host["X"].store[:tokens], p.dtype).f64
+        A = p.host["A"].f64
+        B = p.host["B"].f64
+        dY = I.Tensor(p.host["dY"].store[:tokens], p.dtype).f64
+        t0 = time.perf_counter()
+        Z, _, _ = oracle.cola_fwd(X, A, B, "silu")
+        oracle.cola_bwd(X, Z, A, B, dY, "silu")
+        t_total += time.perf_counter() - t0
+        flops += algo_flops_cola(tokens, p.d_in, p.d_out, p.r)
+    return {"value": flops / t_total / 1e12, "unit": "TFLOP/s", "cores": oracle.num_threads(),
+            "kind": "oracle",
+            "sample": f"first {tokens} of {cfg_T} tokens of each of the {len(projs)} projections, "
+                      f"fwd+bwd in fp64 ({t_total:.1f} s)",
+            "seconds": t_total, "tokens_per_s": tokens / t_total}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (got --gpus {args.gpus}); this build has no "
+              "multi-GPU path", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    from paper_2502_10940_amd import cola
+    from paper_2502_10940_amd import inputs as I
+
+    cola.lib()
+    w = I.WORKLOADS[args.workload]
+    dtype = w["dtype"]
+    T, r = w["T"], w["r"]
+    do_dense = not args.no_dense and args.only in (None, "dense")
+    do_m = not args.no_cola_m and args.only in (None, "cola_m")
+    do_cola = args.only in (None, "cola")
+    t0 = time.time()
+    projs = [Projection(args.workload, name, idx, d_in, d_out, r, T, dtype, do_dense, do_m)
+             for name, idx, d_in, d_out in I.projections(args.workload)]
+    ws = torch.empty(max(p.ws_need for p in projs), dtype=torch.uint8, device="cuda:0")
+    setup_s = time.time() - t0
+
+    def step_cola():
+        for p in projs:
+            p.fwd(ws)
+        for p in reversed(projs):
+            p.bwd(ws)
+
+    def step_cola_m():
+        for p in projs:
+            p.fwd(ws, True)
+        for p in reversed(projs):
+            p.bwd(ws, True)
+
+    def step_dense():
+        for p in projs:
+            p.dense_step(ws)
+
+    flops_cola = sum(algo_flops_cola(T, p.d_in, p.d_out, r) for p in projs)
+    flops_dense = sum(algo_flops_dense(T, p.d_in, p.d_out) for p in projs)
+    peak = BF16_PEAK_TFLOPS if dtype == "bf16" else FP32_PEAK_TFLOPS
+
+    res = {}
+    kernels = {}
+    if do_cola:
+        # timed region with per-kernel HIP events (recorded on the launch stream)
+        cola.timing_enable(False)
+        for _ in range(args.warmup):
+            step_cola()
+        torch.cuda.synchronize()
+        cola.timing_reset()
+        cola.timing_enable(True)
+        ms = timed_steps(step_cola, args.steps, 0)
+        cola.timing_enable(False)
+        kernels = kernel_table(cola)
+        res["cola"] = ms
+    if do_m:
+        res["cola_m"] = timed_steps(step_cola_m, args.steps, args.warmup)
+    if do_dense:
+        res["dense"] = timed_steps(step_dense, args.steps, args.warmup)
+
+    main_mode = "cola" if do_cola else ("cola_m" if do_m else "dense")
+    ms = res[main_mode]
+    flops_main = flops_dense if main_mode == "dense" else flops_cola
+    value = flops_main / (ms * 1e9)
+
+    out = {
+        "metric": "CoLA layer fwd+bwd TFLOP/s (algorithmic) on a LLaMA-1B-shaped block, 7 projections",
+        "value": round(value, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": dtype,
+        "data": "synthetic",
+        "config": {"workload": w["name"], "tokens": T, "d": w["d"], "ffn": w["ffn"], "rank": r,
+                   "projections": [p.name for p in projs], "act": "silu", "mode": main_mode,
+                   "step": "fwd of all projections, then bwd in reverse order"},
+        "pct_of_bf16_mfma_peak": round(100.0 * value / peak, 2),
+        "tokens_per_s": round(T / (ms / 1e3), 1),
+    }
+    if "cola_m" in res:
+        out["cola_m"] = {"ms_per_step": round(res["cola_m"], 4),
+                         "tflops": round(flops_cola / (res["cola_m"] * 1e9), 2),
+                         "tokens_per_s": round(T / (res["cola_m"] / 1e3), 1)}
+    if "dense" in res:
+        out["dense"] = {"ms_per_step": round(res["dense"], 4),
+                        "tflops": round(flops_dense / (res["dense"] * 1e9), 2),
+                        "tokens_per_s": round(T / (res["dense"] / 1e3), 1)}
+        if "cola" in res:
+            out["speedup_vs_dense"] = round(res["dense"] / res["cola"], 3)
+        if "cola_m" in res:
+            out["cola_m"]["speedup_vs_dense"] = round(res["dense"] / res["cola_m"], 3)
+    if kernels:
+        dom = max(kernels, key=lambda k: kernels[k]["total_ms"])
+        kd = kernels[dom]
+        achieved = kd["flops_per_launch"] / (kd["avg_us"] * 1e6)   # TFLOP/s
+        traffic = load_traffic(dom)
+        out["roofline"] = {"kernel": dom, "bound": "mfma", "achieved": round(achieved, 2),
+                           "peak": peak, "unit": "TFLOP/s", "frac": round(achieved / peak, 4),
+                           "traffic": traffic, "avg_us": round(kd["avg_us"], 2),
+                           "flops_per_launch": kd["flops_per_launch"]}
+        out["kernels"] = {k: {kk: (round(vv, 3) if isinstance(vv, float) else vv)
+                              for kk, vv in v.items()} for k, v in kernels.items()}
+    if not args.no_cpu_baseline and main_mode != "dense":
+        out["cpu_baseline"] = cpu_baseline(projs, T, min(args.cpu_tokens, T))
+        out["cpu_baseline"]["value"] = round(out["cpu_baseline"]["value"], 6)
+    out["setup_s"] = round(setup_s, 1)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

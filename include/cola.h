@@ -100,8 +100,9 @@ const char* cola_strerror(int status);
 size_t cola_workspace_bytes(const cola_desc* desc, int phase);
 
 /* Forward (Eq. main-fwd): Z = X A^T, H = sigma(Z), Y = H B^T.
- * Writes Z and Y; writes H when recompute = 0 (H must then be non-NULL) and
- * keeps H in the workspace when recompute = 1 (H must then be NULL). */
+ * Writes Z and Y; writes H when recompute = 0 (H must then be non-NULL unless
+ * T = 0) and keeps H in the workspace when recompute = 1 (H must then be
+ * NULL).  With T = 0 nothing is enqueued and activation pointers may be NULL. */
 int cola_fwd(const cola_desc* desc,
              const void* X, const void* A, const void* B,
              void* Y, void* Z, void* H,

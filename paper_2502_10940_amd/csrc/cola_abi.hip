@@ -301,7 +301,8 @@ int cola_fwd(const cola_desc* desc, const void* X, const void* A, const void* B,
         int st = check_desc(desc, &x);
         if (st != COLA_OK) return st;
         const bool recompute = desc->recompute == 1;
-        if (recompute ? (H != nullptr) : (H == nullptr)) return COLA_ERR_INVALID_ARG;
+        // CoLA-M never takes H; CoLA needs it unless the batch is empty
+        if (recompute ? (H != nullptr) : (H == nullptr && x.T > 0)) return COLA_ERR_INVALID_ARG;
         if (x.T == 0) return COLA_OK;
         if (!X || !A || !B || !Y || !Z) return COLA_ERR_INVALID_ARG;
         const size_t need = fwd_ws(x, recompute);

@@ -140,6 +140,10 @@ def test_empty_forward_is_a_noop():
     # T = 0 is an empty batch: nothing to compute, nothing enqueued
     d = cola.desc(0, 32, 32, 8)
     assert fwd_status(d, X=None, A=None, B=None, Y=None, Z=None) == cola.OK
+    assert fwd_status(d, X=None, A=None, B=None, Y=None, Z=None, H=None) == cola.OK
+    dm = cola.desc(0, 32, 32, 8, recompute=True)
+    assert fwd_status(dm, X=None, A=None, B=None, Y=None, Z=None, H=None) == cola.OK
+    assert fwd_status(dm, H=FAKE) == cola.ERR_INVALID_ARG
 
 
 def test_dense_validation():
