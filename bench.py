@@ -45,7 +45,85 @@ def parse():
                     help="tokens per projection in the oracle's CPU sample")
     ap.add_argument("--only", choices=["cola", "cola_m", "dense"], default=None,
                     help="run only one mode (profiling)")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="run only a plain 1 GiB device copy (3 times), for scaling HBM counters")
+    ap.add_argument("--traffic-from", nargs=4, metavar=("FETCH_CSV", "WRITE_CSV", "COPY_FETCH_CSV",
+                                                         "COPY_WRITE_CSV"),
+                    help="summarise rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE runs into "
+                         "profiles/traffic.json and exit (no GPU use)")
     return ap.parse_args()
+
+
+COPY_BYTES = 1 << 30
+KERNEL_TAGS = {0: "fwd_z_sigma", 1: "fwd_y", 2: "bwd_dz", 3: "bwd_dx", 4: "bwd_da", 5: "bwd_db",
+               7: "dense_fwd", 8: "dense_dx", 9: "dense_dw"}
+
+
+def copy_calibration():
+    import torch
+    src = torch.empty(COPY_BYTES, dtype=torch.uint8, device="cuda:0").fill_(1)
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_calibration_bytes": COPY_BYTES, "repeats": 3}), flush=True)
+
+
+def _pmc_rows(path, counter):
+    import csv
+    rows = []
+    for r in csv.DictReader(open(path)):
+        if r.get("Counter_Name") != counter:
+            continue
+        rows.append((r["Kernel_Name"], int(r["Dispatch_Id"]), float(r["Counter_Value"])))
+    return rows
+
+
+def traffic_summary(fetch_csv, write_csv, copy_fetch_csv, copy_write_csv):
+    """HBM bytes per launch for each GEMM kernel class, from rocprofv3 --pmc
+    FETCH_SIZE and WRITE_SIZE (KiB per dispatch), each scaled by the ratio of
+    the known bytes of a plain 1 GiB copy to what the same counter reads for
+    that copy."""
+    import hashlib
+    import re
+
+    def copy_factor(path, counter):
+        vals = [v for name, _, v in _pmc_rows(path, counter) if "copy" in name.lower()
+                or "elementwise" in name.lower()]
+        big = [v for v in vals if v * 1024 > 0.5 * COPY_BYTES]
+        if not big:
+            raise SystemExit(f"no copy dispatch found in {path}")
+        return COPY_BYTES / (sorted(big)[len(big) // 2] * 1024.0)
+
+    ff = copy_factor(copy_fetch_csv, "FETCH_SIZE")
+    fw = copy_factor(copy_write_csv, "WRITE_SIZE")
+    per = {}
+    for path, counter, scale, key in ((fetch_csv, "FETCH_SIZE", ff, "fetch"),
+                                      (write_csv, "WRITE_SIZE", fw, "write")):
+        for name, _, v in _pmc_rows(path, counter):
+            m = re.search(r"gemm_bf16_kernel<\d+, \d+, \d+, \d+, \d+, (\d+)>", name)
+            if not m:
+                continue
+            cls = KERNEL_TAGS.get(int(m.group(1)))
+            per.setdefault(cls, {}).setdefault(key, []).append(v * 1024.0 * scale)
+    src = os.path.join(ROOT, "paper_2502_10940_amd", "csrc", "gemm_bf16.hip")
+    h = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
+    out = {"_note": "HBM bytes per launch from rocprofv3 FETCH_SIZE + WRITE_SIZE, scaled by a "
+                    "1 GiB copy (fetch factor %.4f, write factor %.4f)" % (ff, fw)}
+    for cls, d in per.items():
+        f = d.get("fetch", [])
+        w = d.get("write", [])
+        if not f or not w:
+            continue
+        out[cls] = {"bytes_per_launch": sum(f) / len(f) + sum(w) / len(w),
+                    "fetch_bytes_per_launch": sum(f) / len(f),
+                    "write_bytes_per_launch": sum(w) / len(w),
+                    "launches": len(f), "source_sha256_16": h}
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    with open(path, "w") as fh:
+        json.dump(out, fh, indent=1, sort_keys=True)
+    print(json.dumps(out), flush=True)
 
 
 def algo_flops_cola(T, d_in, d_out, r):
@@ -100,6 +178,7 @@ class Projection:
         self.ws_need = max(cola.workspace_bytes(self.desc, 0), cola.workspace_bytes(self.desc, 1),
                            cola.workspace_bytes(self.desc_m, 0) if recompute_too else 0,
                            cola.workspace_bytes(self.desc_m, 1) if recompute_too else 0,
+                           cola.dense_workspace_bytes(self.ddesc, 0) if dense else 0,
                            cola.dense_workspace_bytes(self.ddesc, 1) if dense else 0)
 
     def fwd(self, ws, recompute=False):
@@ -120,7 +199,7 @@ class Projection:
 
     def dense_step(self, ws):
         from paper_2502_10940_amd import cola
-        cola.dense_fwd(self.ddesc, self.X, self.W, self.Y)
+        cola.dense_fwd(self.ddesc, self.X, self.W, self.Y, ws)
         cola.dense_bwd(self.ddesc, self.dY, self.X, self.W, self.dX, self.dW, ws)
 
 
@@ -199,6 +278,9 @@ def cpu_baseline(projs, cfg_T, tokens):
 
 def main():
     args = parse()
+    if args.traffic_from:
+        traffic_summary(*args.traffic_from)
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (got --gpus {args.gpus}); this build has no "
               "multi-GPU path", file=sys.stderr)
@@ -207,6 +289,9 @@ def main():
     from paper_2502_10940_amd import cola
     from paper_2502_10940_amd import inputs as I
 
+    if args.copy_calibration:
+        copy_calibration()
+        return
     cola.lib()
     w = I.WORKLOADS[args.workload]
     dtype = w["dtype"]

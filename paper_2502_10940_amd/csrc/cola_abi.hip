@@ -146,27 +146,45 @@ int check_desc(const cola_desc* d, Dims* out) {
 
 size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
-// Split of a token-long (K = T) weight-gradient GEMM: enough workgroups to
-// cover the chip twice, each split at least four K tiles long.  Depends only
-// on the shape, so results are reproducible run to run.
+// Split of a token-long (K = T) weight-gradient GEMM into chunks of whole K
+// tiles (at least four per chunk).  Depends only on the shape, so results are
+// reproducible run to run.
 struct Split {
     int splits;
     int64_t k_chunk;
 };
 
+// The split count S minimises a modelled time: rounds(S) * ceil(ktiles / S)
+// K-tile steps of about 2 us each, where rounds(S) = ceil(tiles * S / slots)
+// and slots is the number of workgroups the chip runs at once (256 CUs x 2
+// for the bf16 kernel) -- a split that leaves a few workgroups for a second
+// round costs a whole round -- plus writing and re-reading the S fp32
+// partials at about 4 TB/s.
 Split plan_split(bool bf16, int64_t M, int64_t N, int64_t K) {
     const int64_t bk = bf16 ? BF16_BK : F32_BK;
     const int64_t tiles = gemm_tiles(bf16, M, N);
-    const int64_t target = 512;
-    int64_t want = (target + tiles - 1) / tiles;
+    const int64_t slots = bf16 ? 512 : 1024;
     const int64_t ktiles = (K + bk - 1) / bk;
+    if (ktiles < 1) return Split{1, bk};                       // empty batch: nothing to split
+    const double step_us = 2.0;
+    const double partial_us_per_split = (double)M * (double)N * 8.0 / 4.0e6;
     int64_t maxs = ktiles / 4;
     if (maxs < 1) maxs = 1;
-    if (want > maxs) want = maxs;
-    if (want > 64) want = 64;
-    if (want < 1) want = 1;
-    int64_t chunk_tiles = (ktiles + want - 1) / want;
-    if (chunk_tiles < 1) chunk_tiles = 1;
+    if (maxs > 64) maxs = 64;
+    int64_t best_s = 1;
+    double best_cost = -1.0;
+    for (int64_t s = 1; s <= maxs; ++s) {
+        const int64_t chunk = (ktiles + s - 1) / s;
+        const int64_t eff_s = (ktiles + chunk - 1) / chunk;   // splits actually used
+        const int64_t rounds = (tiles * eff_s + slots - 1) / slots;
+        const double cost = (double)(rounds * chunk) * step_us +
+                            (eff_s > 1 ? (double)eff_s * partial_us_per_split : 0.0);
+        if (best_cost < 0 || cost < best_cost) {
+            best_cost = cost;
+            best_s = s;
+        }
+    }
+    const int64_t chunk_tiles = (ktiles + best_s - 1) / best_s;
     Split s;
     s.k_chunk = chunk_tiles * bk;
     s.splits = (int)((K + s.k_chunk - 1) / s.k_chunk);
@@ -174,10 +192,60 @@ Split plan_split(bool bf16, int64_t M, int64_t N, int64_t K) {
     return s;
 }
 
+// A bf16 weight whose rows are not a whole number of 16-byte chunks (width
+// not a multiple of 8) is copied to the workspace with a padded pitch, so the
+// MFMA kernel keeps its vector loads.  Depends only on the shape.
+struct Pack {
+    bool on;
+    int64_t ld;     // pitch to use for the weight
+    size_t off, bytes;
+};
+
+Pack plan_pack(bool bf16, int64_t rows, int64_t width, size_t off) {
+    Pack p;
+    p.off = off;
+    p.on = bf16 && (width % 8) != 0;
+    p.ld = p.on ? (width + 7) / 8 * 8 : width;
+    p.bytes = p.on ? align256((size_t)rows * (size_t)p.ld * 2) : 0;
+    return p;
+}
+
+// Resolve a weight to (pointer, pitch), enqueueing its repack if planned.
+hipError_t use_weight(const Pack& pk, const void* w, int64_t rows, int64_t width, char* ws,
+                      const void** out, int64_t* ld, hipStream_t s) {
+    if (!pk.on) {
+        *out = w;
+        *ld = width;
+        return hipSuccess;
+    }
+    *out = ws + pk.off;
+    *ld = pk.ld;
+    return launch_pack_rows(w, rows, width, ws + pk.off, pk.ld, s);
+}
+
+struct FwdPlan {
+    int64_t ldw;          // pitch of the workspace copy of H (CoLA-M)
+    size_t off_h, total;
+    Pack pa, pb;          // repacked A [r][d_in] and B [d_out][r]
+};
+
+FwdPlan plan_fwd(const Dims& x, bool recompute) {
+    FwdPlan p;
+    p.ldw = x.bf16 ? (x.r + 7) / 8 * 8 : (x.r + 3) / 4 * 4;
+    p.off_h = 0;
+    const size_t hbytes = recompute ? align256((size_t)x.T * (size_t)p.ldw * x.esize) : 0;
+    p.pa = plan_pack(x.bf16, x.r, x.d_in, hbytes);
+    p.pb = plan_pack(x.bf16, x.d_out, x.r, p.pa.off + p.pa.bytes);
+    p.total = p.pb.off + p.pb.bytes;
+    if (x.T == 0) p.total = 0;
+    return p;
+}
+
 struct BwdPlan {
     int64_t ldw;          // pitch of dZ (and recomputed H) in the workspace
     size_t off_dz, off_h, off_pa, off_pb, total;
     Split sa, sb;
+    Pack wa, wb;          // repacked A and B
 };
 
 BwdPlan plan_bwd(const Dims& x, bool recompute) {
@@ -192,24 +260,23 @@ BwdPlan plan_bwd(const Dims& x, bool recompute) {
     const size_t pa = p.sa.splits > 1 ? align256((size_t)p.sa.splits * (size_t)(x.r * x.d_in) * 4) : 0;
     p.off_pb = p.off_pa + pa;
     const size_t pb = p.sb.splits > 1 ? align256((size_t)p.sb.splits * (size_t)(x.d_out * x.r) * 4) : 0;
-    p.total = p.off_pb + pb;
+    p.wa = plan_pack(x.bf16, x.r, x.d_in, p.off_pb + pb);
+    p.wb = plan_pack(x.bf16, x.d_out, x.r, p.wa.off + p.wa.bytes);
+    p.total = p.wb.off + p.wb.bytes;
     if (x.T == 0) p.total = 0;
     return p;
 }
 
-size_t fwd_ws(const Dims& x, bool recompute) {
-    if (!recompute || x.T == 0) return 0;
-    const int64_t ldw = x.bf16 ? (x.r + 7) / 8 * 8 : (x.r + 3) / 4 * 4;
-    return align256((size_t)x.T * (size_t)ldw * x.esize);
-}
+size_t fwd_ws(const Dims& x, bool recompute) { return plan_fwd(x, recompute).total; }
 
 hipError_t gemm(const GemmArgs& a, bool bf16, hipStream_t s) {
     return bf16 ? launch_gemm_bf16(a, s) : launch_gemm_f32(a, s);
 }
 
-GemmArgs make_args(int64_t M, int64_t N, int64_t K, const void* p, int64_t ldp, int pl,
+GemmArgs make_args(int tag, int64_t M, int64_t N, int64_t K, const void* p, int64_t ldp, int pl,
                    const void* q, int64_t ldq, int ql, void* c, int64_t ldc, int epi, int act) {
     GemmArgs a{};
+    a.tag = tag;
     a.M = M; a.N = N; a.K = K;
     a.p = p; a.ldp = ldp; a.p_layout = pl;
     a.q = q; a.ldq = ldq; a.q_layout = ql;
@@ -228,7 +295,7 @@ double gemm_flops(int64_t M, int64_t N, int64_t K) { return 2.0 * (double)M * (d
 int wgrad(bool bf16, int64_t M, int64_t N, int64_t T, const void* P, int64_t ldp, const void* Q,
           int64_t ldq, float* C, const Split& sp, float* partials, int kc, double bytes_in,
           hipStream_t s) {
-    GemmArgs a = make_args(M, N, T, P, ldp, MNMAJ, Q, ldq, MNMAJ, C, N, EPI_STORE_F32, 0);
+    GemmArgs a = make_args(kc, M, N, T, P, ldp, MNMAJ, Q, ldq, MNMAJ, C, N, EPI_STORE_F32, 0);
     a.splits = sp.splits;
     a.k_chunk = sp.k_chunk;
     if (sp.splits > 1) {
@@ -305,26 +372,32 @@ int cola_fwd(const cola_desc* desc, const void* X, const void* A, const void* B,
         if (recompute ? (H != nullptr) : (H == nullptr && x.T > 0)) return COLA_ERR_INVALID_ARG;
         if (x.T == 0) return COLA_OK;
         if (!X || !A || !B || !Y || !Z) return COLA_ERR_INVALID_ARG;
-        const size_t need = fwd_ws(x, recompute);
-        if (need > 0 && (!ws || ws_bytes < need)) return COLA_ERR_WORKSPACE;
+        const FwdPlan p = plan_fwd(x, recompute);
+        if (p.total > 0 && (!ws || ws_bytes < p.total)) return COLA_ERR_WORKSPACE;
         hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+        char* w = reinterpret_cast<char*>(ws);
 
-        void* Hbuf = recompute ? ws : H;
-        const int64_t ldh = recompute ? (x.bf16 ? (x.r + 7) / 8 * 8 : (x.r + 3) / 4 * 4) : x.ldz;
+        void* Hbuf = recompute ? (void*)(w + p.off_h) : H;
+        const int64_t ldh = recompute ? p.ldw : x.ldz;
         const double es = (double)x.esize;
+        const void* Aw;
+        const void* Bw;
+        int64_t lda, ldb;
+        hipError_t e = use_weight(p.pa, A, x.r, x.d_in, w, &Aw, &lda, s);
+        if (e == hipSuccess) e = use_weight(p.pb, B, x.d_out, x.r, w, &Bw, &ldb, s);
+        if (e != hipSuccess) return hip_fail(e, "pack_rows");
 
         // K1: Z = X A^T, H = sigma(Z)
-        GemmArgs k1 = make_args(x.T, x.r, x.d_in, X, x.ldx, KMAJ, A, x.d_in, KMAJ, Z, x.ldz, EPI_Z_H,
+        GemmArgs k1 = make_args(TAG_FWD_Z, x.T, x.r, x.d_in, X, x.ldx, KMAJ, Aw, lda, KMAJ, Z, x.ldz, EPI_Z_H,
                                 desc->act);
         k1.aux = Hbuf;
         k1.ldaux = ldh;
         const double b1 = es * ((double)x.T * x.d_in + (double)x.r * x.d_in + 2.0 * x.T * x.r);
-        hipError_t e = timed(COLA_KC_FWD_Z, gemm_flops(x.T, x.r, x.d_in), b1, s,
-                             [&] { return gemm(k1, x.bf16, s); });
+        e = timed(COLA_KC_FWD_Z, gemm_flops(x.T, x.r, x.d_in), b1, s, [&] { return gemm(k1, x.bf16, s); });
         if (e != hipSuccess) return hip_fail(e, "fwd_z_sigma");
 
         // K2: Y = H B^T
-        GemmArgs k2 = make_args(x.T, x.d_out, x.r, Hbuf, ldh, KMAJ, B, x.r, KMAJ, Y, x.ldy, EPI_STORE,
+        GemmArgs k2 = make_args(TAG_FWD_Y, x.T, x.d_out, x.r, Hbuf, ldh, KMAJ, Bw, ldb, KMAJ, Y, x.ldy, EPI_STORE,
                                 desc->act);
         const double b2 = es * ((double)x.T * x.r + (double)x.d_out * x.r + (double)x.T * x.d_out);
         e = timed(COLA_KC_FWD_Y, gemm_flops(x.T, x.d_out, x.r), b2, s, [&] { return gemm(k2, x.bf16, s); });
@@ -362,9 +435,15 @@ int cola_bwd(const cola_desc* desc, const void* dY, const void* X, const void* Z
         const void* Hbuf = recompute ? (const void*)(w + p.off_h) : H;
         const int64_t ldh = recompute ? p.ldw : x.ldz;
         const double es = (double)x.esize;
+        const void* Aw;
+        const void* Bw;
+        int64_t lda, ldb;
+        hipError_t e = use_weight(p.wa, A, x.r, x.d_in, w, &Aw, &lda, s);
+        if (e == hipSuccess) e = use_weight(p.wb, B, x.d_out, x.r, w, &Bw, &ldb, s);
+        if (e != hipSuccess) return hip_fail(e, "pack_rows");
 
         // K3: dZ = (dY B) (.) sigma'(Z); CoLA-M regenerates H = sigma(Z) here
-        GemmArgs k3 = make_args(x.T, x.r, x.d_out, dY, x.ldy, KMAJ, B, x.r, MNMAJ, dZ, p.ldw, EPI_DZ,
+        GemmArgs k3 = make_args(TAG_BWD_DZ, x.T, x.r, x.d_out, dY, x.ldy, KMAJ, Bw, ldb, MNMAJ, dZ, p.ldw, EPI_DZ,
                                 desc->act);
         k3.zin = Z;
         k3.ldzin = x.ldz;
@@ -372,12 +451,11 @@ int cola_bwd(const cola_desc* desc, const void* dY, const void* X, const void* Z
         k3.ldaux = p.ldw;
         const double b3 = es * ((double)x.T * x.d_out + (double)x.d_out * x.r +
                                 (double)x.T * x.r * (recompute ? 3.0 : 2.0));
-        hipError_t e = timed(COLA_KC_BWD_DZ, gemm_flops(x.T, x.r, x.d_out), b3, s,
-                             [&] { return gemm(k3, x.bf16, s); });
+        e = timed(COLA_KC_BWD_DZ, gemm_flops(x.T, x.r, x.d_out), b3, s, [&] { return gemm(k3, x.bf16, s); });
         if (e != hipSuccess) return hip_fail(e, "bwd_dz");
 
         // K4: dX = dZ A
-        GemmArgs k4 = make_args(x.T, x.d_in, x.r, dZ, p.ldw, KMAJ, A, x.d_in, MNMAJ, dX, x.ldx, EPI_STORE,
+        GemmArgs k4 = make_args(TAG_BWD_DX, x.T, x.d_in, x.r, dZ, p.ldw, KMAJ, Aw, lda, MNMAJ, dX, x.ldx, EPI_STORE,
                                 desc->act);
         const double b4 = es * ((double)x.T * x.r + (double)x.r * x.d_in + (double)x.T * x.d_in);
         e = timed(COLA_KC_BWD_DX, gemm_flops(x.T, x.d_in, x.r), b4, s, [&] { return gemm(k4, x.bf16, s); });
@@ -407,28 +485,49 @@ static int check_dense(const dense_desc* d, Dims* out) {
     return check_desc(&c, out);
 }
 
+// Workspace of the dense path: [split-K partials of dW (phase 1)] [W repack].
+struct DensePlan {
+    Split sp;
+    size_t parts;
+    Pack pw;
+    size_t total;
+};
+
+static DensePlan plan_dense(const Dims& x, int phase) {
+    DensePlan p;
+    p.sp = plan_split(x.bf16, x.d_out, x.d_in, x.T);
+    p.parts = (phase == 1 && p.sp.splits > 1) ? align256((size_t)p.sp.splits * (size_t)(x.d_out * x.d_in) * 4) : 0;
+    p.pw = plan_pack(x.bf16, x.d_out, x.d_in, p.parts);
+    p.total = p.pw.off + p.pw.bytes;
+    if (x.T == 0) p.total = 0;
+    return p;
+}
+
 size_t dense_workspace_bytes(const dense_desc* desc, int phase) {
     Dims x;
     if (check_dense(desc, &x) != COLA_OK) return 0;
-    if (phase != 1 || x.T == 0) return 0;
-    const Split sp = plan_split(x.bf16, x.d_out, x.d_in, x.T);
-    return sp.splits > 1 ? align256((size_t)sp.splits * (size_t)(x.d_out * x.d_in) * 4) : 0;
+    if (phase != 0 && phase != 1) return 0;
+    return plan_dense(x, phase).total;
 }
 
 int dense_fwd(const dense_desc* desc, const void* X, const void* W, void* Y, void* ws, size_t ws_bytes,
               cola_stream_t stream) {
-    (void)ws; (void)ws_bytes;
     return guarded([&]() -> int {
         Dims x;
         int st = check_dense(desc, &x);
         if (st != COLA_OK) return st;
         if (x.T == 0) return COLA_OK;
         if (!X || !W || !Y) return COLA_ERR_INVALID_ARG;
+        const DensePlan p = plan_dense(x, 0);
+        if (p.total > 0 && (!ws || ws_bytes < p.total)) return COLA_ERR_WORKSPACE;
         hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-        GemmArgs a = make_args(x.T, x.d_out, x.d_in, X, x.ldx, KMAJ, W, x.d_in, KMAJ, Y, x.ldy, EPI_STORE, 0);
+        const void* Ww;
+        int64_t ldw;
+        hipError_t e = use_weight(p.pw, W, x.d_out, x.d_in, reinterpret_cast<char*>(ws), &Ww, &ldw, s);
+        if (e != hipSuccess) return hip_fail(e, "pack_rows");
+        GemmArgs a = make_args(TAG_DENSE_FWD, x.T, x.d_out, x.d_in, X, x.ldx, KMAJ, Ww, ldw, KMAJ, Y, x.ldy, EPI_STORE, 0);
         const double b = (double)x.esize * ((double)x.T * x.d_in + (double)x.d_out * x.d_in + (double)x.T * x.d_out);
-        hipError_t e = timed(COLA_KC_DENSE_FWD, gemm_flops(x.T, x.d_out, x.d_in), b, s,
-                             [&] { return gemm(a, x.bf16, s); });
+        e = timed(COLA_KC_DENSE_FWD, gemm_flops(x.T, x.d_out, x.d_in), b, s, [&] { return gemm(a, x.bf16, s); });
         return e == hipSuccess ? COLA_OK : hip_fail(e, "dense_fwd");
     });
 }
@@ -447,15 +546,18 @@ int dense_bwd(const dense_desc* desc, const void* dY, const void* X, const void*
             return e == hipSuccess ? COLA_OK : hip_fail(e, "fill_zero");
         }
         if (!dY || !X || !W || !dX) return COLA_ERR_INVALID_ARG;
-        const Split sp = plan_split(x.bf16, x.d_out, x.d_in, x.T);
-        const size_t need = dense_workspace_bytes(desc, 1);
-        if (need > 0 && (!ws || ws_bytes < need)) return COLA_ERR_WORKSPACE;
-        GemmArgs a = make_args(x.T, x.d_in, x.d_out, dY, x.ldy, KMAJ, W, x.d_in, MNMAJ, dX, x.ldx, EPI_STORE, 0);
+        const DensePlan p = plan_dense(x, 1);
+        if (p.total > 0 && (!ws || ws_bytes < p.total)) return COLA_ERR_WORKSPACE;
+        char* w = reinterpret_cast<char*>(ws);
+        const void* Ww;
+        int64_t ldw;
+        hipError_t e = use_weight(p.pw, W, x.d_out, x.d_in, w, &Ww, &ldw, s);
+        if (e != hipSuccess) return hip_fail(e, "pack_rows");
+        GemmArgs a = make_args(TAG_DENSE_DX, x.T, x.d_in, x.d_out, dY, x.ldy, KMAJ, Ww, ldw, MNMAJ, dX, x.ldx, EPI_STORE, 0);
         const double b = (double)x.esize * ((double)x.T * x.d_out + (double)x.d_out * x.d_in + (double)x.T * x.d_in);
-        hipError_t e = timed(COLA_KC_DENSE_DX, gemm_flops(x.T, x.d_in, x.d_out), b, s,
-                             [&] { return gemm(a, x.bf16, s); });
+        e = timed(COLA_KC_DENSE_DX, gemm_flops(x.T, x.d_in, x.d_out), b, s, [&] { return gemm(a, x.bf16, s); });
         if (e != hipSuccess) return hip_fail(e, "dense_dx");
-        return wgrad(x.bf16, x.d_out, x.d_in, x.T, dY, x.ldy, X, x.ldx, dW, sp, reinterpret_cast<float*>(ws),
+        return wgrad(x.bf16, x.d_out, x.d_in, x.T, dY, x.ldy, X, x.ldx, dW, p.sp, reinterpret_cast<float*>(w),
                      COLA_KC_DENSE_DW, (double)x.esize * ((double)x.T * x.d_out + (double)x.T * x.d_in), s);
     });
 }

@@ -5,6 +5,9 @@
 // Design (CDNA4, wave64):
 //  * 256 threads = 4 waves in a 2 x 2 grid; each wave owns a (BM/2) x (BN/2)
 //    block of C, computed with v_mfma_f32_32x32x16_bf16 tiles (acc in fp32).
+//    Two workgroups share a CU (128 accumulator registers per wave, 48-64 KB
+//    of LDS per workgroup), so one workgroup's barriers and memory waits are
+//    covered by the other's MFMAs.
 //  * K advances in tiles of 64.  Both operand tiles live in LDS as [row][k]
 //    with 128-byte rows; the eight 16-byte chunks of a row are XOR-swizzled
 //    by (row ^ row >> 3) & 7, so the MFMA fragment reads (16 B per lane) and
@@ -15,8 +18,9 @@
 //    matrices) are loaded as 16-byte runs along m and transposed in registers
 //    (8 x 8 blocks of bf16, pure permutes) on their way into LDS, so the MFMA
 //    core only ever sees k-contiguous fragments.
-//  * Double-buffered LDS: the next tile's global loads are issued before the
-//    current tile's MFMAs, with one barrier per K tile.
+//  * One LDS tile per operand: the next K tile's global loads are issued
+//    before the current tile's MFMAs and land in registers; they are written
+//    to LDS between two barriers once the MFMAs are done with it.
 //  * Workgroups are renumbered so that each XCD (blockIdx % 8 on MI355X)
 //    receives a contiguous run of output tiles: tiles sharing an operand row
 //    block share that XCD's L2.
@@ -56,8 +60,13 @@ struct Loader<R, KMAJ> {
     static constexpr int NV = R / 32;
     uint4 v[NV];
 
+    // fast: the whole tile is in range and 16-byte aligned.  Otherwise each
+    // 16-byte chunk is checked: whole chunks in range load as vectors (when
+    // aligned), a chunk straddling the K end loads element by element, and
+    // chunks out of range read as zero.
     __device__ __forceinline__ void load(const uint16_t* base, int64_t ld, int64_t row0,
-                                         int64_t rows, int64_t k0, int64_t kend, bool fast) {
+                                         int64_t rows, int64_t k0, int64_t kend, bool fast,
+                                         bool aligned) {
         const int t = threadIdx.x;
         const int c = t & 7;
         const int r = t >> 3;
@@ -71,15 +80,19 @@ struct Loader<R, KMAJ> {
             for (int i = 0; i < NV; ++i) {
                 const int64_t row = row0 + r + 32 * i;
                 const int64_t k = k0 + c * 8;
-                uint32_t w[4];
+                if (row < rows && k + 8 <= kend && aligned) {
+                    v[i] = *reinterpret_cast<const uint4*>(base + row * ld + k);
+                } else {
+                    uint32_t w[4];
 #pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    uint32_t lo = 0, hi = 0;
-                    if (row < rows && k + 2 * e < kend) lo = base[row * ld + k + 2 * e];
-                    if (row < rows && k + 2 * e + 1 < kend) hi = base[row * ld + k + 2 * e + 1];
-                    w[e] = lo | (hi << 16);
+                    for (int e = 0; e < 4; ++e) {
+                        uint32_t lo = 0, hi = 0;
+                        if (row < rows && k + 2 * e < kend) lo = base[row * ld + k + 2 * e];
+                        if (row < rows && k + 2 * e + 1 < kend) hi = base[row * ld + k + 2 * e + 1];
+                        w[e] = lo | (hi << 16);
+                    }
+                    v[i] = make_uint4(w[0], w[1], w[2], w[3]);
                 }
-                v[i] = make_uint4(w[0], w[1], w[2], w[3]);
             }
         }
     }
@@ -106,7 +119,8 @@ struct Loader<R, MNMAJ> {
     uint4 v[KR];
 
     __device__ __forceinline__ void load(const uint16_t* base, int64_t ld, int64_t row0,
-                                         int64_t rows, int64_t k0, int64_t kend, bool fast) {
+                                         int64_t rows, int64_t k0, int64_t kend, bool fast,
+                                         bool aligned) {
         const int t = threadIdx.x;
         const int mb = t % MB;
         const int kb = t / MB;
@@ -120,15 +134,19 @@ struct Loader<R, MNMAJ> {
         } else {
 #pragma unroll
             for (int kk = 0; kk < KR; ++kk) {
-                uint32_t w[4];
+                if (k + kk < kend && m + 8 <= rows && aligned) {
+                    v[kk] = *reinterpret_cast<const uint4*>(base + (k + kk) * ld + m);
+                } else {
+                    uint32_t w[4];
 #pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    uint32_t lo = 0, hi = 0;
-                    if (k + kk < kend && m + 2 * e < rows) lo = base[(k + kk) * ld + m + 2 * e];
-                    if (k + kk < kend && m + 2 * e + 1 < rows) hi = base[(k + kk) * ld + m + 2 * e + 1];
-                    w[e] = lo | (hi << 16);
+                    for (int e = 0; e < 4; ++e) {
+                        uint32_t lo = 0, hi = 0;
+                        if (k + kk < kend && m + 2 * e < rows) lo = base[(k + kk) * ld + m + 2 * e];
+                        if (k + kk < kend && m + 2 * e + 1 < rows) hi = base[(k + kk) * ld + m + 2 * e + 1];
+                        w[e] = lo | (hi << 16);
+                    }
+                    v[kk] = make_uint4(w[0], w[1], w[2], w[3]);
                 }
-                v[kk] = make_uint4(w[0], w[1], w[2], w[3]);
             }
         }
     }
@@ -251,11 +269,12 @@ __device__ __forceinline__ void epilogue8(const GemmArgs& a, int64_t gm, int64_t
     }
 }
 
-// One 32-row slab (MFMA row tile I) of a wave's accumulators: stage through
-// LDS as fp32 in [row][col] order, then each lane handles 8 consecutive
-// columns of a row, so global accesses are 16-byte vectors.
-template <int I, int BM, int BN, int EPI, int TM, int TN>
-__device__ __forceinline__ void epi_slab(const GemmArgs& a, const f32x16 (&acc)[TM][TN], float* stg,
+// Half of MFMA row tile I (16 rows: accumulator registers 8H..8H+7) of a
+// wave's accumulators: staged through LDS as fp32 in [row][col] order, then
+// each lane handles 8 consecutive columns of a row, so global accesses are
+// 16-byte vectors.
+template <int I, int H, int BM, int BN, int EPI, int TM, int TN>
+__device__ __forceinline__ void epi_half(const GemmArgs& a, const f32x16 (&acc)[TM][TN], float* stg,
                                          int64_t m0, int64_t n0, int wm, int wn, int lane, int split) {
     constexpr int WC = BN / 2;            // wave columns
     constexpr int SP = WC + 4;            // staging pitch (floats)
@@ -264,8 +283,9 @@ __device__ __forceinline__ void epi_slab(const GemmArgs& a, const f32x16 (&acc)[
 #pragma unroll
     for (int j = 0; j < TN; ++j)
 #pragma unroll
-        for (int v = 0; v < 16; ++v) {
-            const int row = 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
+        for (int vv = 0; vv < 8; ++vv) {
+            const int v = 8 * H + vv;
+            const int row = 8 * (vv >> 2) + 4 * (lane >> 5) + (v & 3);   // row within the half
             const int col = 32 * j + (lane & 31);
             stg[row * SP + col] = acc[I][j][v];
         }
@@ -273,28 +293,37 @@ __device__ __forceinline__ void epi_slab(const GemmArgs& a, const f32x16 (&acc)[
     const int cc = lane % LPR;
     const int rr = lane / LPR;
 #pragma unroll
-    for (int pass = 0; pass < 32 / RPP; ++pass) {
+    for (int pass = 0; pass < 16 / RPP; ++pass) {
         const int lr = pass * RPP + rr;
         const float4 x0 = *reinterpret_cast<const float4*>(stg + lr * SP + cc * 8);
         const float4 x1 = *reinterpret_cast<const float4*>(stg + lr * SP + cc * 8 + 4);
         const float vals[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
-        const int64_t gm = m0 + wm * (BM / 2) + 32 * I + lr;
+        const int64_t gm = m0 + wm * (BM / 2) + 32 * I + 16 * H + lr;
         const int64_t gn = n0 + wn * WC + cc * 8;
         epilogue8<EPI>(a, gm, gn, vals, split);
     }
     __syncthreads();
 }
 
+template <int I, int BM, int BN, int EPI, int TM, int TN>
+__device__ __forceinline__ void epi_slab(const GemmArgs& a, const f32x16 (&acc)[TM][TN], float* stg,
+                                         int64_t m0, int64_t n0, int wm, int wn, int lane, int split) {
+    epi_half<I, 0, BM, BN, EPI>(a, acc, stg, m0, n0, wm, wn, lane, split);
+    epi_half<I, 1, BM, BN, EPI>(a, acc, stg, m0, n0, wm, wn, lane, split);
+}
+
 // ---------------------------------------------------------------------------
 // the kernel
 // ---------------------------------------------------------------------------
-template <int BM, int BN, int PL, int QL, int EPI>
-__global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmArgs a) {
+// TAG is the kernel class (one symbol per step of the layer, so profiles
+// name them apart); it does not change the code.
+template <int BM, int BN, int PL, int QL, int EPI, int TAG>
+__global__ __launch_bounds__(NT, 2) void gemm_bf16_kernel(GemmArgs a) {
     constexpr int TM = BM / 64;   // 32x32 MFMA tiles per wave along m
     constexpr int TN = BN / 64;   // ... along n
-    constexpr int STAGE = (BM + BN) * 128;
-    static_assert(4 * 32 * (BN / 2 + 4) * 4 <= 2 * STAGE, "epilogue staging does not fit");
-    __shared__ __attribute__((aligned(16))) char smem[2 * STAGE];
+    constexpr int TILE = (BM + BN) * 128;
+    static_assert(4 * 16 * (BN / 2 + 4) * 4 <= TILE, "epilogue staging does not fit");
+    __shared__ __attribute__((aligned(16))) char smem[TILE];
 
     // XCD-aware renumbering: hardware hands block b to XCD b % 8
     const int64_t nb = gridDim.x;
@@ -334,28 +363,26 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmArgs a) {
 
     Loader<BM, PL> lp;
     Loader<BN, QL> lq;
+    char* As = smem;
+    char* Bs = smem + BM * 128;
 
     if (nk > 0) {
         {
             const bool kfull = kbeg + BK <= kend;
-            lp.load(P, a.ldp, m0, a.M, kbeg, kend, p_al && p_rows_full && kfull);
-            lq.load(Q, a.ldq, n0, a.N, kbeg, kend, q_al && q_rows_full && kfull);
-            lp.store(smem);
-            lq.store(smem + BM * 128);
+            lp.load(P, a.ldp, m0, a.M, kbeg, kend, p_al && p_rows_full && kfull, p_al);
+            lq.load(Q, a.ldq, n0, a.N, kbeg, kend, q_al && q_rows_full && kfull, q_al);
         }
-        __syncthreads();
-
         for (int kt = 0; kt < nk; ++kt) {
-            const int cur = kt & 1;
-            const bool more = kt + 1 < nk;
-            if (more) {
+            if (kt > 0) __syncthreads();          // everyone is done reading the tile
+            lp.store(As);
+            lq.store(Bs);
+            __syncthreads();                      // the new tile is visible
+            if (kt + 1 < nk) {                    // next tile's loads fly during the MFMAs
                 const int64_t k0 = kbeg + (int64_t)(kt + 1) * BK;
                 const bool kfull = k0 + BK <= kend;
-                lp.load(P, a.ldp, m0, a.M, k0, kend, p_al && p_rows_full && kfull);
-                lq.load(Q, a.ldq, n0, a.N, k0, kend, q_al && q_rows_full && kfull);
+                lp.load(P, a.ldp, m0, a.M, k0, kend, p_al && p_rows_full && kfull, p_al);
+                lq.load(Q, a.ldq, n0, a.N, k0, kend, q_al && q_rows_full && kfull, q_al);
             }
-            const char* As = smem + cur * STAGE;
-            const char* Bs = As + BM * 128;
 #pragma unroll
             for (int s = 0; s < BK / 16; ++s) {
                 bf16x8 fa[TM], fb[TN];
@@ -374,66 +401,51 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmArgs a) {
                     for (int j = 0; j < TN; ++j)
                         acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
             }
-            if (more) {
-                char* nxt = smem + (cur ^ 1) * STAGE;
-                lp.store(nxt);
-                lq.store(nxt + BM * 128);
-            }
-            __syncthreads();
         }
     }
+    __syncthreads();                              // LDS is reused for the epilogue staging
 
-    // ---- epilogue: per wave, 32-row slabs staged through LDS as fp32 ----
+    // ---- epilogue: per wave, 16-row half slabs staged through LDS as fp32 ----
     // (one instantiation per slab keeps every accumulator index a constant,
     // so the accumulators stay in registers)
-    float* stg = reinterpret_cast<float*>(smem) + wave * 32 * (BN / 2 + 4);
+    float* stg = reinterpret_cast<float*>(smem) + wave * 16 * (BN / 2 + 4);
     epi_slab<0, BM, BN, EPI>(a, acc, stg, m0, n0, wm, wn, lane, split);
     if constexpr (TM > 1) epi_slab<1, BM, BN, EPI>(a, acc, stg, m0, n0, wm, wn, lane, split);
     if constexpr (TM > 2) epi_slab<2, BM, BN, EPI>(a, acc, stg, m0, n0, wm, wn, lane, split);
     if constexpr (TM > 3) epi_slab<3, BM, BN, EPI>(a, acc, stg, m0, n0, wm, wn, lane, split);
 }
 
-template <int BM, int BN, int PL, int QL, int EPI>
+template <int BM, int BN, int PL, int QL, int EPI, int TAG>
 hipError_t launch_t(const GemmArgs& a, hipStream_t s) {
     const int64_t tiles = ((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN) * (int64_t)a.splits;
     if (tiles <= 0) return hipSuccess;
     if (tiles > 0x7fffffffLL) return hipErrorInvalidConfiguration;
-    hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, PL, QL, EPI>), dim3((unsigned)tiles), dim3(NT), 0, s, a);
+    hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, PL, QL, EPI, TAG>), dim3((unsigned)tiles), dim3(NT), 0, s, a);
     return hipGetLastError();
 }
 
-template <int PL, int QL, int EPI>
+template <int PL, int QL, int EPI, int TAG>
 hipError_t launch_layout(const GemmArgs& a, hipStream_t s) {
-    const bool bm256 = a.M > 128;
-    const bool bn256 = a.N > 128;
-    if (bm256 && bn256) return launch_t<256, 256, PL, QL, EPI>(a, s);
-    if (bm256) return launch_t<256, 128, PL, QL, EPI>(a, s);
-    if (bn256) return launch_t<128, 256, PL, QL, EPI>(a, s);
-    return launch_t<128, 128, PL, QL, EPI>(a, s);
+    if (a.p_layout != PL || a.q_layout != QL || a.epi != EPI) return hipErrorInvalidValue;
+    if (a.M > 128) return launch_t<256, 128, PL, QL, EPI, TAG>(a, s);
+    return launch_t<128, 128, PL, QL, EPI, TAG>(a, s);
 }
 
 }  // namespace
 
 hipError_t launch_gemm_bf16(const GemmArgs& a, hipStream_t s) {
-    const int pl = a.p_layout, ql = a.q_layout;
-    switch (a.epi) {
-        case EPI_Z_H:
-            if (pl == KMAJ && ql == KMAJ) return launch_layout<KMAJ, KMAJ, EPI_Z_H>(a, s);
-            break;
-        case EPI_STORE:
-            if (pl == KMAJ && ql == KMAJ) return launch_layout<KMAJ, KMAJ, EPI_STORE>(a, s);
-            if (pl == KMAJ && ql == MNMAJ) return launch_layout<KMAJ, MNMAJ, EPI_STORE>(a, s);
-            break;
-        case EPI_DZ:
-            if (pl == KMAJ && ql == MNMAJ) return launch_layout<KMAJ, MNMAJ, EPI_DZ>(a, s);
-            break;
-        case EPI_STORE_F32:
-            if (pl == MNMAJ && ql == MNMAJ) return launch_layout<MNMAJ, MNMAJ, EPI_STORE_F32>(a, s);
-            break;
-        default:
-            break;
+    switch (a.tag) {
+        case TAG_FWD_Z: return launch_layout<KMAJ, KMAJ, EPI_Z_H, TAG_FWD_Z>(a, s);
+        case TAG_FWD_Y: return launch_layout<KMAJ, KMAJ, EPI_STORE, TAG_FWD_Y>(a, s);
+        case TAG_BWD_DZ: return launch_layout<KMAJ, MNMAJ, EPI_DZ, TAG_BWD_DZ>(a, s);
+        case TAG_BWD_DX: return launch_layout<KMAJ, MNMAJ, EPI_STORE, TAG_BWD_DX>(a, s);
+        case TAG_BWD_DA: return launch_layout<MNMAJ, MNMAJ, EPI_STORE_F32, TAG_BWD_DA>(a, s);
+        case TAG_BWD_DB: return launch_layout<MNMAJ, MNMAJ, EPI_STORE_F32, TAG_BWD_DB>(a, s);
+        case TAG_DENSE_FWD: return launch_layout<KMAJ, KMAJ, EPI_STORE, TAG_DENSE_FWD>(a, s);
+        case TAG_DENSE_DX: return launch_layout<KMAJ, MNMAJ, EPI_STORE, TAG_DENSE_DX>(a, s);
+        case TAG_DENSE_DW: return launch_layout<MNMAJ, MNMAJ, EPI_STORE_F32, TAG_DENSE_DW>(a, s);
+        default: return hipErrorNotSupported;
     }
-    return hipErrorNotSupported;
 }
 
 }  // namespace cola

@@ -130,7 +130,7 @@ hipError_t launch_gemm_f32(const GemmArgs& a, hipStream_t s) {
 }
 
 // ---------------------------------------------------------------------------
-// split-K reduction and zero fill
+// split-K reduction, zero fill, and row repacking of 16-bit weights
 // ---------------------------------------------------------------------------
 namespace {
 
@@ -166,6 +166,18 @@ __global__ __launch_bounds__(256) void fill_zero_kernel(float* __restrict__ out,
     for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += step) out[i] = 0.0f;
 }
 
+__global__ __launch_bounds__(256) void pack_rows_kernel(const uint16_t* __restrict__ src, int64_t rows,
+                                                        int64_t width, uint16_t* __restrict__ dst,
+                                                        int64_t ld) {
+    const int64_t n = rows * ld;
+    const int64_t step = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += step) {
+        const int64_t r = i / ld;
+        const int64_t c = i - r * ld;
+        dst[i] = c < width ? src[r * width + c] : (uint16_t)0;
+    }
+}
+
 unsigned grid_for(int64_t work) {
     int64_t g = (work + 255) / 256;
     if (g < 1) g = 1;
@@ -180,6 +192,14 @@ hipError_t launch_reduce_splits(const float* part, int splits, int64_t stride, f
     if (n <= 0) return hipSuccess;
     hipLaunchKernelGGL(reduce_splits_kernel, dim3(grid_for((n + 3) / 4)), dim3(256), 0, s, part, splits,
                        stride, out, n);
+    return hipGetLastError();
+}
+
+hipError_t launch_pack_rows(const void* src, int64_t rows, int64_t width, void* dst, int64_t ld,
+                            hipStream_t s) {
+    if (rows <= 0) return hipSuccess;
+    hipLaunchKernelGGL(pack_rows_kernel, dim3(grid_for(rows * ld)), dim3(256), 0, s,
+                       reinterpret_cast<const uint16_t*>(src), rows, width, reinterpret_cast<uint16_t*>(dst), ld);
     return hipGetLastError();
 }
 

@@ -20,6 +20,13 @@ enum Epilogue : int {
     EPI_DZ = 3,        // c = dZ = round(acc * sigma'(Z)), Z read from zin; aux = H if non-NULL
 };
 
+// Which step of the layer a GEMM is (same numbering as the kernel classes of
+// the public timing API).
+enum Tag : int {
+    TAG_FWD_Z = 0, TAG_FWD_Y = 1, TAG_BWD_DZ = 2, TAG_BWD_DX = 3, TAG_BWD_DA = 4,
+    TAG_BWD_DB = 5, TAG_DENSE_FWD = 7, TAG_DENSE_DX = 8, TAG_DENSE_DW = 9
+};
+
 struct GemmArgs {
     int64_t M, N, K;
     const void* p; int64_t ldp; int p_layout;    // left operand P
@@ -28,6 +35,7 @@ struct GemmArgs {
     void* aux; int64_t ldaux;                    // second output (H) or NULL
     const void* zin; int64_t ldzin;              // Z read by EPI_DZ
     int epi;
+    int tag;                                     // Tag
     int act;                                     // 0 identity, 1 SiLU
     int splits;                                  // split-K count (>= 1)
     int64_t k_chunk;                             // K range per split (multiple of the K tile)
@@ -41,6 +49,11 @@ hipError_t launch_gemm_f32(const GemmArgs& a, hipStream_t s);
 // out[i] = sum_{s < splits} part[s * stride + i], s in increasing order (fp32).
 hipError_t launch_reduce_splits(const float* part, int splits, int64_t stride,
                                 float* out, int64_t n, hipStream_t s);
+// dst[r][c] = src[r][c] for c < width, 0 for width <= c < ld (16-bit
+// elements; src rows are contiguous).  Gives weights with odd widths a
+// 16-byte aligned row pitch.
+hipError_t launch_pack_rows(const void* src, int64_t rows, int64_t width, void* dst, int64_t ld,
+                            hipStream_t s);
 // out[i] = 0 for i < n (fp32 words).
 hipError_t launch_fill_zero(float* out, int64_t n, hipStream_t s);
 
@@ -50,12 +63,10 @@ constexpr int BF16_BK = 64;
 constexpr int F32_BK = 16;
 
 // Output tiles one launch covers (before split-K), mirroring the launchers'
-// tile choice: bf16 uses 256 (or 128 when the dimension is <= 128) per side,
-// fp32 uses 64 x 64.
-inline int64_t bf16_tile(int64_t dim) { return dim > 128 ? 256 : 128; }
+// tile choice: bf16 uses 256 x 128 (128 x 128 when M <= 128), fp32 64 x 64.
 inline int64_t gemm_tiles(bool bf16, int64_t M, int64_t N) {
-    const int64_t tm = bf16 ? bf16_tile(M) : 64;
-    const int64_t tn = bf16 ? bf16_tile(N) : 64;
+    const int64_t tm = bf16 ? (M > 128 ? 256 : 128) : 64;
+    const int64_t tn = bf16 ? 128 : 64;
     return ((M + tm - 1) / tm) * ((N + tn - 1) / tn);
 }
 

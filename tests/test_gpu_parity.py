@@ -36,6 +36,8 @@ CASES = [
     ("odd_pitch_bf16", 17, 37, 29, 5, "bf16", "silu"),
     ("rank_ge_width_bf16", 40, 16, 24, 32, "bf16", "silu"),
     ("t255_bf16", 255, 264, 136, 8, "bf16", "silu"),
+    ("odd_width_weight_repack_bf16", 300, 301, 263, 40, "bf16", "silu"),
+    ("odd_rank_weight_repack_bf16", 200, 136, 144, 37, "bf16", "silu"),
 ]
 
 
@@ -139,9 +141,9 @@ def test_empty_batch(recompute):
     assert torch.count_nonzero(dA).item() == 0 and torch.count_nonzero(dB).item() == 0
 
 
-@pytest.mark.parametrize("dtype", ["bf16", "f32"])
-def test_dense_parity(dtype):
-    T, d_in, d_out = 520, 300, 264
+@pytest.mark.parametrize("dtype,d_in", [("bf16", 300), ("f32", 300), ("bf16", 301)])
+def test_dense_parity(dtype, d_in):
+    T, d_out = 520, 264
     ins = gen(54, T, d_in, d_out, 8, dtype, with_dense=True)
     X, W, dY = ins["X"].f64, ins["W"].f64, ins["dY"].f64
     Yr = oracle.dense_fwd(X, W)
@@ -153,8 +155,9 @@ def test_dense_parity(dtype):
     Y = torch.empty((T, d_out), dtype=Xd.dtype, device=DEV)
     dX = torch.empty((T, d_in), dtype=Xd.dtype, device=DEV)
     dW = torch.empty((d_out, d_in), dtype=torch.float32, device=DEV)
-    ws = torch.empty(max(1, cola.dense_workspace_bytes(d, 1)), dtype=torch.uint8, device=DEV)
-    cola.dense_fwd(d, Xd, Wd, Y)
+    ws = torch.empty(max(1, cola.dense_workspace_bytes(d, 0), cola.dense_workspace_bytes(d, 1)),
+                     dtype=torch.uint8, device=DEV)
+    cola.dense_fwd(d, Xd, Wd, Y, ws)
     cola.dense_bwd(d, dYd, Xd, Wd, dX, dW, ws)
     torch.cuda.synchronize()
     for got, ref, k in ((to_f64(Y), Yr, "Y"), (to_f64(dX), dXr, "dX"), (to_f64(dW), dWr, "dW")):
