@@ -18,7 +18,10 @@
  *   Z, H   [T][ldz]  (r used per row)         dA  [r][d_in]   fp32, contiguous
  *                                             dB  [d_out][r]  fp32, contiguous
  * A leading dimension of 0 means "contiguous" (ld = width).  Row padding
- * (ld > width) is never read or written.
+ * (ld > width) is never written.  It may be read up to the first multiple of
+ * 8 elements past the width (bf16) -- values read there only reach outputs
+ * that are discarded -- so a padded tensor must be allocated as rows x ld
+ * elements.
  *
  * Precision.  COLA_BF16: activations and weights are bf16, every product is
  * accumulated in fp32, Z/H/dZ are rounded to bf16 (round to nearest even)

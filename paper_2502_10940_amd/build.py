@@ -19,7 +19,7 @@ LIB = os.path.join(PKG, "libcola.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 
-SOURCES = ["gemm_bf16.hip", "gemm_f32.hip", "cola_abi.hip"]
+SOURCES = ["gemm_bf16.hip", "gemm_stream.hip", "gemm_wide.hip", "gemm_f32.hip", "cola_abi.hip"]
 FLAGS = ["-std=c++17", "-O3", "-fPIC", f"--offload-arch={ARCH}", "-I", INCLUDE, "-I", CSRC,
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
          "-Wall", "-Wno-unused-function"]

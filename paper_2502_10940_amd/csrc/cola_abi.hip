@@ -156,14 +156,13 @@ struct Split {
 
 // The split count S minimises a modelled time: rounds(S) * ceil(ktiles / S)
 // K-tile steps of about 2 us each, where rounds(S) = ceil(tiles * S / slots)
-// and slots is the number of workgroups the chip runs at once (256 CUs x 2
-// for the bf16 kernel) -- a split that leaves a few workgroups for a second
-// round costs a whole round -- plus writing and re-reading the S fp32
-// partials at about 4 TB/s.
-Split plan_split(bool bf16, int64_t M, int64_t N, int64_t K) {
+// and slots is the number of workgroups the chip runs at once -- a split that
+// leaves a few workgroups for a second round costs a whole round -- plus
+// writing and re-reading the S fp32 partials at about 4 TB/s.
+Split plan_split(bool bf16, int64_t M, int64_t N, int64_t K, int tag) {
     const int64_t bk = bf16 ? BF16_BK : F32_BK;
-    const int64_t tiles = gemm_tiles(bf16, M, N);
-    const int64_t slots = bf16 ? 512 : 1024;
+    const int64_t tiles = gemm_tiles(bf16, M, N, tag);
+    const int64_t slots = gemm_slots(bf16, M, N, tag);
     const int64_t ktiles = (K + bk - 1) / bk;
     if (ktiles < 1) return Split{1, bk};                       // empty batch: nothing to split
     const double step_us = 2.0;
@@ -252,8 +251,8 @@ BwdPlan plan_bwd(const Dims& x, bool recompute) {
     BwdPlan p;
     p.ldw = x.bf16 ? (x.r + 7) / 8 * 8 : (x.r + 3) / 4 * 4;
     const size_t zbytes = align256((size_t)x.T * (size_t)p.ldw * x.esize);
-    p.sa = plan_split(x.bf16, x.r, x.d_in, x.T);
-    p.sb = plan_split(x.bf16, x.d_out, x.r, x.T);
+    p.sa = plan_split(x.bf16, x.r, x.d_in, x.T, TAG_BWD_DA);
+    p.sb = plan_split(x.bf16, x.d_out, x.r, x.T, TAG_BWD_DB);
     p.off_dz = 0;
     p.off_h = zbytes;
     p.off_pa = p.off_h + (recompute ? zbytes : 0);
@@ -495,7 +494,7 @@ struct DensePlan {
 
 static DensePlan plan_dense(const Dims& x, int phase) {
     DensePlan p;
-    p.sp = plan_split(x.bf16, x.d_out, x.d_in, x.T);
+    p.sp = plan_split(x.bf16, x.d_out, x.d_in, x.T, TAG_DENSE_DW);
     p.parts = (phase == 1 && p.sp.splits > 1) ? align256((size_t)p.sp.splits * (size_t)(x.d_out * x.d_in) * 4) : 0;
     p.pw = plan_pack(x.bf16, x.d_out, x.d_in, p.parts);
     p.total = p.pw.off + p.pw.bytes;

@@ -27,8 +27,10 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
 
 // logistic sigmoid s(z) = 1 / (1 + e^{-z}); e^{-z} = inf for very negative z
 // gives s = 0 exactly, never NaN.
+// bf16 path: hardware exp and reciprocal (about 1 ulp each in fp32, far below
+// the bf16 rounding that follows).
 __device__ __forceinline__ float logistic_fast(float z) {
-    return 1.0f / (1.0f + __expf(-z));
+    return __builtin_amdgcn_rcpf(1.0f + __expf(-z));
 }
 __device__ __forceinline__ float logistic_exact(float z) {
     return 1.0f / (1.0f + expf(-z));

@@ -1,0 +1,331 @@
+// gemm_stream.hip -- the streaming bf16 MFMA GEMM: C[M][N] = sum_k P(m, k) Q(n, k)
+// with fp32 accumulation and the fused epilogues of epilogue.hpp.
+//
+// Design (CDNA4, wave64, two workgroups per CU):
+//  * 256 threads = 4 waves in a 2 x 2 grid; tile BM x 128 (BM = 256, or 128
+//    when M <= 128); each wave owns (BM/2) x 64 of C as 32x32x16 MFMA tiles
+//    (128 fp32 accumulators per lane at BM = 256), so two workgroups fit a
+//    CU and one's barriers, waits and epilogue overlap the other's MFMAs.
+//  * K advances in tiles of 32 through three LDS stages (72 KB at BM = 256):
+//    the loads run two K tiles ahead.  Interior tiles use the direct-to-LDS
+//    loads (global_load_lds_dwordx4): no staging registers and no LDS write
+//    instructions.
+//  * k-contiguous operands sit in LDS as [row][32 k], 64-byte rows, 16-byte
+//    chunks XOR-swizzled by (row >> 1) & 3, read with ds_read_b128;
+//    m-contiguous operands (token-reduction weight gradients, weights in the
+//    backward products) sit as in memory, [32 k][rows], chunks swizzled by
+//    2 (k & 3), read with the transposing ds_read_b64_tr_b16.  Both patterns
+//    are free of LDS bank conflicts.
+//  * Ragged edges: k-contiguous rows past the edge re-read the last row;
+//    m-contiguous chunks past the edge re-read the last chunk (the chunk
+//    holding the last column may run into the row's pitch padding, which the
+//    ABI allows).  Those values only reach outputs that are not stored.  The
+//    K tail and unaligned operands go through guarded register loads.
+#include "internal.hpp"
+#include "device_math.hpp"
+#include "epilogue.hpp"
+
+namespace cola {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef short s16x8 __attribute__((ext_vector_type(8)));
+typedef const __attribute__((address_space(1))) void* gptr_t;
+typedef __attribute__((address_space(3))) void* lptr_t;
+typedef __attribute__((address_space(3))) s16x4* lptr4_t;
+
+constexpr int BN = 128;
+constexpr int BK = 32;
+constexpr int NT = 256;
+constexpr int NSTAGE = 3;
+
+__device__ __forceinline__ bool aligned16(const void* p, int64_t ld) {
+    return ((reinterpret_cast<uintptr_t>(p) & 15u) == 0) && ((ld & 7) == 0);
+}
+
+__device__ __forceinline__ void dtl16(const void* g, char* lds) {
+    __builtin_amdgcn_global_load_lds((gptr_t)g, (lptr_t)lds, 16, 0, 0);
+}
+
+__device__ __forceinline__ uint4 load8_guarded(const uint16_t* p, int valid) {
+    uint32_t w[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        const uint32_t lo = (2 * e < valid) ? p[2 * e] : 0u;
+        const uint32_t hi = (2 * e + 1 < valid) ? p[2 * e + 1] : 0u;
+        w[e] = lo | (hi << 16);
+    }
+    return make_uint4(w[0], w[1], w[2], w[3]);
+}
+
+__device__ __forceinline__ void barrier_lds() {
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
+template <int R, int LAYOUT>
+struct STile;
+
+// ---- k-contiguous operand: LDS [R rows][32 k] (64-byte rows) ----
+template <int R>
+struct STile<R, KMAJ> {
+    static constexpr int BYTES = R * 64;
+    static constexpr int DTL_PER_WAVE = BYTES / 1024 / 4;   // 1 KB per wave instruction
+
+    __device__ static __forceinline__ int off(int row, int c) {
+        return row * 64 + ((c ^ ((row >> 1) & 3)) << 4);
+    }
+
+    // Wave w, instruction j fills LDS bytes [1024 (DPW w + j), +1024): rows
+    // 16 blk .. +16, lane l -> row + l/4, physical chunk l % 4.
+    __device__ static __forceinline__ void dtl(char* lds, const uint16_t* base, int64_t ld, int64_t row0,
+                                               int64_t rows, int64_t k0) {
+        const int wave = threadIdx.x >> 6;
+        const int lane = threadIdx.x & 63;
+#pragma unroll
+        for (int j = 0; j < DTL_PER_WAVE; ++j) {
+            const int blk = DTL_PER_WAVE * wave + j;
+            const int row = 16 * blk + (lane >> 2);
+            const int lc = (lane & 3) ^ ((row >> 1) & 3);
+            int64_t grow = row0 + row;
+            if (grow >= rows) grow = rows - 1;
+            dtl16(base + grow * ld + k0 + 8 * lc, lds + 1024 * blk);
+        }
+    }
+
+    // guarded: chunk id -> (row id / 4, chunk id % 4); R * 4 chunks
+    __device__ static __forceinline__ void load_store(char* lds, const uint16_t* base, int64_t ld, int64_t row0,
+                                                      int64_t rows, int64_t k0, int64_t kend, bool aligned) {
+#pragma unroll
+        for (int i = 0; i < R * 4 / NT; ++i) {
+            const int id = threadIdx.x + NT * i;
+            const int64_t row = row0 + (id >> 2);
+            const int64_t k = k0 + 8 * (id & 3);
+            uint4 v;
+            if (row < rows && k + 8 <= kend && aligned) {
+                v = *reinterpret_cast<const uint4*>(base + row * ld + k);
+            } else {
+                const int64_t valid = row < rows ? kend - k : 0;
+                v = load8_guarded(base + (row < rows ? row : 0) * ld + k,
+                                  (int)(valid < 0 ? 0 : (valid > 8 ? 8 : valid)));
+            }
+            *reinterpret_cast<uint4*>(lds + off(id >> 2, id & 3)) = v;
+        }
+    }
+
+    // 32 rows (row0 ..) x 16 k (16 s ..) fragment, s = 0 or 1
+    __device__ static __forceinline__ bf16x8 frag(const char* lds, int row0, int s, int lane) {
+        return *reinterpret_cast<const bf16x8*>(lds + off(row0 + (lane & 31), 2 * s + (lane >> 5)));
+    }
+};
+
+// ---- m-contiguous operand: LDS [32 k][R m] (2R-byte rows) ----
+template <int R>
+struct STile<R, MNMAJ> {
+    static constexpr int BYTES = 32 * R * 2;
+    static constexpr int DTL_PER_WAVE = BYTES / 1024 / 4;
+    static constexpr int CPR = R / 8;                         // 16-byte chunks per k row
+
+    __device__ static __forceinline__ int off(int k, int c) {
+        return k * (2 * R) + ((c ^ ((k & 3) << 1)) << 4);
+    }
+
+    __device__ static __forceinline__ void dtl(char* lds, const uint16_t* base, int64_t ld, int64_t m0,
+                                               int64_t rows, int64_t k0) {
+        const int wave = threadIdx.x >> 6;
+        const int lane = threadIdx.x & 63;
+        const int64_t mlast = ((rows - 1) >> 3) << 3;
+#pragma unroll
+        for (int j = 0; j < DTL_PER_WAVE; ++j) {
+            const int blk = DTL_PER_WAVE * wave + j;
+            const int k = (1024 / (2 * R)) * blk + lane / CPR;
+            const int lc = (lane % CPR) ^ ((k & 3) << 1);
+            int64_t m = m0 + 8 * lc;
+            if (m > mlast) m = mlast;
+            dtl16(base + (k0 + k) * ld + m, lds + 1024 * blk);
+        }
+    }
+
+    __device__ static __forceinline__ void load_store(char* lds, const uint16_t* base, int64_t ld, int64_t m0,
+                                                      int64_t rows, int64_t k0, int64_t kend, bool aligned) {
+#pragma unroll
+        for (int i = 0; i < 32 * CPR / NT; ++i) {
+            const int id = threadIdx.x + NT * i;
+            const int64_t k = k0 + id / CPR;
+            const int64_t m = m0 + 8 * (id % CPR);
+            uint4 v;
+            if (k < kend && m + 8 <= rows && aligned) {
+                v = *reinterpret_cast<const uint4*>(base + k * ld + m);
+            } else {
+                const int64_t valid = k < kend ? rows - m : 0;
+                v = load8_guarded(base + (k < kend ? k : 0) * ld + (valid > 0 ? m : 0),
+                                  (int)(valid < 0 ? 0 : (valid > 8 ? 8 : valid)));
+            }
+            *reinterpret_cast<uint4*>(lds + off(id / CPR, id % CPR)) = v;
+        }
+    }
+
+    // 32 m (m0 ..) x 16 k (16 s ..) fragment via two transposing reads: in
+    // each 16-lane group, lanes 4q..4q+3 point at k row q of a 4 x 16 block
+    // (four consecutive m each) and lane i receives column m0 + i.
+    __device__ static __forceinline__ bf16x8 frag(const char* lds, int m0, int s, int lane) {
+        const int g = lane >> 4;
+        const int i = lane & 15;
+        const int m = m0 + 16 * (g & 1) + 4 * (i & 3);
+        const int k = 16 * s + 8 * (g >> 1) + (i >> 2);
+        const int byte = (m & 7) * 2;
+        const int c = m >> 3;
+        const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lptr4_t)(lds + off(k, c) + byte));
+        const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lptr4_t)(lds + off(k + 4, c) + byte));
+        const s16x8 s8 = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+        return __builtin_bit_cast(bf16x8, s8);
+    }
+};
+
+template <int BM, int PL, int QL, int EPI, int TAG>
+__global__ __launch_bounds__(NT, 2) void gemm_stream_kernel(GemmArgs a) {
+    using TP = STile<BM, PL>;
+    using TQ = STile<BN, QL>;
+    constexpr int TM = BM / 64;
+    constexpr int TN = BN / 64;
+    constexpr int STAGE = TP::BYTES + TQ::BYTES;
+    constexpr int DTL_OPS = TP::DTL_PER_WAVE + TQ::DTL_PER_WAVE;    // per wave per K tile
+    static_assert(4 * 16 * (BN / 2 + 4) * 4 <= NSTAGE * STAGE, "epilogue staging does not fit");
+    __shared__ __attribute__((aligned(1024))) char smem[NSTAGE * STAGE];
+
+    // XCD-aware renumbering: hardware hands block b to XCD b % 8
+    const int64_t nb = gridDim.x;
+    int64_t b = blockIdx.x;
+    if ((nb & 7) == 0) b = (b & 7) * (nb >> 3) + (b >> 3);
+    const int64_t tiles_n = (a.N + BN - 1) / BN;
+    const int64_t tiles_m = (a.M + BM - 1) / BM;
+    const int64_t per_split = tiles_m * tiles_n;
+    const int split = (int)(b / per_split);
+    const int64_t rem = b - (int64_t)split * per_split;
+    const int64_t m0 = (rem / tiles_n) * BM;
+    const int64_t n0 = (rem % tiles_n) * BN;
+    const int64_t kbeg = (int64_t)split * a.k_chunk;
+    const int64_t kend = min(a.K, kbeg + a.k_chunk);
+    const int nk = (int)((kend - kbeg + BK - 1) / BK);
+
+    const uint16_t* P = reinterpret_cast<const uint16_t*>(a.p);
+    const uint16_t* Q = reinterpret_cast<const uint16_t*>(a.q);
+    const bool p_al = aligned16(a.p, a.ldp);
+    const bool q_al = aligned16(a.q, a.ldq);
+
+    const int tid = threadIdx.x;
+    const int wave = tid >> 6;
+    const int lane = tid & 63;
+    const int wm = wave >> 1;
+    const int wn = wave & 1;
+
+    f32x16 acc[TM][TN];
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.0f;
+
+    // K tile kt uses DTL when whole and aligned; returns whether it did.
+    auto issue = [&](int kt) -> bool {
+        char* As = smem + (kt % NSTAGE) * STAGE;
+        char* Bs = As + TP::BYTES;
+        const int64_t k0 = kbeg + (int64_t)kt * BK;
+        const bool kfull = k0 + BK <= kend;
+        const bool pd = kfull && p_al;
+        const bool qd = kfull && q_al;
+        if (pd) TP::dtl(As, P, a.ldp, m0, a.M, k0);
+        else TP::load_store(As, P, a.ldp, m0, a.M, k0, kend, p_al);
+        if (qd) TQ::dtl(Bs, Q, a.ldq, n0, a.N, k0);
+        else TQ::load_store(Bs, Q, a.ldq, n0, a.N, k0, kend, q_al);
+        return pd && qd;
+    };
+
+    if (nk > 0) {
+        issue(0);
+        bool next_dtl = nk > 1 ? issue(1) : false;   // was K tile kt+1 loaded by DTL only?
+        for (int kt = 0; kt < nk; ++kt) {
+            // K tile kt is complete once only K tile kt+1's loads can still be
+            // outstanding (vector-memory operations complete in issue order)
+            if (kt + 1 < nk && next_dtl) wait_vm<DTL_OPS>();
+            else wait_vm<0>();
+            barrier_lds();
+            bool nn = false;
+            if (kt + 2 < nk) nn = issue(kt + 2);     // into the stage read in iteration kt-1
+            const char* As = smem + (kt % NSTAGE) * STAGE;
+            const char* Bs = As + TP::BYTES;
+            bf16x8 fa[2][TM], fb[2][TN];
+#pragma unroll
+            for (int s = 0; s < 2; ++s) {
+#pragma unroll
+                for (int i = 0; i < TM; ++i) fa[s][i] = TP::frag(As, wm * (BM / 2) + 32 * i, s, lane);
+#pragma unroll
+                for (int j = 0; j < TN; ++j) fb[s][j] = TQ::frag(Bs, wn * (BN / 2) + 32 * j, s, lane);
+            }
+#pragma unroll
+            for (int s = 0; s < 2; ++s)
+#pragma unroll
+                for (int i = 0; i < TM; ++i)
+#pragma unroll
+                    for (int j = 0; j < TN; ++j)
+                        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[s][i], fb[s][j], acc[i][j],
+                                                                            0, 0, 0);
+            // order: first sub-step's reads, second sub-step's reads, then the
+            // MFMAs (the second reads land under the first MFMAs)
+            constexpr int RDP = TM * (PL == KMAJ ? 1 : 2);
+            constexpr int RDQ = TN * (QL == KMAJ ? 1 : 2);
+            __builtin_amdgcn_sched_group_barrier(0x100, RDP + RDQ, 0);
+            __builtin_amdgcn_sched_group_barrier(0x100, RDP + RDQ, 0);
+            __builtin_amdgcn_sched_group_barrier(0x008, 2 * TM * TN, 0);
+            next_dtl = nn;
+        }
+    }
+    wait_vm<0>();
+    barrier_lds();                                   // LDS is reused for the epilogue staging
+
+    float* stg = reinterpret_cast<float*>(smem) + wave * 16 * (BN / 2 + 4);
+    epi_slab<0, BM, BN, EPI>(a, acc, stg, m0, n0, wm, wn, lane, split);
+    if constexpr (TM > 1) epi_slab<1, BM, BN, EPI>(a, acc, stg, m0, n0, wm, wn, lane, split);
+    if constexpr (TM > 2) epi_slab<2, BM, BN, EPI>(a, acc, stg, m0, n0, wm, wn, lane, split);
+    if constexpr (TM > 3) epi_slab<3, BM, BN, EPI>(a, acc, stg, m0, n0, wm, wn, lane, split);
+}
+
+template <int BM, int PL, int QL, int EPI, int TAG>
+hipError_t launch_s(const GemmArgs& a, hipStream_t s) {
+    const int64_t tiles = ((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN) * (int64_t)a.splits;
+    if (tiles <= 0) return hipSuccess;
+    if (tiles > 0x7fffffffLL) return hipErrorInvalidConfiguration;
+    hipLaunchKernelGGL((gemm_stream_kernel<BM, PL, QL, EPI, TAG>), dim3((unsigned)tiles), dim3(NT), 0, s, a);
+    return hipGetLastError();
+}
+
+template <int PL, int QL, int EPI, int TAG>
+hipError_t launch_sl(const GemmArgs& a, hipStream_t s) {
+    if (a.p_layout != PL || a.q_layout != QL || a.epi != EPI) return hipErrorInvalidValue;
+    if (a.M > 128) return launch_s<256, PL, QL, EPI, TAG>(a, s);
+    return launch_s<128, PL, QL, EPI, TAG>(a, s);
+}
+
+}  // namespace
+
+hipError_t launch_gemm_stream(const GemmArgs& a, hipStream_t s) {
+    switch (a.tag) {
+        case TAG_FWD_Z: return launch_sl<KMAJ, KMAJ, EPI_Z_H, TAG_FWD_Z>(a, s);
+        case TAG_FWD_Y: return launch_sl<KMAJ, KMAJ, EPI_STORE, TAG_FWD_Y>(a, s);
+        case TAG_BWD_DZ: return launch_sl<KMAJ, MNMAJ, EPI_DZ, TAG_BWD_DZ>(a, s);
+        case TAG_BWD_DX: return launch_sl<KMAJ, MNMAJ, EPI_STORE, TAG_BWD_DX>(a, s);
+        case TAG_BWD_DA: return launch_sl<MNMAJ, MNMAJ, EPI_STORE_F32, TAG_BWD_DA>(a, s);
+        case TAG_BWD_DB: return launch_sl<MNMAJ, MNMAJ, EPI_STORE_F32, TAG_BWD_DB>(a, s);
+        case TAG_DENSE_FWD: return launch_sl<KMAJ, KMAJ, EPI_STORE, TAG_DENSE_FWD>(a, s);
+        case TAG_DENSE_DX: return launch_sl<KMAJ, MNMAJ, EPI_STORE, TAG_DENSE_DX>(a, s);
+        case TAG_DENSE_DW: return launch_sl<MNMAJ, MNMAJ, EPI_STORE_F32, TAG_DENSE_DW>(a, s);
+        default: return hipErrorNotSupported;
+    }
+}
+
+}  // namespace cola
