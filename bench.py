@@ -41,7 +41,7 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-dense", action="store_true")
     ap.add_argument("--no-cola-m", action="store_true")
-    ap.add_argument("--cpu-tokens", type=int, default=1024,
+    ap.add_argument("--cpu-tokens", type=int, default=8192,
                     help="tokens per projection in the oracle's CPU sample")
     ap.add_argument("--only", choices=["cola", "cola_m", "dense"], default=None,
                     help="run only one mode (profiling)")
@@ -102,13 +102,12 @@ def traffic_summary(fetch_csv, write_csv, copy_fetch_csv, copy_write_csv):
     for path, counter, scale, key in ((fetch_csv, "FETCH_SIZE", ff, "fetch"),
                                       (write_csv, "WRITE_SIZE", fw, "write")):
         for name, _, v in _pmc_rows(path, counter):
-            m = re.search(r"gemm_bf16_kernel<\d+, \d+, \d+, \d+, \d+, (\d+)>", name)
+            m = re.search(r"gemm_\w+_kernel<[^>]*, (\d+)>", name)
             if not m:
                 continue
             cls = KERNEL_TAGS.get(int(m.group(1)))
             per.setdefault(cls, {}).setdefault(key, []).append(v * 1024.0 * scale)
-    src = os.path.join(ROOT, "paper_2502_10940_amd", "csrc", "gemm_bf16.hip")
-    h = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
+    h = kernel_source_hash()
     out = {"_note": "HBM bytes per launch from rocprofv3 FETCH_SIZE + WRITE_SIZE, scaled by a "
                     "1 GiB copy (fetch factor %.4f, write factor %.4f)" % (ff, fw)}
     for cls, d in per.items():
@@ -231,6 +230,19 @@ def kernel_table(cola):
     return out
 
 
+def kernel_source_hash():
+    """sha256 (first 16 hex digits) over every HIP source of the library, so a
+    stored counter reading is dropped as soon as any kernel changes."""
+    import hashlib
+    d = os.path.join(ROOT, "paper_2502_10940_amd", "csrc")
+    h = hashlib.sha256()
+    for name in sorted(os.listdir(d)):
+        if name.endswith((".hip", ".hpp")):
+            h.update(name.encode())
+            h.update(open(os.path.join(d, name), "rb").read())
+    return h.hexdigest()[:16]
+
+
 def load_traffic(kernel):
     """HBM bytes per launch measured by rocprofv3 counters (profiles/traffic.json),
     or None when absent or taken on a different kernel source."""
@@ -244,10 +256,7 @@ def load_traffic(kernel):
     ent = rec.get(kernel)
     if not ent:
         return None
-    import hashlib
-    src = os.path.join(ROOT, "paper_2502_10940_amd", "csrc", "gemm_bf16.hip")
-    h = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
-    if ent.get("source_sha256_16") != h:
+    if ent.get("source_sha256_16") != kernel_source_hash():
         return None
     return ent.get("bytes_per_launch")
 
