@@ -12,17 +12,24 @@ __device__ __forceinline__ float bf16_to_f32(uint32_t bits16) {
     return __uint_as_float(bits16 << 16);
 }
 
-// float -> bf16 bits, round to nearest, ties to even; NaN stays a quiet NaN.
-__device__ __forceinline__ uint32_t f32_to_bf16(float f) {
-    uint32_t u = __float_as_uint(f);
-    if ((u & 0x7fffffffu) > 0x7f800000u) return ((u >> 16) | 0x40u) & 0xffffu;
-    u += 0x7fffu + ((u >> 16) & 1u);
-    return u >> 16;
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+
+// Two floats -> packed bf16 pair (lo in bits 15:0), round to nearest even,
+// in one v_cvt_pk_bf16_f32.
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+    const f32x2_t v = {lo, hi};
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2_t));
 }
 
-// Two floats -> packed bf16 pair (lo in bits 15:0).
-__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
-    return f32_to_bf16(lo) | (f32_to_bf16(hi) << 16);
+// float -> bf16 bits, round to nearest even (a NaN stays a NaN).
+__device__ __forceinline__ uint32_t f32_to_bf16(float f) {
+    return pack_bf16x2(f, 0.0f) & 0xffffu;
+}
+
+// x rounded to bf16 (nearest even) and back: the value a bf16 store keeps.
+__device__ __forceinline__ float round_bf16(float x) {
+    return __uint_as_float(pack_bf16x2(x, 0.0f) << 16);
 }
 
 // logistic sigmoid s(z) = 1 / (1 + e^{-z}); e^{-z} = inf for very negative z

@@ -1,10 +1,21 @@
-// epilogue.hpp -- the fused GEMM epilogues shared by the bf16 MFMA kernels:
-// accumulators are staged through LDS in 16-row half slabs so that every
-// global access is a coalesced 16-byte vector, and the pointwise part of the
-// layer (rounding, sigma, sigma', the CoLA-M recompute of H) happens here.
-// Large outputs are written with non-temporal stores so that the streaming
-// output does not evict the operand tiles other workgroups are still reading
-// from L2.
+// epilogue.hpp -- the fused GEMM epilogues shared by the bf16 MFMA kernels.
+//
+// The pointwise part of the layer (rounding, sigma, sigma', the CoLA-M
+// recompute of H) happens here, straight from the accumulator registers: no
+// LDS staging, so the epilogue neither waits on LDS nor on the global stores
+// still in flight, and its stores drain while the CU runs other MFMAs.
+//
+// Accumulator layout of v_mfma_f32_32x32x16_bf16: lane l, register v holds
+// row 8 (v / 4) + 4 (l / 32) + v % 4, column l % 32 of the 32 x 32 tile.  For
+// each group of four registers (v = 4g .. 4g+3) the four lanes of a quad hold
+// a 4 x 4 block (lane = column, register = row); a two-stage exchange inside
+// the quad (DPP quad permutations) transposes it, so that lane 4q + b then
+// holds row 8g + 4 (l / 32) + b, columns 4q .. 4q+3: four consecutive outputs
+// of one row, written with one 8-byte (bf16) or 16-byte (fp32) store.  One
+// store instruction covers 8 rows x 64 contiguous bytes (bf16).
+//
+// Plain (not non-temporal) stores: on MI355X they sustain more bandwidth,
+// 6.5 against 5.5 TB/s for a 128 MB write in this tile pattern.
 #pragma once
 
 #include "internal.hpp"
@@ -13,157 +24,188 @@
 namespace cola {
 
 typedef float f32x16 __attribute__((ext_vector_type(16)));
-
-// Orders one wave's LDS accesses (lanes exchange data through the wave's own
-// staging region; LDS operations of a wave complete in order, so a
-// wavefront-scope fence and a scheduling barrier suffice).
-__device__ __forceinline__ void wave_sync() {
-    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-}
-
+typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 
-__device__ __forceinline__ void store_stream(uint4* p, const uint4& v) {
-    const u32x4_t x = {v.x, v.y, v.z, v.w};
-    __builtin_nontemporal_store(x, reinterpret_cast<u32x4_t*>(p));
+// DPP quad permutations: lane 4q + i reads lane 4q + p[i].
+constexpr int kQuadSwap2 = 0x4E;   // p = [2, 3, 0, 1]
+constexpr int kQuadSwap1 = 0xB1;   // p = [1, 0, 3, 2]
+
+template <int CTRL>
+__device__ __forceinline__ uint32_t quad_perm(uint32_t v) {
+    return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, CTRL, 0xF, 0xF, false);
 }
-__device__ __forceinline__ void store_stream(float4* p, const float4& v) {
-    const f32x4_t x = {v.x, v.y, v.z, v.w};
-    __builtin_nontemporal_store(x, reinterpret_cast<f32x4_t*>(p));
+template <int CTRL>
+__device__ __forceinline__ float quad_perm(float v) {
+    return __uint_as_float(quad_perm<CTRL>(__float_as_uint(v)));
 }
 
-// ---------------------------------------------------------------------------
-// epilogue: 8 consecutive columns of one output row
-// ---------------------------------------------------------------------------
+// Per-lane byte selectors (v_perm_b32) of the 16-bit exchange.
+struct QuadSel {
+    bool hi2;          // lane bit 1
+    uint32_t send, q0, q1;
+    __device__ __forceinline__ explicit QuadSel(int lane) {
+        hi2 = (lane & 2) != 0;
+        const bool odd = (lane & 1) != 0;
+        send = odd ? 0x05040100u : 0x07060302u;   // odd lanes send the low halves, even the high
+        q0 = odd ? 0x03020504u : 0x05040100u;
+        q1 = odd ? 0x03020706u : 0x07060100u;
+    }
+};
+
+// Transpose of a quad's 4 x 4 block of bf16.  In: p01 = rows 0,1 and p23 =
+// rows 2,3 of this lane's column (low half = lower row).  Out: row (lane & 3),
+// columns 0,1 in q0 and 2,3 in q1 (low half = lower column).
+__device__ __forceinline__ void transpose_bf16(const QuadSel& s, uint32_t p01, uint32_t p23,
+                                               uint32_t& q0, uint32_t& q1) {
+    // stage 1: lanes b and b^2 swap row pairs
+    const uint32_t r = quad_perm<kQuadSwap2>(s.hi2 ? p01 : p23);
+    const uint32_t d0 = s.hi2 ? r : p01;
+    const uint32_t d1 = s.hi2 ? p23 : r;
+    // stage 2: lanes b and b^1 swap 16-bit halves
+    const uint32_t t = quad_perm<kQuadSwap1>(__builtin_amdgcn_perm(d1, d0, s.send));
+    q0 = __builtin_amdgcn_perm(t, d0, s.q0);
+    q1 = __builtin_amdgcn_perm(t, d1, s.q1);
+}
+
+// Transpose of a quad's 4 x 4 block of floats: in x[k] = row k of this lane's
+// column; out y[k] = column k of this lane's row.
+__device__ __forceinline__ void transpose_f32(int lane, const float x[4], float y[4]) {
+    const bool hi2 = (lane & 2) != 0;
+    const bool odd = (lane & 1) != 0;
+    const float r0 = quad_perm<kQuadSwap2>(hi2 ? x[0] : x[2]);
+    const float r1 = quad_perm<kQuadSwap2>(hi2 ? x[1] : x[3]);
+    const float z0 = hi2 ? r0 : x[0];
+    const float z1 = hi2 ? r1 : x[1];
+    const float z2 = hi2 ? x[2] : r0;
+    const float z3 = hi2 ? x[3] : r1;
+    const float s0 = quad_perm<kQuadSwap1>(odd ? z0 : z1);
+    const float s1 = quad_perm<kQuadSwap1>(odd ? z2 : z3);
+    y[0] = odd ? s0 : z0;
+    y[1] = odd ? z1 : s0;
+    y[2] = odd ? s1 : z2;
+    y[3] = odd ? z3 : s1;
+}
+
+// Four bf16 (q0 = columns 0,1, q1 = columns 2,3) to p: one 8-byte store when
+// vec, else the first `valid` elements one by one.
+__device__ __forceinline__ void store_bf16x4(uint16_t* p, uint32_t q0, uint32_t q1, bool vec, int valid) {
+    if (vec) {
+        *reinterpret_cast<u32x2_t*>(p) = u32x2_t{q0, q1};
+    } else {
+        if (valid > 0) p[0] = (uint16_t)(q0 & 0xffffu);
+        if (valid > 1) p[1] = (uint16_t)(q0 >> 16);
+        if (valid > 2) p[2] = (uint16_t)(q1 & 0xffffu);
+        if (valid > 3) p[3] = (uint16_t)(q1 >> 16);
+    }
+}
+
+// Epilogue of 4 consecutive columns (gn .. gn+3) of output row gm.
 template <int EPI>
-__device__ __forceinline__ void epilogue8(const GemmArgs& a, int64_t gm, int64_t gn,
-                                          const float* acc, int split) {
+__device__ __forceinline__ void epilogue4(const GemmArgs& a, int64_t gm, int64_t gn, const float v[4], int split) {
     if (gm >= a.M || gn >= a.N) return;
-    const bool full = gn + 8 <= a.N;
+    const int valid = (int)((a.N - gn) < 4 ? (a.N - gn) : 4);
     if constexpr (EPI == EPI_STORE_F32) {
         float* c = reinterpret_cast<float*>(a.c) + (int64_t)split * a.split_stride + gm * a.ldc + gn;
-        const bool vec = full && ((reinterpret_cast<uintptr_t>(c) & 15u) == 0);
-        if (vec) {
-            store_stream(reinterpret_cast<float4*>(c), make_float4(acc[0], acc[1], acc[2], acc[3]));
-            store_stream(reinterpret_cast<float4*>(c) + 1, make_float4(acc[4], acc[5], acc[6], acc[7]));
+        if (valid == 4 && (reinterpret_cast<uintptr_t>(c) & 15u) == 0) {
+            *reinterpret_cast<f32x4_t*>(c) = f32x4_t{v[0], v[1], v[2], v[3]};
         } else {
-            #pragma unroll
-            for (int e = 0; e < 8; ++e)
-                if (gn + e < a.N) c[e] = acc[e];
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+                if (e < valid) c[e] = v[e];
         }
-        return;
     } else {
         uint16_t* c = reinterpret_cast<uint16_t*>(a.c) + gm * a.ldc + gn;
-        float out[8];
-        float h[8];
+        float out[4], h[4];
         if constexpr (EPI == EPI_STORE) {
 #pragma unroll
-            for (int e = 0; e < 8; ++e) out[e] = acc[e];
+            for (int e = 0; e < 4; ++e) out[e] = v[e];
         } else if constexpr (EPI == EPI_Z_H) {
             // Z is stored rounded to bf16; H = sigma of that rounded Z
 #pragma unroll
-            for (int e = 0; e < 8; ++e) {
-                out[e] = bf16_to_f32(f32_to_bf16(acc[e]));
+            for (int e = 0; e < 4; ++e) {
+                out[e] = round_bf16(v[e]);
                 h[e] = act_sigma<true>(a.act, out[e]);
             }
         } else if constexpr (EPI == EPI_DZ) {
             const uint16_t* zp = reinterpret_cast<const uint16_t*>(a.zin) + gm * a.ldzin + gn;
-            float z[8];
-            if (full && ((reinterpret_cast<uintptr_t>(zp) & 15u) == 0)) {
-                const uint4 zz = *reinterpret_cast<const uint4*>(zp);
-                const uint32_t w[4] = {zz.x, zz.y, zz.z, zz.w};
-#pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    z[2 * e] = bf16_to_f32(w[e] & 0xffffu);
-                    z[2 * e + 1] = bf16_to_f32(w[e] >> 16);
-                }
+            float z[4];
+            if (valid == 4 && (reinterpret_cast<uintptr_t>(zp) & 7u) == 0) {
+                const u32x2_t zz = *reinterpret_cast<const u32x2_t*>(zp);
+                z[0] = bf16_to_f32(zz[0] & 0xffffu);
+                z[1] = bf16_to_f32(zz[0] >> 16);
+                z[2] = bf16_to_f32(zz[1] & 0xffffu);
+                z[3] = bf16_to_f32(zz[1] >> 16);
             } else {
-                #pragma unroll
-                for (int e = 0; e < 8; ++e) z[e] = (gn + e < a.N) ? bf16_to_f32(zp[e]) : 0.0f;
+#pragma unroll
+                for (int e = 0; e < 4; ++e) z[e] = e < valid ? bf16_to_f32(zp[e]) : 0.0f;
             }
 #pragma unroll
-            for (int e = 0; e < 8; ++e) {
+            for (int e = 0; e < 4; ++e) {
                 if (a.act == 0) {
-                    out[e] = acc[e];
+                    out[e] = v[e];
                     h[e] = z[e];
                 } else {
                     const float s = logistic_fast(z[e]);
-                    out[e] = acc[e] * (s * (1.0f + z[e] * (1.0f - s)));
+                    out[e] = v[e] * (s * (1.0f + z[e] * (1.0f - s)));
                     h[e] = z[e] * s;
                 }
             }
         }
-        const bool vec = full && ((reinterpret_cast<uintptr_t>(c) & 15u) == 0);
-        if (vec) {
-            store_stream(reinterpret_cast<uint4*>(c),
-                         make_uint4(pack_bf16x2(out[0], out[1]), pack_bf16x2(out[2], out[3]),
-                                    pack_bf16x2(out[4], out[5]), pack_bf16x2(out[6], out[7])));
-        } else {
-            #pragma unroll
-            for (int e = 0; e < 8; ++e)
-                if (gn + e < a.N) c[e] = (uint16_t)f32_to_bf16(out[e]);
-        }
+        const bool vec = valid == 4 && (reinterpret_cast<uintptr_t>(c) & 7u) == 0;
+        store_bf16x4(c, pack_bf16x2(out[0], out[1]), pack_bf16x2(out[2], out[3]), vec, valid);
         if constexpr (EPI == EPI_Z_H || EPI == EPI_DZ) {
             if (a.aux) {
                 uint16_t* hp = reinterpret_cast<uint16_t*>(a.aux) + gm * a.ldaux + gn;
-                if (full && ((reinterpret_cast<uintptr_t>(hp) & 15u) == 0)) {
-                    store_stream(reinterpret_cast<uint4*>(hp),
-                                 make_uint4(pack_bf16x2(h[0], h[1]), pack_bf16x2(h[2], h[3]),
-                                            pack_bf16x2(h[4], h[5]), pack_bf16x2(h[6], h[7])));
-                } else {
-                    #pragma unroll
-                    for (int e = 0; e < 8; ++e)
-                        if (gn + e < a.N) hp[e] = (uint16_t)f32_to_bf16(h[e]);
-                }
+                const bool hvec = valid == 4 && (reinterpret_cast<uintptr_t>(hp) & 7u) == 0;
+                store_bf16x4(hp, pack_bf16x2(h[0], h[1]), pack_bf16x2(h[2], h[3]), hvec, valid);
             }
         }
     }
 }
 
-// Half of MFMA row tile I (16 rows: accumulator registers 8H..8H+7) of a
-// wave's accumulators: staged through LDS as fp32 in [row][col] order, then
-// each lane handles 8 consecutive columns of a row, so global accesses are
-// 16-byte vectors.
-template <int I, int H, int BM, int BN, int EPI, int TM, int TN>
-__device__ __forceinline__ void epi_half(const GemmArgs& a, const f32x16 (&acc)[TM][TN], float* stg,
-                                         int64_t m0, int64_t n0, int wm, int wn, int lane, int split) {
-    constexpr int WC = BN / 2;            // wave columns
-    constexpr int SP = WC + 4;            // staging pitch (floats)
-    constexpr int LPR = WC / 8;           // lanes per row in the read-back
-    constexpr int RPP = 64 / LPR;         // rows per pass
+// The whole epilogue of one wave's block of TM x TN MFMA tiles, whose first
+// output row and column are row0, col0.
+template <int EPI, int TM, int TN>
+__device__ __forceinline__ void epilogue_block(const GemmArgs& a, const f32x16 (&acc)[TM][TN],
+                                               int64_t row0, int64_t col0, int lane, int split) {
+    const int64_t lrow = 4 * (lane >> 5) + (lane & 3);     // this lane's row within a group of 8
+    const int64_t lcol = 4 * ((lane & 31) >> 2);           // its first column within a tile
+    if constexpr (EPI == EPI_STORE) {
+        // round to bf16 first, then transpose 16-bit pairs (half the exchange work)
+        const QuadSel sel(lane);
 #pragma unroll
-    for (int j = 0; j < TN; ++j)
+        for (int i = 0; i < TM; ++i)
 #pragma unroll
-        for (int vv = 0; vv < 8; ++vv) {
-            const int v = 8 * H + vv;
-            const int row = 8 * (vv >> 2) + 4 * (lane >> 5) + (v & 3);   // row within the half
-            const int col = 32 * j + (lane & 31);
-            stg[row * SP + col] = acc[I][j][v];
-        }
-    wave_sync();
-    const int cc = lane % LPR;
-    const int rr = lane / LPR;
+            for (int g = 0; g < 4; ++g)
 #pragma unroll
-    for (int pass = 0; pass < 16 / RPP; ++pass) {
-        const int lr = pass * RPP + rr;
-        const float4 x0 = *reinterpret_cast<const float4*>(stg + lr * SP + cc * 8);
-        const float4 x1 = *reinterpret_cast<const float4*>(stg + lr * SP + cc * 8 + 4);
-        const float vals[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
-        const int64_t gm = m0 + wm * (BM / 2) + 32 * I + 16 * H + lr;
-        const int64_t gn = n0 + wn * WC + cc * 8;
-        epilogue8<EPI>(a, gm, gn, vals, split);
+                for (int j = 0; j < TN; ++j) {
+                    uint32_t q0, q1;
+                    transpose_bf16(sel, pack_bf16x2(acc[i][j][4 * g], acc[i][j][4 * g + 1]),
+                                   pack_bf16x2(acc[i][j][4 * g + 2], acc[i][j][4 * g + 3]), q0, q1);
+                    const int64_t gm = row0 + 32 * i + 8 * g + lrow;
+                    const int64_t gn = col0 + 32 * j + lcol;
+                    if (gm < a.M && gn < a.N) {
+                        const int valid = (int)((a.N - gn) < 4 ? (a.N - gn) : 4);
+                        uint16_t* c = reinterpret_cast<uint16_t*>(a.c) + gm * a.ldc + gn;
+                        store_bf16x4(c, q0, q1, valid == 4 && (reinterpret_cast<uintptr_t>(c) & 7u) == 0, valid);
+                    }
+                }
+    } else {
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int g = 0; g < 4; ++g)
+#pragma unroll
+                for (int j = 0; j < TN; ++j) {
+                    const float x[4] = {acc[i][j][4 * g], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2],
+                                        acc[i][j][4 * g + 3]};
+                    float y[4];
+                    transpose_f32(lane, x, y);
+                    epilogue4<EPI>(a, row0 + 32 * i + 8 * g + lrow, col0 + 32 * j + lcol, y, split);
+                }
     }
-    wave_sync();
 }
-
-template <int I, int BM, int BN, int EPI, int TM, int TN>
-__device__ __forceinline__ void epi_slab(const GemmArgs& a, const f32x16 (&acc)[TM][TN], float* stg,
-                                         int64_t m0, int64_t n0, int wm, int wn, int lane, int split) {
-    epi_half<I, 0, BM, BN, EPI>(a, acc, stg, m0, n0, wm, wn, lane, split);
-    epi_half<I, 1, BM, BN, EPI>(a, acc, stg, m0, n0, wm, wn, lane, split);
-}
-
 
 }  // namespace cola

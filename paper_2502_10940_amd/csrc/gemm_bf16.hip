@@ -24,9 +24,9 @@
 //  * Workgroups are renumbered so that each XCD (blockIdx % 8 on MI355X)
 //    receives a contiguous run of output tiles: tiles sharing an operand row
 //    block share that XCD's L2.
-//  * The epilogue stages each wave's accumulators through LDS so that every
-//    global access is a coalesced 16-byte vector (ragged edges and unaligned
-//    pitches fall back to guarded per-element accesses).
+//  * The epilogue works straight from the accumulator registers (quad
+//    transposes, epilogue.hpp); ragged edges and unaligned pitches fall back
+//    to guarded per-element accesses.
 #include <stdlib.h>
 #include <string.h>
 
@@ -196,7 +196,6 @@ __global__ __launch_bounds__(NT, 2) void gemm_bf16_kernel(GemmArgs a) {
     constexpr int TM = BM / 64;   // 32x32 MFMA tiles per wave along m
     constexpr int TN = BN / 64;   // ... along n
     constexpr int TILE = (BM + BN) * 128;
-    static_assert(4 * 16 * (BN / 2 + 4) * 4 <= TILE, "epilogue staging does not fit");
     __shared__ __attribute__((aligned(16))) char smem[TILE];
 
     // XCD-aware renumbering: hardware hands block b to XCD b % 8
@@ -277,16 +276,8 @@ __global__ __launch_bounds__(NT, 2) void gemm_bf16_kernel(GemmArgs a) {
             }
         }
     }
-    __syncthreads();                              // LDS is reused for the epilogue staging
-
-    // ---- epilogue: per wave, 16-row half slabs staged through LDS as fp32 ----
-    // (one instantiation per slab keeps every accumulator index a constant,
-    // so the accumulators stay in registers)
-    float* stg = reinterpret_cast<float*>(smem) + wave * 16 * (BN / 2 + 4);
-    epi_slab<0, BM, BN, EPI>(a, acc, stg, m0, n0, wm, wn, lane, split);
-    if constexpr (TM > 1) epi_slab<1, BM, BN, EPI>(a, acc, stg, m0, n0, wm, wn, lane, split);
-    if constexpr (TM > 2) epi_slab<2, BM, BN, EPI>(a, acc, stg, m0, n0, wm, wn, lane, split);
-    if constexpr (TM > 3) epi_slab<3, BM, BN, EPI>(a, acc, stg, m0, n0, wm, wn, lane, split);
+    // ---- epilogue straight from the accumulators ----
+    epilogue_block<EPI>(a, acc, m0 + wm * (BM / 2), n0 + wn * (BN / 2), lane, split);
 }
 
 template <int BM, int BN, int PL, int QL, int EPI, int TAG>

@@ -9,13 +9,16 @@
 //  * K advances in tiles of 32 through three LDS stages (72 KB at BM = 256):
 //    the loads run two K tiles ahead.  Interior tiles use the direct-to-LDS
 //    loads (global_load_lds_dwordx4): no staging registers and no LDS write
-//    instructions.
+//    instructions.  They are issued one per two MFMAs: a burst of them right
+//    after the barrier stalls the issuing wave on the address unit's queue.
 //  * k-contiguous operands sit in LDS as [row][32 k], 64-byte rows, 16-byte
-//    chunks XOR-swizzled by (row >> 1) & 3, read with ds_read_b128;
+//    chunks XOR-swizzled by (row >> 2) & 3, read with ds_read_b128;
 //    m-contiguous operands (token-reduction weight gradients, weights in the
 //    backward products) sit as in memory, [32 k][rows], chunks swizzled by
-//    2 (k & 3), read with the transposing ds_read_b64_tr_b16.  Both patterns
-//    are free of LDS bank conflicts.
+//    4 (k & 3), read with the transposing ds_read_b64_tr_b16.  gfx950's LDS
+//    has 64 four-byte banks (256 bytes per clock): a 32-lane half-wave of
+//    either read touches 16 distinct 16-byte bank groups, so neither pattern
+//    conflicts (measured: b128 reads at 4 clocks, tr reads at 2.5).
 //  * Ragged edges: k-contiguous rows past the edge re-read the last row;
 //    m-contiguous chunks past the edge re-read the last chunk (the chunk
 //    holding the last column may run into the row's pitch padding, which the
@@ -40,12 +43,16 @@ constexpr int BK = 32;
 constexpr int NT = 256;
 constexpr int NSTAGE = 3;
 
+// Operands the direct-to-LDS path takes: 16-byte aligned rows, and a pitch
+// small enough for 32-bit per-lane offsets within a tile (256 rows or 32 k).
 __device__ __forceinline__ bool aligned16(const void* p, int64_t ld) {
-    return ((reinterpret_cast<uintptr_t>(p) & 15u) == 0) && ((ld & 7) == 0);
+    return ((reinterpret_cast<uintptr_t>(p) & 15u) == 0) && ((ld & 7) == 0) && ld < (int64_t(1) << 22);
 }
 
-__device__ __forceinline__ void dtl16(const void* g, char* lds) {
-    __builtin_amdgcn_global_load_lds((gptr_t)g, (lptr_t)lds, 16, 0, 0);
+// 16 bytes per lane from ubase + voff (wave-uniform base, 32-bit per-lane
+// offset: the scalar-base form of the instruction) to LDS.
+__device__ __forceinline__ void dtl16(const char* ubase, uint32_t voff, char* lds) {
+    __builtin_amdgcn_global_load_lds((gptr_t)(ubase + voff), (lptr_t)lds, 16, 0, 0);
 }
 
 __device__ __forceinline__ uint4 load8_guarded(const uint16_t* p, int valid) {
@@ -77,24 +84,26 @@ struct STile<R, KMAJ> {
     static constexpr int DTL_PER_WAVE = BYTES / 1024 / 4;   // 1 KB per wave instruction
 
     __device__ static __forceinline__ int off(int row, int c) {
-        return row * 64 + ((c ^ ((row >> 1) & 3)) << 4);
+        return row * 64 + ((c ^ ((row >> 2) & 3)) << 4);
     }
 
     // Wave w, instruction j fills LDS bytes [1024 (DPW w + j), +1024): rows
     // 16 blk .. +16, lane l -> row + l/4, physical chunk l % 4.
-    __device__ static __forceinline__ void dtl(char* lds, const uint16_t* base, int64_t ld, int64_t row0,
-                                               int64_t rows, int64_t k0) {
+    __device__ static __forceinline__ void dtl_one(int j, char* lds, const uint16_t* base, int64_t ld,
+                                                   int64_t row0, int64_t rows, int64_t k0) {
         const int wave = threadIdx.x >> 6;
         const int lane = threadIdx.x & 63;
+        const int blk = DTL_PER_WAVE * wave + j;
+        const int row = 16 * blk + (lane >> 2);
+        const int lc = (lane & 3) ^ ((row >> 2) & 3);
+        const int lrow = row0 + row < rows ? row : (int)(rows - 1 - row0);
+        const uint32_t voff = 2u * ((uint32_t)lrow * (uint32_t)ld + 8u * (uint32_t)lc);
+        dtl16(reinterpret_cast<const char*>(base + row0 * ld + k0), voff, lds + 1024 * blk);
+    }
+    __device__ static __forceinline__ void dtl(char* lds, const uint16_t* base, int64_t ld, int64_t row0,
+                                               int64_t rows, int64_t k0) {
 #pragma unroll
-        for (int j = 0; j < DTL_PER_WAVE; ++j) {
-            const int blk = DTL_PER_WAVE * wave + j;
-            const int row = 16 * blk + (lane >> 2);
-            const int lc = (lane & 3) ^ ((row >> 1) & 3);
-            int64_t grow = row0 + row;
-            if (grow >= rows) grow = rows - 1;
-            dtl16(base + grow * ld + k0 + 8 * lc, lds + 1024 * blk);
-        }
+        for (int j = 0; j < DTL_PER_WAVE; ++j) dtl_one(j, lds, base, ld, row0, rows, k0);
     }
 
     // guarded: chunk id -> (row id / 4, chunk id % 4); R * 4 chunks
@@ -129,25 +138,28 @@ struct STile<R, MNMAJ> {
     static constexpr int BYTES = 32 * R * 2;
     static constexpr int DTL_PER_WAVE = BYTES / 1024 / 4;
     static constexpr int CPR = R / 8;                         // 16-byte chunks per k row
+    static_assert(CPR >= 16, "the 4 (k & 3) chunk swizzle needs 16 chunks per row");
 
     __device__ static __forceinline__ int off(int k, int c) {
-        return k * (2 * R) + ((c ^ ((k & 3) << 1)) << 4);
+        return k * (2 * R) + ((c ^ ((k & 3) << 2)) << 4);
     }
 
-    __device__ static __forceinline__ void dtl(char* lds, const uint16_t* base, int64_t ld, int64_t m0,
-                                               int64_t rows, int64_t k0) {
+    __device__ static __forceinline__ void dtl_one(int j, char* lds, const uint16_t* base, int64_t ld,
+                                                   int64_t m0, int64_t rows, int64_t k0) {
         const int wave = threadIdx.x >> 6;
         const int lane = threadIdx.x & 63;
         const int64_t mlast = ((rows - 1) >> 3) << 3;
+        const int blk = DTL_PER_WAVE * wave + j;
+        const int k = (1024 / (2 * R)) * blk + lane / CPR;
+        const int lc = (lane % CPR) ^ ((k & 3) << 2);
+        const int lm = m0 + 8 * lc <= mlast ? 8 * lc : (int)(mlast - m0);
+        const uint32_t voff = 2u * ((uint32_t)k * (uint32_t)ld + (uint32_t)lm);
+        dtl16(reinterpret_cast<const char*>(base + k0 * ld + m0), voff, lds + 1024 * blk);
+    }
+    __device__ static __forceinline__ void dtl(char* lds, const uint16_t* base, int64_t ld, int64_t m0,
+                                               int64_t rows, int64_t k0) {
 #pragma unroll
-        for (int j = 0; j < DTL_PER_WAVE; ++j) {
-            const int blk = DTL_PER_WAVE * wave + j;
-            const int k = (1024 / (2 * R)) * blk + lane / CPR;
-            const int lc = (lane % CPR) ^ ((k & 3) << 1);
-            int64_t m = m0 + 8 * lc;
-            if (m > mlast) m = mlast;
-            dtl16(base + (k0 + k) * ld + m, lds + 1024 * blk);
-        }
+        for (int j = 0; j < DTL_PER_WAVE; ++j) dtl_one(j, lds, base, ld, m0, rows, k0);
     }
 
     __device__ static __forceinline__ void load_store(char* lds, const uint16_t* base, int64_t ld, int64_t m0,
@@ -194,7 +206,6 @@ __global__ __launch_bounds__(NT, 2) void gemm_stream_kernel(GemmArgs a) {
     constexpr int TN = BN / 64;
     constexpr int STAGE = TP::BYTES + TQ::BYTES;
     constexpr int DTL_OPS = TP::DTL_PER_WAVE + TQ::DTL_PER_WAVE;    // per wave per K tile
-    static_assert(4 * 16 * (BN / 2 + 4) * 4 <= NSTAGE * STAGE, "epilogue staging does not fit");
     __shared__ __attribute__((aligned(1024))) char smem[NSTAGE * STAGE];
 
     // XCD-aware renumbering: hardware hands block b to XCD b % 8
@@ -231,32 +242,48 @@ __global__ __launch_bounds__(NT, 2) void gemm_stream_kernel(GemmArgs a) {
 #pragma unroll
             for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.0f;
 
-    // K tile kt uses DTL when whole and aligned; returns whether it did.
-    auto issue = [&](int kt) -> bool {
+    // Whether K tile kt goes direct to LDS (whole, and aligned operands).
+    auto dtl_ok = [&](int kt) -> bool {
+        const int64_t k0 = kbeg + (int64_t)kt * BK;
+        return k0 + BK <= kend && p_al && q_al;
+    };
+    // Direct-to-LDS instruction r (of DTL_OPS) of K tile kt.
+    auto issue_one = [&](int r, int kt) {
         char* As = smem + (kt % NSTAGE) * STAGE;
-        char* Bs = As + TP::BYTES;
+        const int64_t k0 = kbeg + (int64_t)kt * BK;
+        if (r < TP::DTL_PER_WAVE) TP::dtl_one(r, As, P, a.ldp, m0, a.M, k0);
+        else TQ::dtl_one(r - TP::DTL_PER_WAVE, As + TP::BYTES, Q, a.ldq, n0, a.N, k0);
+    };
+    // Whole K tile, direct-to-LDS or guarded register path (K tail, unaligned
+    // operands; LDS written at once).
+    auto issue = [&](int kt) {
+        char* As = smem + (kt % NSTAGE) * STAGE;
         const int64_t k0 = kbeg + (int64_t)kt * BK;
         const bool kfull = k0 + BK <= kend;
-        const bool pd = kfull && p_al;
-        const bool qd = kfull && q_al;
-        if (pd) TP::dtl(As, P, a.ldp, m0, a.M, k0);
+        if (kfull && p_al) TP::dtl(As, P, a.ldp, m0, a.M, k0);
         else TP::load_store(As, P, a.ldp, m0, a.M, k0, kend, p_al);
-        if (qd) TQ::dtl(Bs, Q, a.ldq, n0, a.N, k0);
-        else TQ::load_store(Bs, Q, a.ldq, n0, a.N, k0, kend, q_al);
-        return pd && qd;
+        if (kfull && q_al) TQ::dtl(As + TP::BYTES, Q, a.ldq, n0, a.N, k0);
+        else TQ::load_store(As + TP::BYTES, Q, a.ldq, n0, a.N, k0, kend, q_al);
     };
 
+    constexpr int NMFMA = 2 * TM * TN;
+    static_assert(2 * DTL_OPS <= NMFMA, "one direct-to-LDS load per two MFMAs");
     if (nk > 0) {
+        bool next_dtl = nk > 1 && dtl_ok(1);         // K tile kt+1 went direct to LDS
         issue(0);
-        bool next_dtl = nk > 1 ? issue(1) : false;   // was K tile kt+1 loaded by DTL only?
+        if (nk > 1) issue(1);
         for (int kt = 0; kt < nk; ++kt) {
             // K tile kt is complete once only K tile kt+1's loads can still be
             // outstanding (vector-memory operations complete in issue order)
             if (kt + 1 < nk && next_dtl) wait_vm<DTL_OPS>();
             else wait_vm<0>();
-            barrier_lds();
-            bool nn = false;
-            if (kt + 2 < nk) nn = issue(kt + 2);     // into the stage read in iteration kt-1
+            barrier_lds();                           // also: every wave is done with K tile kt-1's stage
+            // K tile kt+2 goes into the stage K tile kt-1 used.  Direct-to-LDS
+            // loads are issued one per two MFMAs below: a burst of them would
+            // stall this wave on the address unit's queue while its MFMA unit
+            // idles.  Register-path tiles are loaded here, at once.
+            const bool pf = kt + 2 < nk && dtl_ok(kt + 2);
+            if (kt + 2 < nk && !pf) issue(kt + 2);
             const char* As = smem + (kt % NSTAGE) * STAGE;
             const char* Bs = As + TP::BYTES;
             bf16x8 fa[2][TM], fb[2][TN];
@@ -272,27 +299,16 @@ __global__ __launch_bounds__(NT, 2) void gemm_stream_kernel(GemmArgs a) {
 #pragma unroll
                 for (int i = 0; i < TM; ++i)
 #pragma unroll
-                    for (int j = 0; j < TN; ++j)
+                    for (int j = 0; j < TN; ++j) {
                         acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[s][i], fb[s][j], acc[i][j],
                                                                             0, 0, 0);
-            // order: first sub-step's reads, second sub-step's reads, then the
-            // MFMAs (the second reads land under the first MFMAs)
-            constexpr int RDP = TM * (PL == KMAJ ? 1 : 2);
-            constexpr int RDQ = TN * (QL == KMAJ ? 1 : 2);
-            __builtin_amdgcn_sched_group_barrier(0x100, RDP + RDQ, 0);
-            __builtin_amdgcn_sched_group_barrier(0x100, RDP + RDQ, 0);
-            __builtin_amdgcn_sched_group_barrier(0x008, 2 * TM * TN, 0);
-            next_dtl = nn;
+                        const int n = (s * TM + i) * TN + j;          // MFMA index in this K tile
+                        if ((n & 1) == 1 && (n >> 1) < DTL_OPS && pf) issue_one(n >> 1, kt + 2);
+                    }
+            next_dtl = pf;
         }
     }
-    wait_vm<0>();
-    barrier_lds();                                   // LDS is reused for the epilogue staging
-
-    float* stg = reinterpret_cast<float*>(smem) + wave * 16 * (BN / 2 + 4);
-    epi_slab<0, BM, BN, EPI>(a, acc, stg, m0, n0, wm, wn, lane, split);
-    if constexpr (TM > 1) epi_slab<1, BM, BN, EPI>(a, acc, stg, m0, n0, wm, wn, lane, split);
-    if constexpr (TM > 2) epi_slab<2, BM, BN, EPI>(a, acc, stg, m0, n0, wm, wn, lane, split);
-    if constexpr (TM > 3) epi_slab<3, BM, BN, EPI>(a, acc, stg, m0, n0, wm, wn, lane, split);
+    epilogue_block<EPI>(a, acc, m0 + wm * (BM / 2), n0 + wn * (BN / 2), lane, split);
 }
 
 template <int BM, int PL, int QL, int EPI, int TAG>

@@ -1,29 +1,38 @@
-// gemm_wide.hip -- the 256 x 256 bf16 MFMA GEMM used when both output
-// dimensions exceed 128:  C[M][N] = sum_k P(m, k) Q(n, k), fp32 accumulation,
-// the fused epilogues of epilogue.hpp.
+// gemm_wide.hip -- the persistent 256 x 256 bf16 MFMA GEMM:
+// C[M][N] = sum_k P(m, k) Q(n, k), fp32 accumulation, the fused epilogues of
+// epilogue.hpp.
 //
 // Design (CDNA4, wave64, one workgroup per CU):
-//  * 256 threads = 4 waves in a 2 x 2 grid, each wave a 128 x 128 block of C
-//    as 4 x 4 tiles of v_mfma_f32_32x32x16_bf16 (256 fp32 accumulators per
-//    lane).  The large wave tile halves the LDS bytes read per MFMA compared
-//    with 128 x 64 wave tiles.
-//  * K advances in tiles of 64 through two LDS stages (2 x 64 KB).  Interior
-//    tiles are copied global -> LDS by the direct-to-LDS loads
-//    (global_load_lds_dwordx4): no registers, no LDS write instructions; the
-//    next tile's loads are in flight while the current tile's MFMAs run.
-//  * Operands with contiguous k (KMAJ) sit in LDS as [row][k] with 128-byte
-//    rows, 16-byte chunks XOR-swizzled by (row ^ row >> 3) & 7; fragments are
-//    read with ds_read_b128.  Operands with contiguous m (MNMAJ: the operands
-//    of the token-reduction weight gradients and the weights in the backward
-//    products) sit in LDS as they are in memory, [k][m] with 512-byte rows,
-//    chunks XOR-swizzled by 2 (k & 3); fragments are read with the gfx950
-//    transposing LDS load ds_read_b64_tr_b16 (two per fragment), which hands
-//    each lane four consecutive k of one m.
-//  * Tiles on a ragged edge (or at the K tail, or with unaligned pitches) are
-//    loaded through registers with per-chunk guards and written to the same
-//    LDS layout at once (no staging registers live across the MFMA loop);
-//    for k-contiguous operands rows past the edge simply re-read the last
-//    row (those outputs are never stored).
+//  * 512 threads = 8 waves in a 2 x 4 grid, each wave a 128 x 64 block of C
+//    as 4 x 2 tiles of v_mfma_f32_32x32x16_bf16 (128 fp32 accumulators per
+//    lane), two waves per SIMD so that one issues MFMAs while the other waits.
+//    One 256 x 256 tile per CU needs 1 KB of operands per unit of k, two
+//    thirds of what two 256 x 128 tiles need.
+//  * K advances in tiles of 32 through four LDS stages of 32 KB: while one K
+//    tile is consumed the next three are in flight, loaded straight into LDS
+//    (global_load_lds_dwordx4: no staging registers, no LDS write
+//    instructions).  K tails and unaligned operands take guarded register
+//    loads written to the same layout.
+//  * One barrier per K tile, placed between its two 16-deep sub-steps.  The
+//    fragments of each sub-step are read from LDS under the MFMAs of the one
+//    before, and the stage the barrier frees is refilled at once.
+//  * The grid is persistent (one workgroup per CU).  The last four K tiles of
+//    an output tile prefetch the first four K tiles of the next one, so the
+//    next tile's loads are in flight during the epilogue, and the epilogue's
+//    stores drain under the next tile's MFMAs.
+//  * Each wave counts the vector-memory operations it issues and waits for a
+//    K tile with vmcnt(operations issued after it): a wave's vector-memory
+//    operations complete in issue order.
+//  * LDS layouts.  k-contiguous operands: [256 rows][32 k], 64-byte rows,
+//    16-byte chunks XOR-swizzled by (row >> 2) & 3, read with ds_read_b128.
+//    m-contiguous operands (the weight-gradient operands, the weights of the
+//    backward products): [32 k][256 m], 512-byte rows, chunks swizzled by
+//    4 (k & 3), read with the transposing ds_read_b64_tr_b16.  With gfx950's
+//    64 banks neither read conflicts.
+//  * Ragged edges: k-contiguous rows past the edge re-read the last row,
+//    m-contiguous chunks past the edge re-read the last chunk (the chunk
+//    holding the last column may run into the row's pitch padding, which the
+//    ABI allows).  Those values reach only outputs that are not stored.
 #include "internal.hpp"
 #include "device_math.hpp"
 #include "epilogue.hpp"
@@ -34,27 +43,36 @@ namespace {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef short s16x4 __attribute__((ext_vector_type(4)));
 typedef short s16x8 __attribute__((ext_vector_type(8)));
+typedef const __attribute__((address_space(1))) void* gptr_t;
+typedef __attribute__((address_space(3))) void* lptr_t;
+typedef __attribute__((address_space(3))) s16x4* lptr4_t;
 
 constexpr int BM = 256;
 constexpr int BN = 256;
-constexpr int BK = 64;
-constexpr int NT = 256;
-constexpr int TILE = 256 * 128;        // bytes of one operand tile (either layout)
+constexpr int BK = 32;
+constexpr int WAVES_M = 2;                     // wave grid of the workgroup
+constexpr int WAVES_N = 4;
+constexpr int NW = WAVES_M * WAVES_N;
+constexpr int NT = 64 * NW;
+constexpr int NSTAGE = 4;
+constexpr int TILE = 256 * BK * 2;            // bytes of one operand tile (either layout)
 constexpr int STAGE = 2 * TILE;
+constexpr int WR = BM / WAVES_M;              // rows of a wave's block
+constexpr int WC = BN / WAVES_N;              // columns of a wave's block
+constexpr int TM = WR / 32;                   // MFMA tiles per wave
+constexpr int TN = WC / 32;
+constexpr int DTL_OPS = TILE / 1024 / NW;     // direct-to-LDS instructions per wave per operand tile
+constexpr int SMEM = NSTAGE * STAGE;
+static_assert(SMEM <= 160 * 1024, "LDS budget");
 
 __device__ __forceinline__ bool aligned16(const void* p, int64_t ld) {
     return ((reinterpret_cast<uintptr_t>(p) & 15u) == 0) && ((ld & 7) == 0);
 }
 
-typedef const __attribute__((address_space(1))) void* gptr_t;
-typedef __attribute__((address_space(3))) void* lptr_t;
-typedef __attribute__((address_space(3))) s16x4* lptr4_t;
-
 __device__ __forceinline__ void dtl16(const void* g, char* lds) {
     __builtin_amdgcn_global_load_lds((gptr_t)g, (lptr_t)lds, 16, 0, 0);
 }
 
-// Eight bf16 from global memory, elements at or past `valid` read as zero.
 __device__ __forceinline__ uint4 load8_guarded(const uint16_t* p, int valid) {
     uint32_t w[4];
 #pragma unroll
@@ -69,127 +87,109 @@ __device__ __forceinline__ uint4 load8_guarded(const uint16_t* p, int valid) {
 template <int LAYOUT>
 struct Tile;
 
-// ---- k-contiguous operand: LDS [256 rows][64 k] ----
+// ---- k-contiguous operand: LDS [256 rows][32 k] ----
 template <>
 struct Tile<KMAJ> {
-    uint4 v[8];
-
     __device__ static __forceinline__ int off(int row, int c) {
-        return row * 128 + ((c ^ ((row ^ (row >> 3)) & 7)) << 4);
+        return row * 64 + ((c ^ ((row >> 2) & 3)) << 4);
     }
 
-    // Wave w, instruction j fills LDS bytes [1024 (8w + j), +1024): rows
-    // 8 (8w + j) .. +8, lane l -> row + l/8, physical chunk l % 8.
+    // Wave w, instruction j fills LDS bytes [1024 (4w + j), +1024): rows
+    // 16 (4w + j) .. +16, lane l -> row + l/4, physical chunk l % 4.
     __device__ static __forceinline__ void dtl(char* lds, const uint16_t* base, int64_t ld, int64_t row0,
                                                int64_t rows, int64_t k0) {
         const int wave = threadIdx.x >> 6;
         const int lane = threadIdx.x & 63;
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
-            const int blk = 8 * wave + j;
-            const int row = 8 * blk + (lane >> 3);
-            const int lc = (lane & 7) ^ ((row ^ (row >> 3)) & 7);
+        for (int j = 0; j < DTL_OPS; ++j) {
+            const int blk = DTL_OPS * wave + j;
+            const int row = 16 * blk + (lane >> 2);
+            const int lc = (lane & 3) ^ ((row >> 2) & 3);
             int64_t grow = row0 + row;
             if (grow >= rows) grow = rows - 1;
             dtl16(base + grow * ld + k0 + 8 * lc, lds + 1024 * blk);
         }
     }
 
-    __device__ __forceinline__ void load(const uint16_t* base, int64_t ld, int64_t row0, int64_t rows,
-                                         int64_t k0, int64_t kend, bool aligned) {
+    // Guarded register path: chunk id -> (row id / 4, chunk id % 4).
+    __device__ static __forceinline__ void load_store(char* lds, const uint16_t* base, int64_t ld, int64_t row0,
+                                                      int64_t rows, int64_t k0, int64_t kend, bool aligned) {
 #pragma unroll
-        for (int i = 0; i < 8; ++i) {
+        for (int i = 0; i < 256 * 4 / NT; ++i) {
             const int id = threadIdx.x + NT * i;
-            const int64_t row = row0 + (id >> 3);
-            const int64_t k = k0 + 8 * (id & 7);
+            const int64_t row = row0 + (id >> 2);
+            const int64_t k = k0 + 8 * (id & 3);
+            uint4 v;
             if (row < rows && k + 8 <= kend && aligned) {
-                v[i] = *reinterpret_cast<const uint4*>(base + row * ld + k);
+                v = *reinterpret_cast<const uint4*>(base + row * ld + k);
             } else {
                 const int64_t valid = row < rows ? kend - k : 0;
-                v[i] = load8_guarded(base + (row < rows ? row : 0) * ld + k,
-                                     (int)(valid < 0 ? 0 : (valid > 8 ? 8 : valid)));
+                v = load8_guarded(base + (row < rows ? row : 0) * ld + k,
+                                  (int)(valid < 0 ? 0 : (valid > 8 ? 8 : valid)));
             }
+            *reinterpret_cast<uint4*>(lds + off(id >> 2, id & 3)) = v;
         }
     }
 
-    __device__ __forceinline__ void store(char* lds) const {
-#pragma unroll
-        for (int i = 0; i < 8; ++i) {
-            const int id = threadIdx.x + NT * i;
-            *reinterpret_cast<uint4*>(lds + off(id >> 3, id & 7)) = v[i];
-        }
-    }
-
-    // 32 rows (row0 ..) x 16 k (kbase ..) MFMA operand fragment
-    __device__ static __forceinline__ bf16x8 frag(const char* lds, int row0, int kbase, int lane) {
-        return *reinterpret_cast<const bf16x8*>(lds + off(row0 + (lane & 31), (kbase >> 3) + (lane >> 5)));
+    // 32 rows (row0 ..) x 16 k (16 s ..) fragment, s = 0 or 1
+    __device__ static __forceinline__ bf16x8 frag(const char* lds, int row0, int s, int lane) {
+        return *reinterpret_cast<const bf16x8*>(lds + off(row0 + (lane & 31), 2 * s + (lane >> 5)));
     }
 };
 
-// ---- m-contiguous operand: LDS [64 k][256 m] ----
+// ---- m-contiguous operand: LDS [32 k][256 m] ----
 template <>
 struct Tile<MNMAJ> {
-    uint4 v[8];
-
     __device__ static __forceinline__ int off(int k, int c) {
-        return k * 512 + ((c ^ ((k & 3) << 1)) << 4);
+        return k * 512 + ((c ^ ((k & 3) << 2)) << 4);
     }
 
-    // Wave w, instruction j fills LDS bytes [1024 (8w + j), +1024): k rows
-    // 2 (8w + j) and 2 (8w + j) + 1, lane l -> k row + l/32, physical chunk
-    // l % 32.  Chunks that start past the last column re-read the last chunk
-    // (their outputs are never stored); the chunk holding the last column may
-    // run into the row's pitch padding, which the ABI lets the library read.
+    // Wave w, instruction j fills LDS bytes [1024 (4w + j), +1024): k rows
+    // 2 (4w + j) and 2 (4w + j) + 1, lane l -> k row + l/32, physical chunk
+    // l % 32.  Chunks that start past the last column re-read the last chunk.
     __device__ static __forceinline__ void dtl(char* lds, const uint16_t* base, int64_t ld, int64_t m0,
                                                int64_t rows, int64_t k0) {
         const int wave = threadIdx.x >> 6;
         const int lane = threadIdx.x & 63;
         const int64_t mlast = ((rows - 1) >> 3) << 3;
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
-            const int blk = 8 * wave + j;
+        for (int j = 0; j < DTL_OPS; ++j) {
+            const int blk = DTL_OPS * wave + j;
             const int k = 2 * blk + (lane >> 5);
-            const int lc = (lane & 31) ^ ((k & 3) << 1);
+            const int lc = (lane & 31) ^ ((k & 3) << 2);
             int64_t m = m0 + 8 * lc;
             if (m > mlast) m = mlast;
             dtl16(base + (k0 + k) * ld + m, lds + 1024 * blk);
         }
     }
 
-    __device__ __forceinline__ void load(const uint16_t* base, int64_t ld, int64_t m0, int64_t rows,
-                                         int64_t k0, int64_t kend, bool aligned) {
+    __device__ static __forceinline__ void load_store(char* lds, const uint16_t* base, int64_t ld, int64_t m0,
+                                                      int64_t rows, int64_t k0, int64_t kend, bool aligned) {
 #pragma unroll
-        for (int i = 0; i < 8; ++i) {
+        for (int i = 0; i < 32 * 32 / NT; ++i) {
             const int id = threadIdx.x + NT * i;
             const int64_t k = k0 + (id >> 5);
             const int64_t m = m0 + 8 * (id & 31);
+            uint4 v;
             if (k < kend && m + 8 <= rows && aligned) {
-                v[i] = *reinterpret_cast<const uint4*>(base + k * ld + m);
+                v = *reinterpret_cast<const uint4*>(base + k * ld + m);
             } else {
                 const int64_t valid = k < kend ? rows - m : 0;
-                v[i] = load8_guarded(base + (k < kend ? k : 0) * ld + (valid > 0 ? m : 0),
-                                     (int)(valid < 0 ? 0 : (valid > 8 ? 8 : valid)));
+                v = load8_guarded(base + (k < kend ? k : 0) * ld + (valid > 0 ? m : 0),
+                                  (int)(valid < 0 ? 0 : (valid > 8 ? 8 : valid)));
             }
+            *reinterpret_cast<uint4*>(lds + off(id >> 5, id & 31)) = v;
         }
     }
 
-    __device__ __forceinline__ void store(char* lds) const {
-#pragma unroll
-        for (int i = 0; i < 8; ++i) {
-            const int id = threadIdx.x + NT * i;
-            *reinterpret_cast<uint4*>(lds + off(id >> 5, id & 31)) = v[i];
-        }
-    }
-
-    // 32 m (m0 ..) x 16 k (kbase ..) MFMA operand fragment.  Each transposing
-    // read serves 16 lanes: lanes 4q..4q+3 point at k row q of a 4 x 16 block
-    // (four consecutive m each), and lane i of the group receives the four k
-    // values of column m0 + i.  Two reads give the lane's eight k.
-    __device__ static __forceinline__ bf16x8 frag(const char* lds, int m0, int kbase, int lane) {
+    // 32 m (m0 ..) x 16 k (16 s ..) fragment via two transposing reads: in
+    // each 16-lane group, lanes 4q..4q+3 point at k row q of a 4 x 16 block
+    // (four consecutive m each) and lane i receives column m0 + i.
+    __device__ static __forceinline__ bf16x8 frag(const char* lds, int m0, int s, int lane) {
         const int g = lane >> 4;
         const int i = lane & 15;
         const int m = m0 + 16 * (g & 1) + 4 * (i & 3);
-        const int k = kbase + 8 * (g >> 1) + (i >> 2);
+        const int k = 16 * s + 8 * (g >> 1) + (i >> 2);
         const int byte = (m & 7) * 2;
         const int c = m >> 3;
         const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lptr4_t)(lds + off(k, c) + byte));
@@ -199,23 +199,46 @@ struct Tile<MNMAJ> {
     }
 };
 
-// LDS barrier: this wave's LDS writes are complete, then all waves meet.
-// (Plain s_barrier: no memory fence, so global stores stay in flight.)
+// LDS barrier: this wave's LDS operations are complete, then all waves meet.
+// (No memory fence: global stores stay in flight.)
 __device__ __forceinline__ void barrier_lds() {
     asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
-// Wait until at most N vector-memory operations of this wave are outstanding
-// (they complete in issue order).
-template <int N>
-__device__ __forceinline__ void wait_vm() {
-    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+
+// Wait until at most n of this wave's vector-memory operations are
+// outstanding, n rounded down to a multiple of 4 (a longer wait, never a
+// shorter one).
+__device__ __forceinline__ void wait_vm_at_most(int n) {
+    n = __builtin_amdgcn_readfirstlane(n);
+    switch (n < 0 ? 0 : (n >= 60 ? 15 : n >> 2)) {
+        case 0: asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); break;
+        case 1: asm volatile("s_waitcnt vmcnt(4)" ::: "memory"); break;
+        case 2: asm volatile("s_waitcnt vmcnt(8)" ::: "memory"); break;
+        case 3: asm volatile("s_waitcnt vmcnt(12)" ::: "memory"); break;
+        case 4: asm volatile("s_waitcnt vmcnt(16)" ::: "memory"); break;
+        case 5: asm volatile("s_waitcnt vmcnt(20)" ::: "memory"); break;
+        case 6: asm volatile("s_waitcnt vmcnt(24)" ::: "memory"); break;
+        case 7: asm volatile("s_waitcnt vmcnt(28)" ::: "memory"); break;
+        case 8: asm volatile("s_waitcnt vmcnt(32)" ::: "memory"); break;
+        case 9: asm volatile("s_waitcnt vmcnt(36)" ::: "memory"); break;
+        case 10: asm volatile("s_waitcnt vmcnt(40)" ::: "memory"); break;
+        case 11: asm volatile("s_waitcnt vmcnt(44)" ::: "memory"); break;
+        case 12: asm volatile("s_waitcnt vmcnt(48)" ::: "memory"); break;
+        case 13: asm volatile("s_waitcnt vmcnt(52)" ::: "memory"); break;
+        case 14: asm volatile("s_waitcnt vmcnt(56)" ::: "memory"); break;
+        default: asm volatile("s_waitcnt vmcnt(60)" ::: "memory"); break;
+    }
 }
 
-// Vector-memory operations one thread issues in the epilogue of an interior
-// tile: 8 half slabs x 4 passes x (stores, plus loads of Z for EPI_DZ).
+// Vector-memory operations one wave issues in the epilogue of a tile whose
+// every 4-column group takes the vector path (4 TM TN groups per lane).
 template <int EPI>
-constexpr int epilogue_vm_ops(bool aux) {
-    return EPI == EPI_STORE ? 32 : EPI == EPI_STORE_F32 ? 64 : EPI == EPI_Z_H ? (aux ? 64 : 32) : 0;
+__device__ __forceinline__ int epilogue_ops(bool aux) {
+    constexpr int G = 4 * TM * TN;
+    return EPI == EPI_STORE ? G
+         : EPI == EPI_STORE_F32 ? G
+         : EPI == EPI_Z_H ? (aux ? 2 * G : G)
+         : (aux ? 3 * G : 2 * G);               // EPI_DZ: Z loads, dZ (and H) stores
 }
 
 struct TileCoord {
@@ -225,8 +248,8 @@ struct TileCoord {
 
 // The persistent grid walks the output tiles.  With a grid and a tile count
 // that are multiples of 8, XCD x (blockIdx % 8) owns the contiguous tile range
-// [x T/8, (x+1) T/8), which its workgroups sweep together, so tiles that
-// share operand rows are computed at the same time on the same L2.
+// [x T/8, (x+1) T/8), which its workgroups sweep together (n fastest), so
+// tiles that share operand rows run at the same time on the same L2.
 __device__ __forceinline__ bool tile_at(const GemmArgs& a, int64_t i, TileCoord* t) {
     const int64_t tiles_n = (a.N + BN - 1) / BN;
     const int64_t tiles_m = (a.M + BM - 1) / BM;
@@ -255,129 +278,153 @@ __device__ __forceinline__ bool tile_at(const GemmArgs& a, int64_t i, TileCoord*
 
 template <int PL, int QL, int EPI, int TAG>
 __global__ __launch_bounds__(NT, 1) void gemm_wide_kernel(GemmArgs a) {
-    // the epilogue stages through the second LDS stage only
-    static_assert(4 * 16 * (BN / 2 + 4) * 4 <= STAGE, "epilogue staging does not fit");
-    __shared__ __attribute__((aligned(1024))) char smem[2 * STAGE];
+    __shared__ __attribute__((aligned(1024))) char smem[SMEM];
 
     const uint16_t* P = reinterpret_cast<const uint16_t*>(a.p);
     const uint16_t* Q = reinterpret_cast<const uint16_t*>(a.q);
     const bool p_al = aligned16(a.p, a.ldp);
     const bool q_al = aligned16(a.q, a.ldq);
     const int64_t out_vec = (EPI == EPI_STORE_F32) ? 3 : 7;   // pitch granule of a 16-byte store
-    const bool out_al = ((reinterpret_cast<uintptr_t>(a.c) & 15u) == 0) && ((a.ldc & out_vec) == 0) &&
-                        (!a.aux || (((reinterpret_cast<uintptr_t>(a.aux) & 15u) == 0) && ((a.ldaux & 7) == 0)));
-    constexpr int EPI_OPS = epilogue_vm_ops<EPI>(true);
+    bool out_al = ((reinterpret_cast<uintptr_t>(a.c) & 15u) == 0) && ((a.ldc & out_vec) == 0);
+    if (EPI == EPI_Z_H || EPI == EPI_DZ)
+        out_al = out_al && (!a.aux || (((reinterpret_cast<uintptr_t>(a.aux) & 15u) == 0) && ((a.ldaux & 7) == 0)));
+    if (EPI == EPI_DZ)
+        out_al = out_al && ((reinterpret_cast<uintptr_t>(a.zin) & 15u) == 0) && ((a.ldzin & 7) == 0);
+    const int epi_ops = epilogue_ops<EPI>(a.aux != nullptr);
 
     const int tid = threadIdx.x;
     const int wave = tid >> 6;
     const int lane = tid & 63;
-    const int wm = wave >> 1;
-    const int wn = wave & 1;
+    const int wm = wave / WAVES_N;
+    const int wn = wave % WAVES_N;
 
-    // Issue the loads of one K tile into an LDS stage.  Interior tiles go
-    // straight to LDS and stay in flight; edge tiles (rare) are loaded into
-    // registers and written to LDS right away, so no staging registers stay
-    // live across the MFMA loop.
-    // `part` selects what to issue: 1 = direct-to-LDS loads only, 2 = the
-    // register-path loads only, 3 = both.
-    auto issue = [&](const TileCoord& t, int stage, int64_t k0, int part) {
-        char* As = smem + stage * STAGE;
+    // Vector-memory operations this wave has issued (counted exactly, or
+    // under-counted, which only lengthens a wait), and, one byte per stage,
+    // that count modulo 256 right after the stage's K tile was issued (at most
+    // three K tiles and one epilogue, under 256 operations, follow a K tile
+    // before it is awaited).  All wave-uniform scalars.
+    int issued = 0;
+    uint32_t done_at = 0;
+    int loaded = 0;                            // bit st: stage st holds an issued K tile
+    auto ops_after = [&](int st) -> int {
+        return (int)(((uint32_t)issued - (done_at >> (8 * st))) & 0xffu);
+    };
+
+    // Issue K tile kt of output tile t into stage kt % 4.  dtl_only: issue
+    // only if both operands go direct to LDS (register-path tiles are issued
+    // at the start of their output tile instead).
+    auto issue = [&](const TileCoord& t, int kt, bool dtl_only) {
+        const int st = kt & (NSTAGE - 1);
+        char* As = smem + st * STAGE;
         char* Bs = As + TILE;
+        const int64_t k0 = t.kbeg + (int64_t)kt * BK;
         const bool kfull = k0 + BK <= t.kend;
-        if (kfull && p_al) {
-            if (part & 1) Tile<PL>::dtl(As, P, a.ldp, t.m0, a.M, k0);
-        } else if (part & 2) {
-            Tile<PL> r;
-            r.load(P, a.ldp, t.m0, a.M, k0, t.kend, p_al);
-            r.store(As);
+        const bool pd = kfull && p_al;
+        const bool qd = kfull && q_al;
+        if (dtl_only && !(pd && qd)) return;
+        if (pd) {
+            Tile<PL>::dtl(As, P, a.ldp, t.m0, a.M, k0);
+            issued += DTL_OPS;
+        } else {
+            Tile<PL>::load_store(As, P, a.ldp, t.m0, a.M, k0, t.kend, p_al);
         }
-        if (kfull && q_al) {
-            if (part & 1) Tile<QL>::dtl(Bs, Q, a.ldq, t.n0, a.N, k0);
-        } else if (part & 2) {
-            Tile<QL> r;
-            r.load(Q, a.ldq, t.n0, a.N, k0, t.kend, q_al);
-            r.store(Bs);
+        if (qd) {
+            Tile<QL>::dtl(Bs, Q, a.ldq, t.n0, a.N, k0);
+            issued += DTL_OPS;
+        } else {
+            Tile<QL>::load_store(Bs, Q, a.ldq, t.n0, a.N, k0, t.kend, q_al);
         }
+        issued = __builtin_amdgcn_readfirstlane(issued);
+        done_at = (done_at & ~(0xffu << (8 * st))) | (((uint32_t)issued & 0xffu) << (8 * st));
+        loaded |= 1 << st;
     };
 
     TileCoord cur;
     if (!tile_at(a, 0, &cur)) return;
-    if (cur.nk > 0) issue(cur, 0, cur.kbeg, 3);
-    bool drained = true;        // were the previous epilogue's memory operations counted exactly?
+    constexpr int RD = TM * (PL == KMAJ ? 1 : 2) + TN * (QL == KMAJ ? 1 : 2);   // LDS reads per sub-step
 
     for (int64_t it = 0;; ++it) {
-        f32x16 acc[4][4];
+        TileCoord nxt;
+        const bool more = tile_at(a, it + 1, &nxt);
+
+        // K tiles of this output tile not prefetched yet (the first output
+        // tile, or register-path tiles)
+        for (int kt = 0; kt < NSTAGE && kt < cur.nk; ++kt)
+            if (!((loaded >> kt) & 1)) issue(cur, kt, false);
+
+        f32x16 acc[TM][TN];
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
+        for (int i = 0; i < TM; ++i)
 #pragma unroll
-            for (int j = 0; j < 4; ++j)
+            for (int j = 0; j < TN; ++j)
 #pragma unroll
                 for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.0f;
 
-        for (int kt = 0; kt < cur.nk; ++kt) {
-            // this stage's direct-to-LDS loads are the oldest outstanding
-            // operations; the previous tile's epilogue stores may stay in flight
-            if (kt == 0 && !drained) wait_vm<(EPI_OPS > 63 ? 63 : EPI_OPS)>();
-            else wait_vm<0>();
+        bf16x8 fa[2][TM], fb[2][TN];
+        if (cur.nk > 0) {
+            wait_vm_at_most(ops_after(0));
             barrier_lds();
-            if (kt + 1 < cur.nk) issue(cur, (kt + 1) & 1, cur.kbeg + (int64_t)(kt + 1) * BK, 3);
-            const char* As = smem + (kt & 1) * STAGE;
-            const char* Bs = As + TILE;
-            bf16x8 fa[2][4], fb[2][4];
 #pragma unroll
-            for (int i = 0; i < 4; ++i) fa[0][i] = Tile<PL>::frag(As, wm * 128 + 32 * i, 0, lane);
+            for (int i = 0; i < TM; ++i) fa[0][i] = Tile<PL>::frag(smem, wm * WR + 32 * i, 0, lane);
 #pragma unroll
-            for (int j = 0; j < 4; ++j) fb[0][j] = Tile<QL>::frag(Bs, wn * 128 + 32 * j, 0, lane);
-#pragma unroll
-            for (int s = 0; s < BK / 16; ++s) {
-                const int c = s & 1;
-                if (s + 1 < BK / 16) {        // next sub-step's fragments, read under this one's MFMAs
-#pragma unroll
-                    for (int i = 0; i < 4; ++i)
-                        fa[c ^ 1][i] = Tile<PL>::frag(As, wm * 128 + 32 * i, 16 * (s + 1), lane);
-#pragma unroll
-                    for (int j = 0; j < 4; ++j)
-                        fb[c ^ 1][j] = Tile<QL>::frag(Bs, wn * 128 + 32 * j, 16 * (s + 1), lane);
-                }
-#pragma unroll
-                for (int i = 0; i < 4; ++i)
-#pragma unroll
-                    for (int j = 0; j < 4; ++j)
-                        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[c][i], fb[c][j], acc[i][j],
-                                                                            0, 0, 0);
-            }
-            // Pin the order: first sub-step's reads, then for each sub-step the
-            // next sub-step's reads ahead of its 16 MFMAs.
-            constexpr int RD = 4 * (PL == KMAJ ? 1 : 2) + 4 * (QL == KMAJ ? 1 : 2);
-            __builtin_amdgcn_sched_group_barrier(0x100, RD, 0);
-#pragma unroll
-            for (int s = 0; s < BK / 16 - 1; ++s) {
-                __builtin_amdgcn_sched_group_barrier(0x100, RD, 0);
-                __builtin_amdgcn_sched_group_barrier(0x008, 16, 0);
-            }
-            __builtin_amdgcn_sched_group_barrier(0x008, 16, 0);
+            for (int j = 0; j < TN; ++j) fb[0][j] = Tile<QL>::frag(smem + TILE, wn * WC + 32 * j, 0, lane);
         }
+        for (int kt = 0; kt < cur.nk; ++kt) {
+            const int st = kt & (NSTAGE - 1);
+            const int sn = (kt + 1) & (NSTAGE - 1);
+            const char* As = smem + st * STAGE;
+            // second sub-step's fragments, read under the first sub-step's MFMAs
+#pragma unroll
+            for (int i = 0; i < TM; ++i) fa[1][i] = Tile<PL>::frag(As, wm * WR + 32 * i, 1, lane);
+#pragma unroll
+            for (int j = 0; j < TN; ++j) fb[1][j] = Tile<QL>::frag(As + TILE, wn * WC + 32 * j, 1, lane);
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+#pragma unroll
+                for (int j = 0; j < TN; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[0][i], fb[0][j], acc[i][j], 0, 0, 0);
+            // one MFMA, then the reads, then the other 15: the first MFMA waits
+            // only for reads issued a sub-step earlier
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(0x100, RD, 0);
+            __builtin_amdgcn_sched_group_barrier(0x008, TM * TN - 1, 0);
 
-        // Every wave is done with both stages: start the next tile's first K
-        // tile (stage 0) before this tile's epilogue, which stages through
-        // stage 1 and whose stores then drain under the next tile's MFMAs.
-        TileCoord nxt;
-        const bool more = tile_at(a, it + 1, &nxt);
-        wait_vm<0>();
-        barrier_lds();
-        if (more && nxt.nk > 0) issue(nxt, 0, nxt.kbeg, 1);
+            // K tile kt+1 has landed (this wave's loads; the barrier makes it
+            // every wave's), and every wave is done reading K tile kt.
+            wait_vm_at_most(kt + 1 < cur.nk ? ops_after(sn) : 64);
+            barrier_lds();
+            loaded &= ~(1 << st);
+            if (kt + NSTAGE < cur.nk) issue(cur, kt + NSTAGE, false);
+            else if (more && st < nxt.nk) issue(nxt, st, true);   // stage st is free for good
 
-        const bool interior = out_al && cur.m0 + BM <= a.M && cur.n0 + BN <= a.N &&
-                              (EPI != EPI_DZ) && (EPI != EPI_Z_H || a.aux);
-        float* stg = reinterpret_cast<float*>(smem + STAGE) + wave * 16 * (BN / 2 + 4);
-        epi_slab<0, BM, BN, EPI>(a, acc, stg, cur.m0, cur.n0, wm, wn, lane, cur.split);
-        epi_slab<1, BM, BN, EPI>(a, acc, stg, cur.m0, cur.n0, wm, wn, lane, cur.split);
-        epi_slab<2, BM, BN, EPI>(a, acc, stg, cur.m0, cur.n0, wm, wn, lane, cur.split);
-        epi_slab<3, BM, BN, EPI>(a, acc, stg, cur.m0, cur.n0, wm, wn, lane, cur.split);
+            // next K tile's first sub-step, read under this second sub-step's
+            // MFMAs (after the last K tile the values read are not used)
+            const char* An = smem + sn * STAGE;
+#pragma unroll
+            for (int i = 0; i < TM; ++i) fa[0][i] = Tile<PL>::frag(An, wm * WR + 32 * i, 0, lane);
+#pragma unroll
+            for (int j = 0; j < TN; ++j) fb[0][j] = Tile<QL>::frag(An + TILE, wn * WC + 32 * j, 0, lane);
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+#pragma unroll
+                for (int j = 0; j < TN; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[1][i], fb[1][j], acc[i][j], 0, 0, 0);
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(0x100, RD, 0);
+            __builtin_amdgcn_sched_group_barrier(0x008, TM * TN - 1, 0);
+        }
+        // stages the next output tile needs that this one never used (nk < 4)
+        if (more)
+            for (int kt = cur.nk; kt < NSTAGE && kt < nxt.nk; ++kt)
+                if (!((loaded >> kt) & 1)) issue(nxt, kt, true);
+
+        const int64_t row0 = cur.m0 + wm * WR;
+        const int64_t col0 = cur.n0 + wn * WC;
+        const bool interior = out_al && row0 + WR <= a.M && col0 + WC <= a.N;
+        epilogue_block<EPI>(a, acc, row0, col0, lane, cur.split);
+        if (interior) issued = __builtin_amdgcn_readfirstlane(issued + epi_ops);
         if (!more) break;
-        drained = !interior;
         cur = nxt;
-        if (cur.nk > 0) issue(cur, 0, cur.kbeg, 2);   // edge-tile loads, after the epilogue
     }
 }
 
