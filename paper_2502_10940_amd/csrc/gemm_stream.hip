@@ -39,9 +39,7 @@ typedef __attribute__((address_space(3))) void* lptr_t;
 typedef __attribute__((address_space(3))) s16x4* lptr4_t;
 
 constexpr int BN = 128;
-constexpr int BK = 32;
 constexpr int NT = 256;
-constexpr int NSTAGE = 3;
 
 // Operands the direct-to-LDS path takes: 16-byte aligned rows, and a pitch
 // small enough for 32-bit per-lane offsets within a tile (256 rows or 32 k).
@@ -74,28 +72,35 @@ __device__ __forceinline__ void wait_vm() {
     asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
 }
 
-template <int R, int LAYOUT>
+template <int R, int LAYOUT, int BK>
 struct STile;
 
-// ---- k-contiguous operand: LDS [R rows][32 k] (64-byte rows) ----
-template <int R>
-struct STile<R, KMAJ> {
-    static constexpr int BYTES = R * 64;
+// ---- k-contiguous operand: LDS [R rows][BK k] (2 BK-byte rows) ----
+// CR = BK / 8 16-byte chunks per row; chunk c of row r sits at chunk
+// c ^ ((r / (16 / CR)) % CR): for BK = 32 (64-byte rows) (r >> 2) & 3, for
+// BK = 16 (32-byte rows) (r >> 3) & 1.  Either way the 32 rows a half-wave
+// reads cover all 64 banks once.
+template <int R, int BK>
+struct STile<R, KMAJ, BK> {
+    static constexpr int CR = BK / 8;
+    static constexpr int RPI = 64 / CR;                      // rows per 1 KB instruction
+    static constexpr int BYTES = R * BK * 2;
     static constexpr int DTL_PER_WAVE = BYTES / 1024 / 4;   // 1 KB per wave instruction
+    static_assert(CR == 2 || CR == 4, "BK of 16 or 32");
 
     __device__ static __forceinline__ int off(int row, int c) {
-        return row * 64 + ((c ^ ((row >> 2) & 3)) << 4);
+        return row * (2 * BK) + ((c ^ ((row / (16 / CR)) & (CR - 1))) << 4);
     }
 
     // Wave w, instruction j fills LDS bytes [1024 (DPW w + j), +1024): rows
-    // 16 blk .. +16, lane l -> row + l/4, physical chunk l % 4.
+    // RPI blk .. +RPI, lane l -> row + l / CR, physical chunk l % CR.
     __device__ static __forceinline__ void dtl_one(int j, char* lds, const uint16_t* base, int64_t ld,
                                                    int64_t row0, int64_t rows, int64_t k0) {
         const int wave = threadIdx.x >> 6;
         const int lane = threadIdx.x & 63;
         const int blk = DTL_PER_WAVE * wave + j;
-        const int row = 16 * blk + (lane >> 2);
-        const int lc = (lane & 3) ^ ((row >> 2) & 3);
+        const int row = RPI * blk + lane / CR;
+        const int lc = (lane % CR) ^ ((row / (16 / CR)) & (CR - 1));
         const int lrow = row0 + row < rows ? row : (int)(rows - 1 - row0);
         const uint32_t voff = 2u * ((uint32_t)lrow * (uint32_t)ld + 8u * (uint32_t)lc);
         dtl16(reinterpret_cast<const char*>(base + row0 * ld + k0), voff, lds + 1024 * blk);
@@ -106,14 +111,14 @@ struct STile<R, KMAJ> {
         for (int j = 0; j < DTL_PER_WAVE; ++j) dtl_one(j, lds, base, ld, row0, rows, k0);
     }
 
-    // guarded: chunk id -> (row id / 4, chunk id % 4); R * 4 chunks
+    // guarded: chunk id -> (row id / CR, chunk id % CR); R * CR chunks
     __device__ static __forceinline__ void load_store(char* lds, const uint16_t* base, int64_t ld, int64_t row0,
                                                       int64_t rows, int64_t k0, int64_t kend, bool aligned) {
 #pragma unroll
-        for (int i = 0; i < R * 4 / NT; ++i) {
+        for (int i = 0; i < R * CR / NT; ++i) {
             const int id = threadIdx.x + NT * i;
-            const int64_t row = row0 + (id >> 2);
-            const int64_t k = k0 + 8 * (id & 3);
+            const int64_t row = row0 + id / CR;
+            const int64_t k = k0 + 8 * (id % CR);
             uint4 v;
             if (row < rows && k + 8 <= kend && aligned) {
                 v = *reinterpret_cast<const uint4*>(base + row * ld + k);
@@ -122,20 +127,20 @@ struct STile<R, KMAJ> {
                 v = load8_guarded(base + (row < rows ? row : 0) * ld + k,
                                   (int)(valid < 0 ? 0 : (valid > 8 ? 8 : valid)));
             }
-            *reinterpret_cast<uint4*>(lds + off(id >> 2, id & 3)) = v;
+            *reinterpret_cast<uint4*>(lds + off(id / CR, id % CR)) = v;
         }
     }
 
-    // 32 rows (row0 ..) x 16 k (16 s ..) fragment, s = 0 or 1
+    // 32 rows (row0 ..) x 16 k (16 s ..) fragment
     __device__ static __forceinline__ bf16x8 frag(const char* lds, int row0, int s, int lane) {
         return *reinterpret_cast<const bf16x8*>(lds + off(row0 + (lane & 31), 2 * s + (lane >> 5)));
     }
 };
 
-// ---- m-contiguous operand: LDS [32 k][R m] (2R-byte rows) ----
-template <int R>
-struct STile<R, MNMAJ> {
-    static constexpr int BYTES = 32 * R * 2;
+// ---- m-contiguous operand: LDS [BK k][R m] (2R-byte rows) ----
+template <int R, int BK>
+struct STile<R, MNMAJ, BK> {
+    static constexpr int BYTES = BK * R * 2;
     static constexpr int DTL_PER_WAVE = BYTES / 1024 / 4;
     static constexpr int CPR = R / 8;                         // 16-byte chunks per k row
     static_assert(CPR >= 16, "the 4 (k & 3) chunk swizzle needs 16 chunks per row");
@@ -144,6 +149,9 @@ struct STile<R, MNMAJ> {
         return k * (2 * R) + ((c ^ ((k & 3) << 2)) << 4);
     }
 
+    // Wave w, instruction j fills LDS bytes [1024 (DPW w + j), +1024): k rows
+    // (1024 / 2R) blk .., lane l -> k row + l / CPR, physical chunk l % CPR.
+    // Chunks that start past the last column re-read the last chunk.
     __device__ static __forceinline__ void dtl_one(int j, char* lds, const uint16_t* base, int64_t ld,
                                                    int64_t m0, int64_t rows, int64_t k0) {
         const int wave = threadIdx.x >> 6;
@@ -165,7 +173,7 @@ struct STile<R, MNMAJ> {
     __device__ static __forceinline__ void load_store(char* lds, const uint16_t* base, int64_t ld, int64_t m0,
                                                       int64_t rows, int64_t k0, int64_t kend, bool aligned) {
 #pragma unroll
-        for (int i = 0; i < 32 * CPR / NT; ++i) {
+        for (int i = 0; i < BK * CPR / NT; ++i) {
             const int id = threadIdx.x + NT * i;
             const int64_t k = k0 + id / CPR;
             const int64_t m = m0 + 8 * (id % CPR);
@@ -198,14 +206,31 @@ struct STile<R, MNMAJ> {
     }
 };
 
-template <int BM, int PL, int QL, int EPI, int TAG>
+// Wait until at most DTL_OPS * c vector-memory operations are outstanding.
+template <int DTL_OPS, int D>
+__device__ __forceinline__ void wait_tiles(int c) {
+    static_assert(D <= 5, "up to four K tiles after the awaited one");
+    switch (c) {
+        case 0: wait_vm<0>(); break;
+        case 1: wait_vm<DTL_OPS>(); break;
+        case 2: if constexpr (D > 2) wait_vm<2 * DTL_OPS>(); else wait_vm<DTL_OPS>(); break;
+        case 3: if constexpr (D > 3) wait_vm<3 * DTL_OPS>(); else wait_vm<DTL_OPS>(); break;
+        default: if constexpr (D > 4) wait_vm<4 * DTL_OPS>(); else wait_vm<DTL_OPS>(); break;
+    }
+}
+
+template <int BM, int BK, int NSTAGE, int PL, int QL, int EPI, int TAG>
 __global__ __launch_bounds__(NT, 2) void gemm_stream_kernel(GemmArgs a) {
-    using TP = STile<BM, PL>;
-    using TQ = STile<BN, QL>;
+    using TP = STile<BM, PL, BK>;
+    using TQ = STile<BN, QL, BK>;
     constexpr int TM = BM / 64;
     constexpr int TN = BN / 64;
+    constexpr int NSUB = BK / 16;                                    // MFMA k-steps per K tile
+    constexpr int D = NSTAGE - 1;                                    // K tiles loaded ahead
     constexpr int STAGE = TP::BYTES + TQ::BYTES;
     constexpr int DTL_OPS = TP::DTL_PER_WAVE + TQ::DTL_PER_WAVE;    // per wave per K tile
+    constexpr int NMFMA = NSUB * TM * TN;                            // per wave per K tile
+    static_assert(2 * DTL_OPS <= NMFMA, "one direct-to-LDS load per two MFMAs");
     __shared__ __attribute__((aligned(1024))) char smem[NSTAGE * STAGE];
 
     // XCD-aware renumbering: hardware hands block b to XCD b % 8
@@ -227,6 +252,8 @@ __global__ __launch_bounds__(NT, 2) void gemm_stream_kernel(GemmArgs a) {
     const uint16_t* Q = reinterpret_cast<const uint16_t*>(a.q);
     const bool p_al = aligned16(a.p, a.ldp);
     const bool q_al = aligned16(a.q, a.ldq);
+    // K tiles 0 .. nk_dtl-1 go direct to LDS: whole tiles of aligned operands
+    const int nk_dtl = (p_al && q_al) ? (int)((kend - kbeg) / BK) : 0;
 
     const int tid = threadIdx.x;
     const int wave = tid >> 6;
@@ -242,11 +269,6 @@ __global__ __launch_bounds__(NT, 2) void gemm_stream_kernel(GemmArgs a) {
 #pragma unroll
             for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.0f;
 
-    // Whether K tile kt goes direct to LDS (whole, and aligned operands).
-    auto dtl_ok = [&](int kt) -> bool {
-        const int64_t k0 = kbeg + (int64_t)kt * BK;
-        return k0 + BK <= kend && p_al && q_al;
-    };
     // Direct-to-LDS instruction r (of DTL_OPS) of K tile kt.
     auto issue_one = [&](int r, int kt) {
         char* As = smem + (kt % NSTAGE) * STAGE;
@@ -254,69 +276,74 @@ __global__ __launch_bounds__(NT, 2) void gemm_stream_kernel(GemmArgs a) {
         if (r < TP::DTL_PER_WAVE) TP::dtl_one(r, As, P, a.ldp, m0, a.M, k0);
         else TQ::dtl_one(r - TP::DTL_PER_WAVE, As + TP::BYTES, Q, a.ldq, n0, a.N, k0);
     };
-    // Whole K tile, direct-to-LDS or guarded register path (K tail, unaligned
-    // operands; LDS written at once).
+    // Whole K tile: direct-to-LDS, or the guarded register path (K tail,
+    // unaligned operands; LDS written at once).
     auto issue = [&](int kt) {
         char* As = smem + (kt % NSTAGE) * STAGE;
         const int64_t k0 = kbeg + (int64_t)kt * BK;
-        const bool kfull = k0 + BK <= kend;
-        if (kfull && p_al) TP::dtl(As, P, a.ldp, m0, a.M, k0);
-        else TP::load_store(As, P, a.ldp, m0, a.M, k0, kend, p_al);
-        if (kfull && q_al) TQ::dtl(As + TP::BYTES, Q, a.ldq, n0, a.N, k0);
-        else TQ::load_store(As + TP::BYTES, Q, a.ldq, n0, a.N, k0, kend, q_al);
+        if (kt < nk_dtl) {
+            TP::dtl(As, P, a.ldp, m0, a.M, k0);
+            TQ::dtl(As + TP::BYTES, Q, a.ldq, n0, a.N, k0);
+        } else {
+            TP::load_store(As, P, a.ldp, m0, a.M, k0, kend, p_al);
+            TQ::load_store(As + TP::BYTES, Q, a.ldq, n0, a.N, k0, kend, q_al);
+        }
     };
 
-    constexpr int NMFMA = 2 * TM * TN;
-    static_assert(2 * DTL_OPS <= NMFMA, "one direct-to-LDS load per two MFMAs");
-    if (nk > 0) {
-        bool next_dtl = nk > 1 && dtl_ok(1);         // K tile kt+1 went direct to LDS
-        issue(0);
-        if (nk > 1) issue(1);
-        for (int kt = 0; kt < nk; ++kt) {
-            // K tile kt is complete once only K tile kt+1's loads can still be
-            // outstanding (vector-memory operations complete in issue order)
-            if (kt + 1 < nk && next_dtl) wait_vm<DTL_OPS>();
-            else wait_vm<0>();
-            barrier_lds();                           // also: every wave is done with K tile kt-1's stage
-            // K tile kt+2 goes into the stage K tile kt-1 used.  Direct-to-LDS
-            // loads are issued one per two MFMAs below: a burst of them would
-            // stall this wave on the address unit's queue while its MFMA unit
-            // idles.  Register-path tiles are loaded here, at once.
-            const bool pf = kt + 2 < nk && dtl_ok(kt + 2);
-            if (kt + 2 < nk && !pf) issue(kt + 2);
-            const char* As = smem + (kt % NSTAGE) * STAGE;
-            const char* Bs = As + TP::BYTES;
-            bf16x8 fa[2][TM], fb[2][TN];
-#pragma unroll
-            for (int s = 0; s < 2; ++s) {
-#pragma unroll
-                for (int i = 0; i < TM; ++i) fa[s][i] = TP::frag(As, wm * (BM / 2) + 32 * i, s, lane);
-#pragma unroll
-                for (int j = 0; j < TN; ++j) fb[s][j] = TQ::frag(Bs, wn * (BN / 2) + 32 * j, s, lane);
-            }
-#pragma unroll
-            for (int s = 0; s < 2; ++s)
-#pragma unroll
-                for (int i = 0; i < TM; ++i)
-#pragma unroll
-                    for (int j = 0; j < TN; ++j) {
-                        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[s][i], fb[s][j], acc[i][j],
-                                                                            0, 0, 0);
-                        const int n = (s * TM + i) * TN + j;          // MFMA index in this K tile
-                        if ((n & 1) == 1 && (n >> 1) < DTL_OPS && pf) issue_one(n >> 1, kt + 2);
-                    }
-            next_dtl = pf;
+    for (int kt = 0; kt < D && kt < nk; ++kt) issue(kt);
+    for (int kt = 0; kt < nk; ++kt) {
+        // K tile kt is complete once at most the direct-to-LDS operations of
+        // the K tiles issued after it are outstanding (vector-memory
+        // operations complete in issue order; register-path tiles leave none).
+        {
+            int after = min(kt + D - 1, nk - 1);
+            if (after > nk_dtl - 1) after = nk_dtl - 1;
+            wait_tiles<DTL_OPS, D>(after > kt ? after - kt : 0);
         }
+        barrier_lds();                               // also: every wave is done with K tile kt-1's stage
+        // K tile kt+D goes into the stage K tile kt-1 used.  Direct-to-LDS
+        // loads are issued one per two MFMAs below: a burst of them would stall
+        // this wave on the address unit's queue while its MFMA unit idles.
+        // Register-path tiles are loaded here, at once.
+        const bool pf = kt + D < nk_dtl;
+        if (kt + D < nk && !pf) issue(kt + D);
+        const char* As = smem + (kt % NSTAGE) * STAGE;
+        const char* Bs = As + TP::BYTES;
+        bf16x8 fa[NSUB][TM], fb[NSUB][TN];
+#pragma unroll
+        for (int s = 0; s < NSUB; ++s) {
+#pragma unroll
+            for (int i = 0; i < TM; ++i) fa[s][i] = TP::frag(As, wm * (BM / 2) + 32 * i, s, lane);
+#pragma unroll
+            for (int j = 0; j < TN; ++j) fb[s][j] = TQ::frag(Bs, wn * (BN / 2) + 32 * j, s, lane);
+        }
+#pragma unroll
+        for (int s = 0; s < NSUB; ++s)
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+#pragma unroll
+                for (int j = 0; j < TN; ++j) {
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[s][i], fb[s][j], acc[i][j], 0, 0, 0);
+                    const int n = (s * TM + i) * TN + j;          // MFMA index in this K tile
+                    if ((n & 1) == 1 && (n >> 1) < DTL_OPS && pf) issue_one(n >> 1, kt + D);
+                }
     }
     epilogue_block<EPI>(a, acc, m0 + wm * (BM / 2), n0 + wn * (BN / 2), lane, split);
 }
+
+// K tile and LDS stages: 32 x 3 (72 KB at BM = 256, two K tiles in flight).
+// (16 x 6 keeps more bytes in flight but halves the MFMAs between barriers;
+// measured slower on MI355X.)
+constexpr int kStreamBK = 32;
+constexpr int kStreamStages = 3;
 
 template <int BM, int PL, int QL, int EPI, int TAG>
 hipError_t launch_s(const GemmArgs& a, hipStream_t s) {
     const int64_t tiles = ((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN) * (int64_t)a.splits;
     if (tiles <= 0) return hipSuccess;
     if (tiles > 0x7fffffffLL) return hipErrorInvalidConfiguration;
-    hipLaunchKernelGGL((gemm_stream_kernel<BM, PL, QL, EPI, TAG>), dim3((unsigned)tiles), dim3(NT), 0, s, a);
+    hipLaunchKernelGGL((gemm_stream_kernel<BM, kStreamBK, kStreamStages, PL, QL, EPI, TAG>), dim3((unsigned)tiles),
+                       dim3(NT), 0, s, a);
     return hipGetLastError();
 }
 
