@@ -101,14 +101,30 @@ __device__ __forceinline__ void store_bf16x4(uint16_t* p, uint32_t q0, uint32_t 
     }
 }
 
-// Epilogue of 4 consecutive columns (gn .. gn+3) of output row gm.
-template <int EPI>
-__device__ __forceinline__ void epilogue4(const GemmArgs& a, int64_t gm, int64_t gn, const float v[4], int split) {
-    if (gm >= a.M || gn >= a.N) return;
+// Z (bf16) at 4 consecutive columns gn .. gn+3 of row gm, packed as two
+// bf16 pairs; columns past the edge read as 0.  (EPI_DZ)
+__device__ __forceinline__ u32x2_t load_z4(const GemmArgs& a, int64_t gm, int64_t gn) {
+    if (gm >= a.M || gn >= a.N) return u32x2_t{0u, 0u};
     const int valid = (int)((a.N - gn) < 4 ? (a.N - gn) : 4);
+    const uint16_t* zp = reinterpret_cast<const uint16_t*>(a.zin) + gm * a.ldzin + gn;
+    if (valid == 4 && (reinterpret_cast<uintptr_t>(zp) & 7u) == 0) return *reinterpret_cast<const u32x2_t*>(zp);
+    uint32_t e[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) e[k] = k < valid ? (uint32_t)zp[k] : 0u;
+    return u32x2_t{e[0] | (e[1] << 16), e[2] | (e[3] << 16)};
+}
+
+// Epilogue of 4 consecutive columns (gn .. gn+3) of output row gm; zz: the
+// matching Z values (EPI_DZ only).  FAST: the 4 columns exist and every
+// pointer is aligned for one vector access (checked once per block).
+template <int EPI, bool FAST>
+__device__ __forceinline__ void epilogue4(const GemmArgs& a, int64_t gm, int64_t gn, const float v[4], int split,
+                                          u32x2_t zz = u32x2_t{0u, 0u}) {
+    if (!FAST && (gm >= a.M || gn >= a.N)) return;
+    const int valid = FAST ? 4 : (int)((a.N - gn) < 4 ? (a.N - gn) : 4);
     if constexpr (EPI == EPI_STORE_F32) {
         float* c = reinterpret_cast<float*>(a.c) + (int64_t)split * a.split_stride + gm * a.ldc + gn;
-        if (valid == 4 && (reinterpret_cast<uintptr_t>(c) & 15u) == 0) {
+        if (FAST || (valid == 4 && (reinterpret_cast<uintptr_t>(c) & 15u) == 0)) {
             *reinterpret_cast<f32x4_t*>(c) = f32x4_t{v[0], v[1], v[2], v[3]};
         } else {
 #pragma unroll
@@ -129,18 +145,8 @@ __device__ __forceinline__ void epilogue4(const GemmArgs& a, int64_t gm, int64_t
                 h[e] = act_sigma<true>(a.act, out[e]);
             }
         } else if constexpr (EPI == EPI_DZ) {
-            const uint16_t* zp = reinterpret_cast<const uint16_t*>(a.zin) + gm * a.ldzin + gn;
-            float z[4];
-            if (valid == 4 && (reinterpret_cast<uintptr_t>(zp) & 7u) == 0) {
-                const u32x2_t zz = *reinterpret_cast<const u32x2_t*>(zp);
-                z[0] = bf16_to_f32(zz[0] & 0xffffu);
-                z[1] = bf16_to_f32(zz[0] >> 16);
-                z[2] = bf16_to_f32(zz[1] & 0xffffu);
-                z[3] = bf16_to_f32(zz[1] >> 16);
-            } else {
-#pragma unroll
-                for (int e = 0; e < 4; ++e) z[e] = e < valid ? bf16_to_f32(zp[e]) : 0.0f;
-            }
+            const float z[4] = {bf16_to_f32(zz[0] & 0xffffu), bf16_to_f32(zz[0] >> 16),
+                                bf16_to_f32(zz[1] & 0xffffu), bf16_to_f32(zz[1] >> 16)};
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
                 if (a.act == 0) {
@@ -153,23 +159,30 @@ __device__ __forceinline__ void epilogue4(const GemmArgs& a, int64_t gm, int64_t
                 }
             }
         }
-        const bool vec = valid == 4 && (reinterpret_cast<uintptr_t>(c) & 7u) == 0;
+        const bool vec = FAST || (valid == 4 && (reinterpret_cast<uintptr_t>(c) & 7u) == 0);
         store_bf16x4(c, pack_bf16x2(out[0], out[1]), pack_bf16x2(out[2], out[3]), vec, valid);
         if constexpr (EPI == EPI_Z_H || EPI == EPI_DZ) {
             if (a.aux) {
                 uint16_t* hp = reinterpret_cast<uint16_t*>(a.aux) + gm * a.ldaux + gn;
-                const bool hvec = valid == 4 && (reinterpret_cast<uintptr_t>(hp) & 7u) == 0;
+                const bool hvec = FAST || (valid == 4 && (reinterpret_cast<uintptr_t>(hp) & 7u) == 0);
                 store_bf16x4(hp, pack_bf16x2(h[0], h[1]), pack_bf16x2(h[2], h[3]), hvec, valid);
             }
         }
     }
 }
 
-// The whole epilogue of one wave's block of TM x TN MFMA tiles, whose first
-// output row and column are row0, col0.
-template <int EPI, int TM, int TN>
-__device__ __forceinline__ void epilogue_block(const GemmArgs& a, const f32x16 (&acc)[TM][TN],
-                                               int64_t row0, int64_t col0, int lane, int split) {
+// Z for the lane's 4 columns of row gm (FAST: one unguarded vector load).
+template <bool FAST>
+__device__ __forceinline__ u32x2_t z4(const GemmArgs& a, int64_t gm, int64_t gn) {
+    if constexpr (FAST)
+        return *reinterpret_cast<const u32x2_t*>(reinterpret_cast<const uint16_t*>(a.zin) + gm * a.ldzin + gn);
+    else
+        return load_z4(a, gm, gn);
+}
+
+template <int EPI, bool FAST, int TM, int TN>
+__device__ __forceinline__ void epilogue_block_impl(const GemmArgs& a, const f32x16 (&acc)[TM][TN],
+                                                    int64_t row0, int64_t col0, int lane, int split) {
     const int64_t lrow = 4 * (lane >> 5) + (lane & 3);     // this lane's row within a group of 8
     const int64_t lcol = 4 * ((lane & 31) >> 2);           // its first column within a tile
     if constexpr (EPI == EPI_STORE) {
@@ -186,12 +199,44 @@ __device__ __forceinline__ void epilogue_block(const GemmArgs& a, const f32x16 (
                                    pack_bf16x2(acc[i][j][4 * g + 2], acc[i][j][4 * g + 3]), q0, q1);
                     const int64_t gm = row0 + 32 * i + 8 * g + lrow;
                     const int64_t gn = col0 + 32 * j + lcol;
-                    if (gm < a.M && gn < a.N) {
+                    uint16_t* c = reinterpret_cast<uint16_t*>(a.c) + gm * a.ldc + gn;
+                    if (FAST) {
+                        *reinterpret_cast<u32x2_t*>(c) = u32x2_t{q0, q1};
+                    } else if (gm < a.M && gn < a.N) {
                         const int valid = (int)((a.N - gn) < 4 ? (a.N - gn) : 4);
-                        uint16_t* c = reinterpret_cast<uint16_t*>(a.c) + gm * a.ldc + gn;
                         store_bf16x4(c, q0, q1, valid == 4 && (reinterpret_cast<uintptr_t>(c) & 7u) == 0, valid);
                     }
                 }
+    } else if constexpr (EPI == EPI_DZ) {
+        // Z for row tile i+1 is loaded before row tile i's stores: a wave's
+        // vector-memory operations complete in order, so a Z load issued
+        // after a store would also wait for that store.
+        u32x2_t zb[2][4][TN];
+#pragma unroll
+        for (int g = 0; g < 4; ++g)
+#pragma unroll
+            for (int j = 0; j < TN; ++j) zb[0][g][j] = z4<FAST>(a, row0 + 8 * g + lrow, col0 + 32 * j + lcol);
+#pragma unroll
+        for (int i = 0; i < TM; ++i) {
+            if (i + 1 < TM) {
+#pragma unroll
+                for (int g = 0; g < 4; ++g)
+#pragma unroll
+                    for (int j = 0; j < TN; ++j)
+                        zb[(i + 1) & 1][g][j] = z4<FAST>(a, row0 + 32 * (i + 1) + 8 * g + lrow, col0 + 32 * j + lcol);
+            }
+#pragma unroll
+            for (int g = 0; g < 4; ++g)
+#pragma unroll
+                for (int j = 0; j < TN; ++j) {
+                    const float x[4] = {acc[i][j][4 * g], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2],
+                                        acc[i][j][4 * g + 3]};
+                    float y[4];
+                    transpose_f32(lane, x, y);
+                    epilogue4<EPI, FAST>(a, row0 + 32 * i + 8 * g + lrow, col0 + 32 * j + lcol, y, split,
+                                         zb[i & 1][g][j]);
+                }
+        }
     } else {
 #pragma unroll
         for (int i = 0; i < TM; ++i)
@@ -203,9 +248,31 @@ __device__ __forceinline__ void epilogue_block(const GemmArgs& a, const f32x16 (
                                         acc[i][j][4 * g + 3]};
                     float y[4];
                     transpose_f32(lane, x, y);
-                    epilogue4<EPI>(a, row0 + 32 * i + 8 * g + lrow, col0 + 32 * j + lcol, y, split);
+                    epilogue4<EPI, FAST>(a, row0 + 32 * i + 8 * g + lrow, col0 + 32 * j + lcol, y, split);
                 }
     }
+}
+
+// The whole epilogue of one wave's block of TM x TN MFMA tiles, whose first
+// output row and column are row0, col0.  Blocks wholly inside the output with
+// aligned pointers (the common case) take the unguarded vector path.
+template <int EPI, int TM, int TN>
+__device__ __forceinline__ void epilogue_block(const GemmArgs& a, const f32x16 (&acc)[TM][TN],
+                                               int64_t row0, int64_t col0, int lane, int split) {
+    auto al = [](const void* p, int64_t ld, int64_t elems) {   // rows of elems-element vectors
+        return p != nullptr && (reinterpret_cast<uintptr_t>(p) % (2 * elems)) == 0 && ld % elems == 0;
+    };
+    bool fast = row0 + 32 * TM <= a.M && col0 + 32 * TN <= a.N;
+    if constexpr (EPI == EPI_STORE_F32) {
+        const float* c = reinterpret_cast<const float*>(a.c) + (int64_t)split * a.split_stride;
+        fast = fast && (reinterpret_cast<uintptr_t>(c) & 15u) == 0 && a.ldc % 4 == 0;
+    } else {
+        fast = fast && al(a.c, a.ldc, 4);
+    }
+    if constexpr (EPI == EPI_Z_H || EPI == EPI_DZ) fast = fast && (a.aux == nullptr || al(a.aux, a.ldaux, 4));
+    if constexpr (EPI == EPI_DZ) fast = fast && al(a.zin, a.ldzin, 4);
+    if (fast) epilogue_block_impl<EPI, true>(a, acc, row0, col0, lane, split);
+    else epilogue_block_impl<EPI, false>(a, acc, row0, col0, lane, split);
 }
 
 }  // namespace cola
