@@ -65,9 +65,11 @@ typedef void* cola_stream_t;
 
 typedef enum { COLA_F32 = 0, COLA_BF16 = 1 } cola_dtype;
 
-/* sigma: identity (the conventional low-rank product B A x, Sec. 3.3) or
- * SiLU z * logistic(z) (Swish, the activation of the paper's LLaMA runs). */
-typedef enum { COLA_ACT_IDENTITY = 0, COLA_ACT_SILU = 1 } cola_act;
+/* sigma: identity (the conventional low-rank product B A x, Sec. 3.3),
+ * SiLU z * logistic(z) (Swish, the activation of the paper's LLaMA runs), or
+ * GeLU z * Phi(z) with Phi the standard normal CDF (the exact form; the
+ * paper names GeLU for its BERT runs without saying which form). */
+typedef enum { COLA_ACT_IDENTITY = 0, COLA_ACT_SILU = 1, COLA_ACT_GELU = 2 } cola_act;
 
 typedef enum {
     COLA_OK = 0,

@@ -63,7 +63,7 @@ def use_library(path=None):
         _load(path)
 
 
-ACT = {"identity": 0, "silu": 1}
+ACT = {"identity": 0, "silu": 1, "gelu": 2}
 
 
 def _act(act):

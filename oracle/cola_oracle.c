@@ -27,7 +27,10 @@
  * sigma: act 0 = identity, act 1 = SiLU (Swish with beta = 1), the
  * activation the paper names for its LLaMA runs (Sec. 5.2, the closing remark
  * naming GeLU and Swish).  SiLU(z) = z s(z), s = logistic sigmoid,
- * SiLU'(z) = s(z) (1 + z (1 - s(z))).
+ * SiLU'(z) = s(z) (1 + z (1 - s(z))).  act 2 = GeLU, the other activation
+ * that remark names (the BERT runs, App. E); the paper does not say which
+ * form, this is the exact one: GeLU(z) = z Phi(z), Phi the standard normal
+ * CDF, GeLU'(z) = Phi(z) + z phi(z), phi its density.
  *
  * Every matrix product is a textbook triple loop, no blocking, no BLAS,
  * no fast-math; OpenMP splits only the outermost output-row loop, so each
@@ -84,13 +87,19 @@ static double logistic(double z) {
     return e / (1.0 + e);
 }
 
+/* standard normal CDF through erfc (no cancellation for negative z) and density */
+static double normal_cdf(double z) { return 0.5 * erfc(-z * 0.70710678118654752440); }
+static double normal_pdf(double z) { return 0.39894228040143267794 * exp(-0.5 * z * z); }
+
 double oracle_sigma(int act, double z) {
     if (act == 0) return z;
+    if (act == 2) return z * normal_cdf(z);
     return z * logistic(z);
 }
 
 double oracle_sigma_prime(int act, double z) {
     if (act == 0) return 1.0;
+    if (act == 2) return normal_cdf(z) + z * normal_pdf(z);
     double s = logistic(z);
     return s * (1.0 + z * (1.0 - s));
 }

@@ -14,9 +14,9 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(PKG, "libcola.so")
 
 F32, BF16 = 0, 1
-ACT_IDENTITY, ACT_SILU = 0, 1
+ACT_IDENTITY, ACT_SILU, ACT_GELU = 0, 1, 2
 DTYPES = {"f32": F32, "bf16": BF16}
-ACTS = {"identity": ACT_IDENTITY, "silu": ACT_SILU}
+ACTS = {"identity": ACT_IDENTITY, "silu": ACT_SILU, "gelu": ACT_GELU}
 
 OK, ERR_INVALID_ARG, ERR_BAD_SHAPE, ERR_WORKSPACE, ERR_HIP, ERR_UNSUPPORTED = range(6)
 

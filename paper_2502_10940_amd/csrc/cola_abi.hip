@@ -122,7 +122,8 @@ struct Dims {
 int check_desc(const cola_desc* d, Dims* out) {
     if (!d) return COLA_ERR_INVALID_ARG;
     if (d->dtype != COLA_F32 && d->dtype != COLA_BF16) return COLA_ERR_INVALID_ARG;
-    if (d->act != COLA_ACT_IDENTITY && d->act != COLA_ACT_SILU) return COLA_ERR_INVALID_ARG;
+    if (d->act != COLA_ACT_IDENTITY && d->act != COLA_ACT_SILU && d->act != COLA_ACT_GELU)
+        return COLA_ERR_INVALID_ARG;
     if (d->recompute != 0 && d->recompute != 1) return COLA_ERR_INVALID_ARG;
     if (d->T < 0 || d->d_in < 1 || d->d_out < 1 || d->r < 1) return COLA_ERR_BAD_SHAPE;
     if (d->T > kMaxDim || d->d_in > kMaxDim || d->d_out > kMaxDim || d->r > kMaxDim)

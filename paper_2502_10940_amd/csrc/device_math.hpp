@@ -43,11 +43,23 @@ __device__ __forceinline__ float logistic_exact(float z) {
     return 1.0f / (1.0f + expf(-z));
 }
 
-// sigma(z) and sigma'(z) for act 0 (identity) and 1 (SiLU = z s(z),
-// SiLU' = s (1 + z (1 - s))).  FAST selects the hardware exp (bf16 path).
+// Standard normal CDF Phi(z) = erfc(-z / sqrt 2) / 2 and density phi(z).
+template <bool FAST>
+__device__ __forceinline__ float normal_cdf(float z) {
+    return 0.5f * erfcf(-z * 0.70710678118654752f);
+}
+template <bool FAST>
+__device__ __forceinline__ float normal_pdf(float z) {
+    return 0.39894228040143268f * (FAST ? __expf(-0.5f * z * z) : expf(-0.5f * z * z));
+}
+
+// sigma(z) and sigma'(z) for act 0 (identity), 1 (SiLU = z s(z),
+// SiLU' = s (1 + z (1 - s))) and 2 (GeLU = z Phi(z), GeLU' = Phi + z phi).
+// FAST selects the hardware exp and reciprocal (bf16 path).
 template <bool FAST>
 __device__ __forceinline__ float act_sigma(int act, float z) {
     if (act == 0) return z;
+    if (act == 2) return z * normal_cdf<FAST>(z);
     float s = FAST ? logistic_fast(z) : logistic_exact(z);
     return z * s;
 }
@@ -55,8 +67,27 @@ __device__ __forceinline__ float act_sigma(int act, float z) {
 template <bool FAST>
 __device__ __forceinline__ float act_sigma_prime(int act, float z) {
     if (act == 0) return 1.0f;
+    if (act == 2) return normal_cdf<FAST>(z) + z * normal_pdf<FAST>(z);
     float s = FAST ? logistic_fast(z) : logistic_exact(z);
     return s * (1.0f + z * (1.0f - s));
+}
+
+// Both at once (the dZ epilogue needs sigma' and, for CoLA-M, H = sigma(z)),
+// sharing the transcendental work.
+template <bool FAST>
+__device__ __forceinline__ void act_sigma_both(int act, float z, float& sig, float& sigp) {
+    if (act == 0) {
+        sig = z;
+        sigp = 1.0f;
+    } else if (act == 2) {
+        const float cdf = normal_cdf<FAST>(z);
+        sig = z * cdf;
+        sigp = cdf + z * normal_pdf<FAST>(z);
+    } else {
+        const float s = FAST ? logistic_fast(z) : logistic_exact(z);
+        sig = z * s;
+        sigp = s * (1.0f + z * (1.0f - s));
+    }
 }
 
 }  // namespace cola

@@ -149,14 +149,9 @@ __device__ __forceinline__ void epilogue4(const GemmArgs& a, int64_t gm, int64_t
                                 bf16_to_f32(zz[1] & 0xffffu), bf16_to_f32(zz[1] >> 16)};
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
-                if (a.act == 0) {
-                    out[e] = v[e];
-                    h[e] = z[e];
-                } else {
-                    const float s = logistic_fast(z[e]);
-                    out[e] = v[e] * (s * (1.0f + z[e] * (1.0f - s)));
-                    h[e] = z[e] * s;
-                }
+                float sp;
+                act_sigma_both<true>(a.act, z[e], h[e], sp);
+                out[e] = a.act == 0 ? v[e] : v[e] * sp;
             }
         }
         const bool vec = FAST || (valid == 4 && (reinterpret_cast<uintptr_t>(c) & 7u) == 0);

@@ -70,7 +70,7 @@ def bwd_status(d, dY=FAKE, X=FAKE, Z=FAKE, H=FAKE, A=FAKE, B=FAKE, dX=FAKE, dA=F
 def test_invalid_descriptors():
     assert fwd_status(None) == cola.ERR_INVALID_ARG
     assert bwd_status(None) == cola.ERR_INVALID_ARG
-    for kw, code in ((dict(dtype=7), cola.ERR_INVALID_ARG), (dict(act=5), cola.ERR_INVALID_ARG),
+    for kw, code in ((dict(dtype=7), cola.ERR_INVALID_ARG), (dict(act=3), cola.ERR_INVALID_ARG),
                      (dict(recompute=True), None)):
         d = cola.desc(16, 32, 32, 8, **{k: v for k, v in kw.items() if k != "recompute"})
         if "recompute" in kw:

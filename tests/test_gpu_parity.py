@@ -38,6 +38,8 @@ CASES = [
     ("t255_bf16", 255, 264, 136, 8, "bf16", "silu"),
     ("odd_width_weight_repack_bf16", 300, 301, 263, 40, "bf16", "silu"),
     ("odd_rank_weight_repack_bf16", 200, 136, 144, 37, "bf16", "silu"),
+    ("gelu_bf16", 600, 520, 264, 136, "bf16", "gelu"),
+    ("gelu_f32", 256, 512, 512, 128, "f32", "gelu"),
 ]
 
 

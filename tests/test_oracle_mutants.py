@@ -24,6 +24,11 @@ MUTANTS = {
     "wgrad_dB_uses_dZ": ("for (int64_t t = 0; t < T; ++t) s += dY[t * d_out + o] * H[t];",
                          "for (int64_t t = 0; t < T; ++t) s += dY[t * d_out + o] * dZ[t];"),
     "H_skips_sigma": ("H[i] = oracle_sigma(act, Z[i]);\n    gemm_nt", "H[i] = Z[i];\n    gemm_nt"),
+    "gelu_prime_drops_pdf_term": ("if (act == 2) return normal_cdf(z) + z * normal_pdf(z);",
+                                  "if (act == 2) return normal_cdf(z);"),
+    "gelu_cdf_wrong_sign": ("return 0.5 * erfc(-z * 0.70710678118654752440);",
+                            "return 0.5 * erfc(z * 0.70710678118654752440);"),
+    "gelu_pdf_wrong_scale": ("exp(-0.5 * z * z)", "exp(-z * z)"),
     "mac_counter_fwd_only_one_gemm": ("static void gemm_nt(int64_t M, int64_t N, int64_t K,\n                    const double* P, const double* Q, double* C) {\n    g_mac_count += M * N * K;",
                                       "static void gemm_nt(int64_t M, int64_t N, int64_t K,\n                    const double* P, const double* Q, double* C) {\n    g_mac_count += M * N;"),
 }
@@ -36,8 +41,12 @@ def battery():
         ("silu_fd", pins.test_silu_derivative_by_central_difference, (1.0,)),
         ("silu_expit", pins.test_silu_against_scipy_expit, ()),
         ("identity", pins.test_identity_sigma_is_low_rank_product, ((7, 5, 4, 3),)),
-        ("fd_grads", pins.test_gradients_by_central_differences, ((3, 5, 4, 2),)),
-        ("torch", pins.test_against_torch_fp64_autograd, ((16, 32, 24, 8),)),
+        ("fd_grads", pins.test_gradients_by_central_differences, ((3, 5, 4, 2), "silu")),
+        ("torch", pins.test_against_torch_fp64_autograd, ((16, 32, 24, 8), "silu")),
+        ("gelu_values", pins.test_gelu_special_values, ()),
+        ("gelu_ndtr", pins.test_gelu_against_scipy_ndtr, ()),
+        ("gelu_fd", pins.test_gelu_derivative_by_central_difference, (-0.75,)),
+        ("fd_grads_gelu", pins.test_gradients_by_central_differences, ((3, 5, 4, 2), "gelu")),
         ("prop1", pins.test_prop1_limit_construction, ()),
         ("lemma", pins.test_lemma_esigma_zero_construction, ()),
         ("sampled", pins.test_sampled_rows_and_columns_match_full, ()),

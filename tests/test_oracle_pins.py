@@ -74,6 +74,44 @@ def test_silu_against_scipy_expit():
 
 
 # --------------------------------------------------------------------------
+# GeLU (exact form): values against scipy's normal CDF, derivative by central
+# differences, and the Prop. 1 hypotheses sigma(0) = 0, sigma'(0) = 1/2
+# --------------------------------------------------------------------------
+
+def test_gelu_special_values():
+    assert oracle.sigma("gelu", 0.0) == 0.0
+    assert oracle.sigma_prime("gelu", 0.0) == 0.5
+    # GeLU(1) = Phi(1), GeLU(-1) = -Phi(-1) = -(1 - Phi(1))
+    assert oracle.sigma("gelu", 1.0) == pytest.approx(0.8413447460685429, rel=1e-15)
+    assert oracle.sigma("gelu", -1.0) == pytest.approx(-0.15865525393145707, rel=1e-14)
+    # no overflow far out; GeLU(z) -> z and GeLU'(z) -> 1 for large z, -> 0 for very negative z
+    assert oracle.sigma("gelu", 40.0) == 40.0
+    assert oracle.sigma_prime("gelu", 40.0) == 1.0
+    assert abs(oracle.sigma("gelu", -40.0)) < 1e-300
+    assert oracle.sigma_prime("gelu", -40.0) == 0.0 or abs(oracle.sigma_prime("gelu", -40.0)) < 1e-300
+
+
+def test_gelu_against_scipy_ndtr():
+    zs = np.linspace(-12, 12, 481)
+    ours = np.array([oracle.sigma("gelu", z) for z in zs])
+    np.testing.assert_allclose(ours, zs * scipy.special.ndtr(zs), rtol=1e-13, atol=1e-300)
+
+
+@pytest.mark.parametrize("z", [-6.0, -2.0, -0.75, -0.1, 0.0, 0.3, 1.0, 3.5])
+def test_gelu_derivative_by_central_difference(z):
+    h = 1e-5
+    fd = (oracle.sigma("gelu", z + h) - oracle.sigma("gelu", z - h)) / (2 * h)
+    assert oracle.sigma_prime("gelu", z) == pytest.approx(fd, abs=1e-9)
+
+
+@pytest.mark.parametrize("z", [-5.0, -0.7, 0.3, 2.0, 9.0])
+def test_gelu_odd_part_identities(z):
+    # Phi(z) + Phi(-z) = 1: GeLU(z) - GeLU(-z) = z and GeLU'(z) + GeLU'(-z) = 1
+    assert oracle.sigma("gelu", z) - oracle.sigma("gelu", -z) == pytest.approx(z, rel=1e-14)
+    assert oracle.sigma_prime("gelu", z) + oracle.sigma_prime("gelu", -z) == pytest.approx(1.0, rel=1e-14)
+
+
+# --------------------------------------------------------------------------
 # identity sigma: the layer is the conventional low-rank product B A X (Sec. 3.3)
 # --------------------------------------------------------------------------
 
@@ -111,16 +149,17 @@ def test_dense_oracle_against_numpy_and_merged_cola():
 # SiLU gradients: brute-force central differences of L = <dY, Y(X, A, B)>
 # --------------------------------------------------------------------------
 
+@pytest.mark.parametrize("act", ["silu", "gelu"])
 @pytest.mark.parametrize("shape", [(1, 1, 1, 1), (3, 5, 4, 2), (7, 1, 4, 3), (7, 5, 1, 3)])
-def test_gradients_by_central_differences(shape):
+def test_gradients_by_central_differences(shape, act):
     T, d_in, d_out, r = shape
     X, A, B, dY = rand_layer(21 + T, T, d_in, d_out, r, scale_a=0.9, scale_b=0.8)
 
     def loss(X_, A_, B_):
-        return float(np.sum(dY * oracle.cola_fwd(X_, A_, B_, act="silu")[2]))
+        return float(np.sum(dY * oracle.cola_fwd(X_, A_, B_, act=act)[2]))
 
-    Z, _, _ = oracle.cola_fwd(X, A, B, act="silu")
-    _, dX, dA, dB = oracle.cola_bwd(X, Z, A, B, dY, act="silu")
+    Z, _, _ = oracle.cola_fwd(X, A, B, act=act)
+    _, dX, dA, dB = oracle.cola_bwd(X, Z, A, B, dY, act=act)
     h = 1e-5
     for name, arr, grad in (("X", X, dX), ("A", A, dA), ("B", B, dB)):
         fd = np.zeros_like(arr)
@@ -138,8 +177,9 @@ def test_gradients_by_central_differences(shape):
 # library cross-check: torch fp64 autograd on the CPU
 # --------------------------------------------------------------------------
 
+@pytest.mark.parametrize("act", ["silu", "gelu"])
 @pytest.mark.parametrize("shape", [(16, 32, 24, 8), (37, 13, 29, 5), (64, 64, 64, 16)])
-def test_against_torch_fp64_autograd(shape):
+def test_against_torch_fp64_autograd(shape, act):
     T, d_in, d_out, r = shape
     X, A, B, dY = rand_layer(31, T, d_in, d_out, r)
     tX = torch.tensor(X, requires_grad=True)
@@ -147,11 +187,14 @@ def test_against_torch_fp64_autograd(shape):
     tB = torch.tensor(B, requires_grad=True)
     tZ = tX @ tA.T
     tZ.retain_grad()
-    tH = torch.nn.functional.silu(tZ)
+    if act == "silu":
+        tH = torch.nn.functional.silu(tZ)
+    else:
+        tH = torch.nn.functional.gelu(tZ, approximate="none")
     tY = tH @ tB.T
     tY.backward(torch.tensor(dY))
-    Z, H, Y = oracle.cola_fwd(X, A, B, act="silu")
-    dZ, dX, dA, dB = oracle.cola_bwd(X, Z, A, B, dY, act="silu")
+    Z, H, Y = oracle.cola_fwd(X, A, B, act=act)
+    dZ, dX, dA, dB = oracle.cola_bwd(X, Z, A, B, dY, act=act)
     for ours, ref in ((Z, tZ), (H, tH), (Y, tY), (dZ, tZ.grad), (dX, tX.grad),
                       (dA, tA.grad), (dB, tB.grad)):
         assert relerr(ours, ref.detach().numpy()) < 1e-13
