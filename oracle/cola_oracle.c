@@ -28,7 +28,7 @@
  * activation the paper names for its LLaMA runs (Sec. 5.2, the closing remark
  * naming GeLU and Swish).  SiLU(z) = z s(z), s = logistic sigmoid,
  * SiLU'(z) = s(z) (1 + z (1 - s(z))).  act 2 = GeLU, the other activation
- * that remark names (the BERT runs, App. E); the paper does not say which
+ * that remark names (the BERT runs, App. D); the paper does not say which
  * form, this is the exact one: GeLU(z) = z Phi(z), Phi the standard normal
  * CDF, GeLU'(z) = Phi(z) + z phi(z), phi its density.
  *
