@@ -254,6 +254,17 @@ __global__ __launch_bounds__(NT, 2) void gemm_stream_kernel(GemmArgs a) {
     const bool q_al = aligned16(a.q, a.ldq);
     // K tiles 0 .. nk_dtl-1 go direct to LDS: whole tiles of aligned operands
     const int nk_dtl = (p_al && q_al) ? (int)((kend - kbeg) / BK) : 0;
+    // Row blocks start their K sweep at different K tiles (rotated by 5 tiles
+    // per row block, when every K tile is whole and aligned), so the row
+    // blocks running together do not all fetch the same rows of the shared
+    // operand at the same moment.  The order of the sum is fixed per tile:
+    // results stay bitwise reproducible.
+    const int rot = (nk_dtl == nk && nk > 1) ? (int)(((rem / tiles_n) * 5) % nk) : 0;
+    auto kofs = [&](int kt) -> int64_t {
+        int p = kt + rot;
+        if (p >= nk) p -= nk;
+        return kbeg + (int64_t)p * BK;
+    };
 
     const int tid = threadIdx.x;
     const int wave = tid >> 6;
@@ -272,7 +283,7 @@ __global__ __launch_bounds__(NT, 2) void gemm_stream_kernel(GemmArgs a) {
     // Direct-to-LDS instruction r (of DTL_OPS) of K tile kt.
     auto issue_one = [&](int r, int kt) {
         char* As = smem + (kt % NSTAGE) * STAGE;
-        const int64_t k0 = kbeg + (int64_t)kt * BK;
+        const int64_t k0 = kofs(kt);
         if (r < TP::DTL_PER_WAVE) TP::dtl_one(r, As, P, a.ldp, m0, a.M, k0);
         else TQ::dtl_one(r - TP::DTL_PER_WAVE, As + TP::BYTES, Q, a.ldq, n0, a.N, k0);
     };
@@ -280,7 +291,7 @@ __global__ __launch_bounds__(NT, 2) void gemm_stream_kernel(GemmArgs a) {
     // unaligned operands; LDS written at once).
     auto issue = [&](int kt) {
         char* As = smem + (kt % NSTAGE) * STAGE;
-        const int64_t k0 = kbeg + (int64_t)kt * BK;
+        const int64_t k0 = kofs(kt);
         if (kt < nk_dtl) {
             TP::dtl(As, P, a.ldp, m0, a.M, k0);
             TQ::dtl(As + TP::BYTES, Q, a.ldq, n0, a.N, k0);
@@ -317,6 +328,9 @@ __global__ __launch_bounds__(NT, 2) void gemm_stream_kernel(GemmArgs a) {
 #pragma unroll
             for (int j = 0; j < TN; ++j) fb[s][j] = TQ::frag(Bs, wn * (BN / 2) + 32 * j, s, lane);
         }
+        // Raised issue priority while this wave runs its MFMAs: the other
+        // workgroup's wave on the SIMD fills the gaps with its loads and reads.
+        __builtin_amdgcn_s_setprio(1);
 #pragma unroll
         for (int s = 0; s < NSUB; ++s)
 #pragma unroll
@@ -327,6 +341,7 @@ __global__ __launch_bounds__(NT, 2) void gemm_stream_kernel(GemmArgs a) {
                     const int n = (s * TM + i) * TN + j;          // MFMA index in this K tile
                     if ((n & 1) == 1 && (n >> 1) < DTL_OPS && pf) issue_one(n >> 1, kt + D);
                 }
+        __builtin_amdgcn_s_setprio(0);
     }
     epilogue_block<EPI>(a, acc, m0 + wm * (BM / 2), n0 + wn * (BN / 2), lane, split);
 }
