@@ -125,6 +125,63 @@ int cola_bwd(const cola_desc* desc,
              void* dX, float* dA, float* dB,
              void* ws, size_t ws_bytes, cola_stream_t stream);
 
+/* ------------------------------------------------------------------------
+ * Grouped projections that read the same input (Sec. 3.2 applied to every
+ * projection of a block: q, k, v of attention read the same X, and so do
+ * gate and up of the MLP).  Projection p is its own CoLA layer
+ * (A_p [r_p][d_in], B_p [d_out_p][r_p], one sigma for the group); the group
+ * runs the shared-input products once:
+ *   forward:  Z_all = X [A_1; ..; A_n]^T           one GEMM, N = R = sum r_p
+ *             H_p = sigma(Z_p),  Y_p = H_p B_p^T    per projection
+ *   backward: dZ_p = (dY_p B_p) (.) sigma'(Z_p)     per projection
+ *             dX = sum_p dZ_p A_p                  one GEMM, K = R
+ *             [dA_1; ..; dA_n] = dZ_all^T X         one GEMM, M = R
+ *             dB_p = dY_p^T H_p                     per projection
+ * The results are those of cola_fwd / cola_bwd run on each projection, except
+ * that dX is the sum of the projections' input gradients (the gradient of
+ * the shared input).  X is read once instead of n times in each direction.
+ *
+ * Layout: A_all [R][d_in] and dA_all [R][d_in] (fp32) contiguous, projection
+ * p in rows R_p .. R_p + r_p - 1 with R_p = r_0 + .. + r_{p-1};
+ * Z_all, H_all [T][ldz], projection p in columns R_p ..; per projection
+ * B_p [d_out_p][r_p] and dB_p (fp32) contiguous, Y_p / dY_p [T][ldy_p];
+ * X, dX [T][ldx].  B, Y, dY, dB are arrays of n pointers.  Ownership,
+ * streams, padding, precision, errors and CoLA-M (recompute = 1: H_all NULL,
+ * kept in the workspace) follow cola_fwd / cola_bwd.  n is 1 .. 8.
+ * ------------------------------------------------------------------------ */
+#define COLA_GROUP_MAX 8
+
+typedef struct {
+    int64_t T;                        /* tokens (rows); T = 0 is an empty batch */
+    int64_t d_in;                     /* shared input width (>= 1) */
+    int32_t n;                        /* projections, 1 .. COLA_GROUP_MAX */
+    int32_t dtype;                    /* cola_dtype */
+    int32_t act;                      /* cola_act */
+    int32_t recompute;                /* 0 = CoLA, 1 = CoLA-M */
+    int64_t r[COLA_GROUP_MAX];        /* ranks (>= 1); R = r[0] + .. + r[n-1] */
+    int64_t d_out[COLA_GROUP_MAX];    /* output widths (>= 1) */
+    int64_t ldy[COLA_GROUP_MAX];      /* row pitch of Y_p and dY_p, 0 = d_out[p] */
+    int64_t ldx;                      /* row pitch of X and dX, 0 = d_in */
+    int64_t ldz;                      /* row pitch of Z_all and H_all, 0 = R */
+} cola_group_desc;
+
+/* Workspace bytes for phase 0 (forward) or 1 (backward); 0 on an invalid
+ * descriptor. */
+size_t cola_group_workspace_bytes(const cola_group_desc* desc, int phase);
+
+int cola_group_fwd(const cola_group_desc* desc,
+                   const void* X, const void* A_all, const void* const* B,
+                   void* const* Y, void* Z_all, void* H_all,
+                   void* ws, size_t ws_bytes, cola_stream_t stream);
+
+/* dX is overwritten with sum_p dZ_p A_p; dA_all and every dB_p are
+ * overwritten (fp32).  T = 0 writes dA_all = 0 and dB_p = 0. */
+int cola_group_bwd(const cola_group_desc* desc,
+                   const void* const* dY, const void* X, const void* Z_all, const void* H_all,
+                   const void* A_all, const void* const* B,
+                   void* dX, float* dA_all, float* const* dB,
+                   void* ws, size_t ws_bytes, cola_stream_t stream);
+
 /* Dense full-rank baseline on the same kernels (Eq. full-rank-linear and
  * the 2x rule of Sec. 3.4): Y = X W^T, dX = dY W, dW = dY^T X, with
  * W [d_out][d_in] contiguous and dW fp32 contiguous. */

@@ -42,6 +42,16 @@ class DenseDesc(ctypes.Structure):
                 ("ldx", ctypes.c_int64), ("ldy", ctypes.c_int64), ("dtype", ctypes.c_int32)]
 
 
+GROUP_MAX = 8
+
+
+class GroupDesc(ctypes.Structure):
+    _fields_ = [("T", ctypes.c_int64), ("d_in", ctypes.c_int64), ("n", ctypes.c_int32),
+                ("dtype", ctypes.c_int32), ("act", ctypes.c_int32), ("recompute", ctypes.c_int32),
+                ("r", ctypes.c_int64 * GROUP_MAX), ("d_out", ctypes.c_int64 * GROUP_MAX),
+                ("ldy", ctypes.c_int64 * GROUP_MAX), ("ldx", ctypes.c_int64), ("ldz", ctypes.c_int64)]
+
+
 _lib = None
 
 _P = ctypes.c_void_p
@@ -57,6 +67,10 @@ EXPORTS = {
     "dense_workspace_bytes": ([ctypes.POINTER(DenseDesc), ctypes.c_int], _SZ),
     "dense_fwd": ([ctypes.POINTER(DenseDesc), _P, _P, _P, _P, _SZ, _P], ctypes.c_int),
     "dense_bwd": ([ctypes.POINTER(DenseDesc), _P, _P, _P, _P, _P, _P, _SZ, _P], ctypes.c_int),
+    "cola_group_workspace_bytes": ([ctypes.POINTER(GroupDesc), ctypes.c_int], _SZ),
+    "cola_group_fwd": ([ctypes.POINTER(GroupDesc), _P, _P, _P, _P, _P, _P, _P, _SZ, _P], ctypes.c_int),
+    "cola_group_bwd": ([ctypes.POINTER(GroupDesc), _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _SZ, _P],
+                       ctypes.c_int),
     "cola_timing_enable": ([ctypes.c_int], ctypes.c_int),
     "cola_timing_reset": ([], ctypes.c_int),
     "cola_timing_read": ([ctypes.c_int, ctypes.POINTER(ctypes.c_int64), ctypes.POINTER(ctypes.c_double),
@@ -107,6 +121,50 @@ def desc(T, d_in, d_out, r, dtype="bf16", act="silu", recompute=False, ldx=0, ld
     return ColaDesc(T, d_in, d_out, r, ldx, ldy, ldz,
                     DTYPES[dtype] if isinstance(dtype, str) else int(dtype),
                     ACTS[act] if isinstance(act, str) else int(act), int(bool(recompute)))
+
+
+def group_desc(T, d_in, r, d_out, dtype="bf16", act="silu", recompute=False, ldx=0, ldz=0, ldy=None):
+    """Descriptor of n projections reading the same input (r, d_out, ldy: per projection)."""
+    n = len(r)
+    if len(d_out) != n or not 1 <= n <= GROUP_MAX:
+        raise ValueError("r and d_out need the same length, 1 .. %d" % GROUP_MAX)
+    ldy = list(ldy) if ldy is not None else [0] * n
+    pad = lambda v: (ctypes.c_int64 * GROUP_MAX)(*(list(v) + [0] * (GROUP_MAX - n)))
+    return GroupDesc(T, d_in, n, DTYPES[dtype] if isinstance(dtype, str) else int(dtype),
+                     ACTS[act] if isinstance(act, str) else int(act), int(bool(recompute)),
+                     pad(r), pad(d_out), pad(ldy), ldx, ldz)
+
+
+def _ptr_array(xs):
+    if xs is None:
+        return None, None
+    arr = (ctypes.c_void_p * len(xs))(*[_ptr(x) for x in xs])
+    return ctypes.cast(arr, ctypes.c_void_p), arr      # keep arr alive with the cast
+
+
+def group_workspace_bytes(d: GroupDesc, phase: int) -> int:
+    return int(lib().cola_group_workspace_bytes(ctypes.byref(d), phase))
+
+
+def group_fwd(d: GroupDesc, X, A_all, B, Y, Z_all, H_all, ws=None, ws_bytes=None, stream=None):
+    """Z_all = X A_all^T, H_all = sigma(Z_all), Y_p = H_p B_p^T (B, Y: lists)."""
+    if ws_bytes is None:
+        ws_bytes = ws.numel() * ws.element_size() if ws is not None else 0
+    pb, _kb = _ptr_array(B)
+    py, _ky = _ptr_array(Y)
+    _check(lib().cola_group_fwd(ctypes.byref(d), _ptr(X), _ptr(A_all), pb, py, _ptr(Z_all), _ptr(H_all),
+                                _ptr(ws), ws_bytes, _stream(stream)))
+
+
+def group_bwd(d: GroupDesc, dY, X, Z_all, H_all, A_all, B, dX, dA_all, dB, ws=None, ws_bytes=None, stream=None):
+    """dZ_p = (dY_p B_p) * sigma'(Z_p), dX = sum_p dZ_p A_p, dA_all = dZ_all^T X, dB_p = dY_p^T H_p."""
+    if ws_bytes is None:
+        ws_bytes = ws.numel() * ws.element_size() if ws is not None else 0
+    pdy, _k1 = _ptr_array(dY)
+    pb, _k2 = _ptr_array(B)
+    pdb, _k3 = _ptr_array(dB)
+    _check(lib().cola_group_bwd(ctypes.byref(d), pdy, _ptr(X), _ptr(Z_all), _ptr(H_all), _ptr(A_all), pb,
+                                _ptr(dX), _ptr(dA_all), pdb, _ptr(ws), ws_bytes, _stream(stream)))
 
 
 def dense_desc(T, d_in, d_out, dtype="bf16", ldx=0, ldy=0):

@@ -602,3 +602,243 @@ int cola_timing_read(int kc, int64_t* launches, double* ms, double* flops, doubl
 }
 
 }  // extern "C"
+
+// ---------------------------------------------------------------------------
+// grouped projections that read the same input
+// ---------------------------------------------------------------------------
+namespace {
+
+struct GDims {
+    int64_t T, d_in, ldx, ldz, R;
+    int n;
+    int64_t r[COLA_GROUP_MAX], d_out[COLA_GROUP_MAX], ldy[COLA_GROUP_MAX], off[COLA_GROUP_MAX];
+    bool bf16;
+    size_t esize;
+};
+
+int check_group(const cola_group_desc* d, GDims* out) {
+    if (!d) return COLA_ERR_INVALID_ARG;
+    if (d->n < 1 || d->n > COLA_GROUP_MAX) return COLA_ERR_INVALID_ARG;
+    GDims g{};
+    g.n = d->n;
+    g.R = 0;
+    for (int p = 0; p < g.n; ++p) {
+        // each projection must be a valid single layer (enums, shapes, pitches)
+        cola_desc c{};
+        c.T = d->T; c.d_in = d->d_in; c.d_out = d->d_out[p]; c.r = d->r[p];
+        c.ldx = d->ldx; c.ldy = d->ldy[p]; c.ldz = 0;
+        c.dtype = d->dtype; c.act = d->act; c.recompute = d->recompute;
+        Dims x;
+        const int st = check_desc(&c, &x);
+        if (st != COLA_OK) return st;
+        g.r[p] = x.r; g.d_out[p] = x.d_out; g.ldy[p] = x.ldy; g.off[p] = g.R;
+        g.R += x.r;
+        g.T = x.T; g.d_in = x.d_in; g.ldx = x.ldx; g.bf16 = x.bf16; g.esize = x.esize;
+    }
+    if (g.R > kMaxDim) return COLA_ERR_BAD_SHAPE;
+    g.ldz = d->ldz ? d->ldz : g.R;
+    if (g.ldz < g.R || g.ldz > kMaxDim) return COLA_ERR_BAD_SHAPE;
+    if ((double)g.T * (double)g.ldz > 4.0e18 || (double)g.R * (double)g.d_in > 4.0e18) return COLA_ERR_BAD_SHAPE;
+    *out = g;
+    return COLA_OK;
+}
+
+// Workspace: [H_all copy (CoLA-M)] [repacked A_all] [repacked B_p ...]
+struct GFwdPlan {
+    int64_t ldw;
+    size_t off_h, total;
+    Pack pa, pb[COLA_GROUP_MAX];
+};
+
+GFwdPlan plan_group_fwd(const GDims& g, bool recompute) {
+    GFwdPlan p;
+    p.ldw = g.bf16 ? (g.R + 7) / 8 * 8 : (g.R + 3) / 4 * 4;
+    p.off_h = 0;
+    const size_t hbytes = recompute ? align256((size_t)g.T * (size_t)p.ldw * g.esize) : 0;
+    p.pa = plan_pack(g.bf16, g.R, g.d_in, hbytes);
+    size_t next = p.pa.off + p.pa.bytes;
+    for (int q = 0; q < g.n; ++q) {
+        p.pb[q] = plan_pack(g.bf16, g.d_out[q], g.r[q], next);
+        next = p.pb[q].off + p.pb[q].bytes;
+    }
+    p.total = g.T == 0 ? 0 : next;
+    return p;
+}
+
+// Workspace: [dZ_all] [H_all (CoLA-M)] [dA partials] [dB partials, reused
+// projection after projection] [repacked A_all] [repacked B_p ...]
+struct GBwdPlan {
+    int64_t ldw;
+    size_t off_dz, off_h, off_pa, off_pb, total;
+    Split sa, sb[COLA_GROUP_MAX];
+    Pack wa, wb[COLA_GROUP_MAX];
+};
+
+GBwdPlan plan_group_bwd(const GDims& g, bool recompute) {
+    GBwdPlan p;
+    p.ldw = g.bf16 ? (g.R + 7) / 8 * 8 : (g.R + 3) / 4 * 4;
+    const size_t zbytes = align256((size_t)g.T * (size_t)p.ldw * g.esize);
+    p.off_dz = 0;
+    p.off_h = zbytes;
+    p.off_pa = p.off_h + (recompute ? zbytes : 0);
+    p.sa = plan_split(g.bf16, g.R, g.d_in, g.T, TAG_BWD_DA);
+    const size_t pa = p.sa.splits > 1 ? align256((size_t)p.sa.splits * (size_t)(g.R * g.d_in) * 4) : 0;
+    p.off_pb = p.off_pa + pa;
+    size_t pb = 0;
+    for (int q = 0; q < g.n; ++q) {
+        p.sb[q] = plan_split(g.bf16, g.d_out[q], g.r[q], g.T, TAG_BWD_DB);
+        const size_t b = p.sb[q].splits > 1 ? align256((size_t)p.sb[q].splits * (size_t)(g.d_out[q] * g.r[q]) * 4) : 0;
+        if (b > pb) pb = b;
+    }
+    p.wa = plan_pack(g.bf16, g.R, g.d_in, p.off_pb + pb);
+    size_t next = p.wa.off + p.wa.bytes;
+    for (int q = 0; q < g.n; ++q) {
+        p.wb[q] = plan_pack(g.bf16, g.d_out[q], g.r[q], next);
+        next = p.wb[q].off + p.wb[q].bytes;
+    }
+    p.total = g.T == 0 ? 0 : next;
+    return p;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t cola_group_workspace_bytes(const cola_group_desc* desc, int phase) {
+    GDims g;
+    if (check_group(desc, &g) != COLA_OK) return 0;
+    if (phase == 0) return plan_group_fwd(g, desc->recompute == 1).total;
+    if (phase == 1) return plan_group_bwd(g, desc->recompute == 1).total;
+    return 0;
+}
+
+int cola_group_fwd(const cola_group_desc* desc, const void* X, const void* A_all, const void* const* B,
+                   void* const* Y, void* Z_all, void* H_all, void* ws, size_t ws_bytes, cola_stream_t stream) {
+    return guarded([&]() -> int {
+        GDims g;
+        int st = check_group(desc, &g);
+        if (st != COLA_OK) return st;
+        const bool recompute = desc->recompute == 1;
+        if (recompute ? (H_all != nullptr) : (H_all == nullptr && g.T > 0)) return COLA_ERR_INVALID_ARG;
+        if (g.T == 0) return COLA_OK;
+        if (!X || !A_all || !B || !Y || !Z_all) return COLA_ERR_INVALID_ARG;
+        for (int q = 0; q < g.n; ++q)
+            if (!B[q] || !Y[q]) return COLA_ERR_INVALID_ARG;
+        const GFwdPlan p = plan_group_fwd(g, recompute);
+        if (p.total > 0 && (!ws || ws_bytes < p.total)) return COLA_ERR_WORKSPACE;
+        hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+        char* w = reinterpret_cast<char*>(ws);
+        char* Hbuf = recompute ? w + p.off_h : reinterpret_cast<char*>(H_all);
+        const int64_t ldh = recompute ? p.ldw : g.ldz;
+        const double es = (double)g.esize;
+
+        const void* Aw;
+        int64_t lda;
+        hipError_t e = use_weight(p.pa, A_all, g.R, g.d_in, w, &Aw, &lda, s);
+        if (e != hipSuccess) return hip_fail(e, "pack_rows");
+
+        // K1 for every projection at once: Z_all = X A_all^T, H_all = sigma(Z_all)
+        GemmArgs k1 = make_args(TAG_FWD_Z, g.T, g.R, g.d_in, X, g.ldx, KMAJ, Aw, lda, KMAJ, Z_all, g.ldz, EPI_Z_H,
+                                desc->act);
+        k1.aux = Hbuf;
+        k1.ldaux = ldh;
+        const double b1 = es * ((double)g.T * g.d_in + (double)g.R * g.d_in + 2.0 * g.T * g.R);
+        e = timed(COLA_KC_FWD_Z, gemm_flops(g.T, g.R, g.d_in), b1, s, [&] { return gemm(k1, g.bf16, s); });
+        if (e != hipSuccess) return hip_fail(e, "fwd_z_sigma");
+
+        // K2 per projection: Y_p = H_p B_p^T
+        for (int q = 0; q < g.n; ++q) {
+            const void* Bw;
+            int64_t ldb;
+            e = use_weight(p.pb[q], B[q], g.d_out[q], g.r[q], w, &Bw, &ldb, s);
+            if (e != hipSuccess) return hip_fail(e, "pack_rows");
+            GemmArgs k2 = make_args(TAG_FWD_Y, g.T, g.d_out[q], g.r[q], Hbuf + g.off[q] * g.esize, ldh, KMAJ, Bw,
+                                    ldb, KMAJ, Y[q], g.ldy[q], EPI_STORE, desc->act);
+            const double b2 = es * ((double)g.T * g.r[q] + (double)g.d_out[q] * g.r[q] + (double)g.T * g.d_out[q]);
+            e = timed(COLA_KC_FWD_Y, gemm_flops(g.T, g.d_out[q], g.r[q]), b2, s, [&] { return gemm(k2, g.bf16, s); });
+            if (e != hipSuccess) return hip_fail(e, "fwd_y");
+        }
+        return COLA_OK;
+    });
+}
+
+int cola_group_bwd(const cola_group_desc* desc, const void* const* dY, const void* X, const void* Z_all,
+                   const void* H_all, const void* A_all, const void* const* B, void* dX, float* dA_all,
+                   float* const* dB, void* ws, size_t ws_bytes, cola_stream_t stream) {
+    return guarded([&]() -> int {
+        GDims g;
+        int st = check_group(desc, &g);
+        if (st != COLA_OK) return st;
+        const bool recompute = desc->recompute == 1;
+        if (recompute ? (H_all != nullptr) : (H_all == nullptr && g.T > 0)) return COLA_ERR_INVALID_ARG;
+        if (!dA_all || !dB) return COLA_ERR_INVALID_ARG;
+        for (int q = 0; q < g.n; ++q)
+            if (!dB[q]) return COLA_ERR_INVALID_ARG;
+        hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+        if (g.T == 0) {
+            // empty batch: the token sums are empty
+            hipError_t e = timed(COLA_KC_FILL, 0.0, 4.0 * g.R * g.d_in, s,
+                                 [&] { return launch_fill_zero(dA_all, g.R * g.d_in, s); });
+            for (int q = 0; q < g.n && e == hipSuccess; ++q)
+                e = timed(COLA_KC_FILL, 0.0, 4.0 * g.d_out[q] * g.r[q], s,
+                          [&] { return launch_fill_zero(dB[q], g.d_out[q] * g.r[q], s); });
+            return e == hipSuccess ? COLA_OK : hip_fail(e, "fill_zero");
+        }
+        if (!dY || !X || !Z_all || !A_all || !B || !dX) return COLA_ERR_INVALID_ARG;
+        for (int q = 0; q < g.n; ++q)
+            if (!dY[q] || !B[q]) return COLA_ERR_INVALID_ARG;
+        const GBwdPlan p = plan_group_bwd(g, recompute);
+        if (!ws || ws_bytes < p.total) return COLA_ERR_WORKSPACE;
+
+        char* w = reinterpret_cast<char*>(ws);
+        char* dZ = w + p.off_dz;
+        const char* Hbuf = recompute ? w + p.off_h : reinterpret_cast<const char*>(H_all);
+        const int64_t ldh = recompute ? p.ldw : g.ldz;
+        const double es = (double)g.esize;
+        const void* Aw;
+        int64_t lda;
+        hipError_t e = use_weight(p.wa, A_all, g.R, g.d_in, w, &Aw, &lda, s);
+        if (e != hipSuccess) return hip_fail(e, "pack_rows");
+
+        // K3 per projection: dZ_p = (dY_p B_p) (.) sigma'(Z_p)  [+ H_p for CoLA-M]
+        for (int q = 0; q < g.n; ++q) {
+            const void* Bw;
+            int64_t ldb;
+            e = use_weight(p.wb[q], B[q], g.d_out[q], g.r[q], w, &Bw, &ldb, s);
+            if (e != hipSuccess) return hip_fail(e, "pack_rows");
+            GemmArgs k3 = make_args(TAG_BWD_DZ, g.T, g.r[q], g.d_out[q], dY[q], g.ldy[q], KMAJ, Bw, ldb, MNMAJ,
+                                    dZ + g.off[q] * g.esize, p.ldw, EPI_DZ, desc->act);
+            k3.zin = reinterpret_cast<const char*>(Z_all) + g.off[q] * g.esize;
+            k3.ldzin = g.ldz;
+            k3.aux = recompute ? (void*)(w + p.off_h + g.off[q] * g.esize) : nullptr;
+            k3.ldaux = p.ldw;
+            const double b3 = es * ((double)g.T * g.d_out[q] + (double)g.d_out[q] * g.r[q] +
+                                    (double)g.T * g.r[q] * (recompute ? 3.0 : 2.0));
+            e = timed(COLA_KC_BWD_DZ, gemm_flops(g.T, g.r[q], g.d_out[q]), b3, s, [&] { return gemm(k3, g.bf16, s); });
+            if (e != hipSuccess) return hip_fail(e, "bwd_dz");
+        }
+
+        // K4 for every projection at once: dX = dZ_all A_all = sum_p dZ_p A_p
+        GemmArgs k4 = make_args(TAG_BWD_DX, g.T, g.d_in, g.R, dZ, p.ldw, KMAJ, Aw, lda, MNMAJ, dX, g.ldx, EPI_STORE,
+                                desc->act);
+        const double b4 = es * ((double)g.T * g.R + (double)g.R * g.d_in + (double)g.T * g.d_in);
+        e = timed(COLA_KC_BWD_DX, gemm_flops(g.T, g.d_in, g.R), b4, s, [&] { return gemm(k4, g.bf16, s); });
+        if (e != hipSuccess) return hip_fail(e, "bwd_dx");
+
+        // K5 for every projection at once: dA_all = dZ_all^T X
+        st = wgrad(g.bf16, g.R, g.d_in, g.T, dZ, p.ldw, X, g.ldx, dA_all, p.sa,
+                   reinterpret_cast<float*>(w + p.off_pa), COLA_KC_BWD_DA,
+                   es * ((double)g.T * g.R + (double)g.T * g.d_in), s);
+        if (st != COLA_OK) return st;
+        // K6 per projection: dB_p = dY_p^T H_p
+        for (int q = 0; q < g.n; ++q) {
+            st = wgrad(g.bf16, g.d_out[q], g.r[q], g.T, dY[q], g.ldy[q], Hbuf + g.off[q] * g.esize, ldh, dB[q],
+                       p.sb[q], reinterpret_cast<float*>(w + p.off_pb), COLA_KC_BWD_DB,
+                       es * ((double)g.T * g.d_out[q] + (double)g.T * g.r[q]), s);
+            if (st != COLA_OK) return st;
+        }
+        return COLA_OK;
+    });
+}
+
+}  // extern "C"

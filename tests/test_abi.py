@@ -26,7 +26,8 @@ def test_header_declares_expected_calls():
     names = declared_functions()
     for n in ("cola_fwd", "cola_bwd", "cola_workspace_bytes", "cola_strerror", "cola_abi_version",
               "dense_fwd", "dense_bwd", "dense_workspace_bytes", "cola_timing_enable",
-              "cola_timing_read", "cola_timing_reset", "cola_kernel_name"):
+              "cola_timing_read", "cola_timing_reset", "cola_kernel_name",
+              "cola_group_fwd", "cola_group_bwd", "cola_group_workspace_bytes"):
         assert n in names
 
 
@@ -176,3 +177,75 @@ def test_binding_raises_on_error():
     with pytest.raises(cola.ColaError) as e:
         cola.fwd(d, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, stream=0)
     assert e.value.status == cola.ERR_BAD_SHAPE
+
+
+# --------------------------------------------------------------------------
+# grouped projections (shared input): validation before any GPU work
+# --------------------------------------------------------------------------
+
+def group_fwd_status(d, X=FAKE, A=FAKE, B=FAKE, Y=FAKE, Z=FAKE, H=FAKE, ws=None, ws_bytes=0, n=None):
+    n = d.n if (d is not None and n is None) else (n or 1)
+    arr = lambda v: None if v is None else ctypes.cast((ctypes.c_void_p * max(n, 1))(*([v] * max(n, 1))),
+                                                      ctypes.c_void_p)
+    p = ctypes.byref(d) if d is not None else None
+    return cola.lib().cola_group_fwd(p, X, A, arr(B), arr(Y), Z, H, ws, ws_bytes, None)
+
+
+def test_group_struct_layout_matches_header():
+    # offsets of the C struct (compiled from include/cola.h) against the binding's
+    src = os.path.join(os.path.dirname(os.path.abspath(__file__)), "_sz.c")
+    exe = os.path.join(os.path.dirname(os.path.abspath(__file__)), "_sz")
+    code = ('#include "cola.h"\n#include <stdio.h>\n#include <stddef.h>\n'
+            'int main(void){printf("%zu %zu %zu %zu %zu\\n", sizeof(cola_group_desc),'
+            'offsetof(cola_group_desc, r), offsetof(cola_group_desc, d_out),'
+            'offsetof(cola_group_desc, ldy), offsetof(cola_group_desc, ldz)); return 0;}\n')
+    try:
+        open(src, "w").write(code)
+        subprocess.run(["gcc", "-I", os.path.join(ROOT, "include"), src, "-o", exe], check=True)
+        got = [int(v) for v in subprocess.run([exe], capture_output=True, text=True, check=True).stdout.split()]
+    finally:
+        for f in (src, exe):
+            if os.path.exists(f):
+                os.remove(f)
+    G = cola.GroupDesc
+    assert got == [ctypes.sizeof(G), G.r.offset, G.d_out.offset, G.ldy.offset, G.ldz.offset]
+
+
+def test_group_invalid_descriptors():
+    ok = cola.group_desc(64, 32, [8, 16, 8], [32, 32, 16])
+    assert cola.group_workspace_bytes(ok, 1) > 0
+    bad = [
+        cola.group_desc(64, 32, [8], [32], dtype=7),
+        cola.group_desc(64, 32, [8], [32], act=3),
+        cola.group_desc(64, 0, [8], [32]),
+        cola.group_desc(64, 32, [8, 0], [32, 32]),
+        cola.group_desc(64, 32, [8, 8], [32, 0]),
+        cola.group_desc(-1, 32, [8], [32]),
+        cola.group_desc(64, 32, [8, 8], [32, 32], ldz=15),       # ldz < R = 16
+        cola.group_desc(64, 32, [8], [32], ldx=31),
+        cola.group_desc(64, 32, [8], [32], ldy=[31]),
+    ]
+    for d in bad:
+        assert cola.group_workspace_bytes(d, 0) == 0
+        assert cola.group_workspace_bytes(d, 1) == 0
+        assert group_fwd_status(d) in (cola.ERR_INVALID_ARG, cola.ERR_BAD_SHAPE)
+    for n in (0, 9):
+        d = cola.group_desc(64, 32, [8], [32])
+        d.n = n
+        assert cola.group_workspace_bytes(d, 0) == 0
+        assert group_fwd_status(d, n=1) == cola.ERR_INVALID_ARG
+    assert group_fwd_status(None) == cola.ERR_INVALID_ARG
+
+
+def test_group_pointer_and_workspace_checks():
+    d = cola.group_desc(64, 32, [8, 16], [32, 24])
+    assert group_fwd_status(d, H=None) == cola.ERR_INVALID_ARG          # CoLA needs H
+    assert group_fwd_status(d, X=None) == cola.ERR_INVALID_ARG
+    assert group_fwd_status(d, B=None) == cola.ERR_INVALID_ARG
+    assert group_fwd_status(d, Y=None) == cola.ERR_INVALID_ARG
+    m = cola.group_desc(64, 32, [8, 16], [32, 24], recompute=True)
+    assert group_fwd_status(m) == cola.ERR_INVALID_ARG                  # CoLA-M takes no H
+    assert group_fwd_status(m, H=None) == cola.ERR_WORKSPACE            # H_all copy needs workspace
+    # an empty batch enqueues nothing
+    e = cola.group_desc(0, 32, [8, 16], [32, 24])
+    assert group_fwd_status(e, X=None, A=None, B=None, Y=None, Z=None, H=None) == cola.OK
