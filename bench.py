@@ -8,7 +8,10 @@ Reported value: algorithmic TFLOP/s = sum over projections of
 6 T r (d_in + d_out) per step (Sec. 3.4: 2MNK per GEMM, sigma excluded),
 divided by the measured step time.  Inputs are resident in HBM before the
 timed region.  Also measured on the same harness: the CoLA-M step and the
-dense full-rank step (6 T d_in d_out), for tokens/s and the speedup.
+dense full-rank step (6 T d_in d_out), for tokens/s and the speedup; the
+block with same-input projections grouped (q+k+v and gate+up share one
+input: one GEMM for their Z, dX and dA each); and the inference forward of
+that block (nothing kept for a backward pass) against the dense forward.
 
 Prints ONE JSON line.
 """
@@ -43,6 +46,8 @@ def parse():
     ap.add_argument("--no-cola-m", action="store_true")
     ap.add_argument("--cpu-tokens", type=int, default=8192,
                     help="tokens per projection in the oracle's CPU sample")
+    ap.add_argument("--no-fused", action="store_true",
+                    help="skip the block with same-input projections grouped (q,k,v and gate,up)")
     ap.add_argument("--only", choices=["cola", "cola_m", "dense"], default=None,
                     help="run only one mode (profiling)")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -175,6 +180,7 @@ class Projection:
         self.desc_m = cola.desc(T, d_in, d_out, r, dtype, "silu", True, self.ldx, self.ldy, self.ldz)
         self.ddesc = cola.dense_desc(T, d_in, d_out, dtype, self.ldx, self.ldy)
         self.ws_need = max(cola.workspace_bytes(self.desc, 0), cola.workspace_bytes(self.desc, 1),
+                           cola.workspace_bytes(self.desc, 2),
                            cola.workspace_bytes(self.desc_m, 0) if recompute_too else 0,
                            cola.workspace_bytes(self.desc_m, 1) if recompute_too else 0,
                            cola.dense_workspace_bytes(self.ddesc, 0) if dense else 0,
@@ -196,10 +202,59 @@ class Projection:
             cola.bwd(self.desc, self.dY, self.X, self.Z, self.H, self.A, self.B, self.dX, self.dA,
                      self.dB, ws)
 
+    def infer(self, ws):
+        from paper_2502_10940_amd import cola
+        cola.infer(self.desc, self.X, self.A, self.B, self.Y, ws)
+
+    def dense_fwd(self, ws):
+        from paper_2502_10940_amd import cola
+        cola.dense_fwd(self.ddesc, self.X, self.W, self.Y, ws)
+
     def dense_step(self, ws):
         from paper_2502_10940_amd import cola
         cola.dense_fwd(self.ddesc, self.X, self.W, self.Y, ws)
         cola.dense_bwd(self.ddesc, self.dY, self.X, self.W, self.dX, self.dW, ws)
+
+
+class Group:
+    """Projections that read the same input (q, k, v; gate, up) run through the
+    grouped entry points: the first member's X is the shared input; the members'
+    weights, output and gradient buffers are reused."""
+
+    def __init__(self, members, dtype):
+        import torch
+        from paper_2502_10940_amd import cola
+        from paper_2502_10940_amd import inputs as I
+        self.m = members
+        p0 = members[0]
+        T, d_in = p0.T, p0.d_in
+        ranks = [p.r for p in members]
+        self.R = sum(ranks)
+        tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+        dev = "cuda:0"
+        self.ldz = I.padded_ld(self.R, dtype)
+        self.A_all = torch.cat([p.A for p in members], dim=0).contiguous()
+        self.Z = torch.empty((T, self.ldz), dtype=tdt, device=dev)
+        self.H = torch.empty((T, self.ldz), dtype=tdt, device=dev)
+        self.dA = torch.empty((self.R, d_in), dtype=torch.float32, device=dev)
+        self.desc = cola.group_desc(T, d_in, ranks, [p.d_out for p in members], dtype, "silu", False,
+                                    ldx=p0.ldx, ldz=self.ldz, ldy=[p.ldy for p in members])
+        self.ws_need = max(cola.group_workspace_bytes(self.desc, p) for p in (0, 1, 2))
+
+    def fwd(self, ws):
+        from paper_2502_10940_amd import cola
+        p0 = self.m[0]
+        cola.group_fwd(self.desc, p0.X, self.A_all, [p.B for p in self.m], [p.Y for p in self.m], self.Z, self.H, ws)
+
+    def infer(self, ws):
+        from paper_2502_10940_amd import cola
+        cola.group_infer(self.desc, self.m[0].X, self.A_all, [p.B for p in self.m], [p.Y for p in self.m], ws)
+
+    def bwd(self, ws):
+        from paper_2502_10940_amd import cola
+        p0 = self.m[0]
+        cola.group_bwd(self.desc, [p.dY for p in self.m], p0.X, self.Z, self.H, self.A_all, [p.B for p in self.m],
+                       p0.dX, self.dA, [p.dB for p in self.m], ws)
 
 
 def timed_steps(step, steps, warmup):
@@ -311,7 +366,14 @@ def main():
     t0 = time.time()
     projs = [Projection(args.workload, name, idx, d_in, d_out, r, T, dtype, do_dense, do_m)
              for name, idx, d_in, d_out in I.projections(args.workload)]
-    ws = torch.empty(max(p.ws_need for p in projs), dtype=torch.uint8, device="cuda:0")
+    do_fused = not args.no_fused and args.only is None and args.workload != 1
+    units = []          # the fused block: groups for same-input projections, single layers otherwise
+    if do_fused:
+        by = {p.name: p for p in projs}
+        units = [Group([by["q"], by["k"], by["v"]], dtype), by["o"], Group([by["gate"], by["up"]], dtype),
+                 by["down"]]
+    ws_need = max([p.ws_need for p in projs] + [u.ws_need for u in units if isinstance(u, Group)])
+    ws = torch.empty(ws_need, dtype=torch.uint8, device="cuda:0")
     setup_s = time.time() - t0
 
     def step_cola():
@@ -326,9 +388,23 @@ def main():
         for p in reversed(projs):
             p.bwd(ws, True)
 
+    def step_fused():
+        for u in units:
+            u.fwd(ws)
+        for u in reversed(units):
+            u.bwd(ws)
+
     def step_dense():
         for p in projs:
             p.dense_step(ws)
+
+    def step_infer():
+        for u in units:
+            u.infer(ws)
+
+    def step_dense_infer():
+        for p in projs:
+            p.dense_fwd(ws)
 
     flops_cola = sum(algo_flops_cola(T, p.d_in, p.d_out, r) for p in projs)
     flops_dense = sum(algo_flops_dense(T, p.d_in, p.d_out) for p in projs)
@@ -352,6 +428,11 @@ def main():
         res["cola_m"] = timed_steps(step_cola_m, args.steps, args.warmup)
     if do_dense:
         res["dense"] = timed_steps(step_dense, args.steps, args.warmup)
+    if do_fused:
+        res["fused"] = timed_steps(step_fused, args.steps, args.warmup)
+        res["infer"] = timed_steps(step_infer, args.steps, args.warmup)
+        if do_dense:
+            res["dense_infer"] = timed_steps(step_dense_infer, args.steps, args.warmup)
 
     main_mode = "cola" if do_cola else ("cola_m" if do_m else "dense")
     ms = res[main_mode]
@@ -389,6 +470,23 @@ def main():
             out["speedup_vs_dense"] = round(res["dense"] / res["cola"], 3)
         if "cola_m" in res:
             out["cola_m"]["speedup_vs_dense"] = round(res["dense"] / res["cola_m"], 3)
+    if "fused" in res:
+        # same algorithmic flops; q, k, v read one X and gate, up another
+        out["fused_block"] = {"ms_per_step": round(res["fused"], 4),
+                              "tflops": round(flops_cola / (res["fused"] * 1e9), 2),
+                              "tokens_per_s": round(T / (res["fused"] / 1e3), 1),
+                              "groups": ["q+k+v", "o", "gate+up", "down"]}
+        if "dense" in res:
+            out["fused_block"]["speedup_vs_dense"] = round(res["dense"] / res["fused"], 3)
+    if "infer" in res:
+        # forward only, nothing kept for a backward pass; grouped as fused_block
+        fl = sum(2.0 * T * r * (p.d_in + p.d_out) for p in projs)
+        out["inference"] = {"ms_per_step": round(res["infer"], 4),
+                            "tflops": round(fl / (res["infer"] * 1e9), 2),
+                            "tokens_per_s": round(T / (res["infer"] / 1e3), 1)}
+        if "dense_infer" in res:
+            out["inference"]["dense_tokens_per_s"] = round(T / (res["dense_infer"] / 1e3), 1)
+            out["inference"]["speedup_vs_dense"] = round(res["dense_infer"] / res["infer"], 3)
     if kernels:
         dom = max(kernels, key=lambda k: kernels[k]["total_ms"])
         kd = kernels[dom]

@@ -98,10 +98,12 @@ int cola_abi_version(void);
 /* Text for a status code; for COLA_ERR_HIP the text of the last failure. */
 const char* cola_strerror(int status);
 
-/* Workspace bytes for phase 0 (cola_fwd) or 1 (cola_bwd); 0 on an invalid
- * descriptor.  Forward needs T*r elements when recompute = 1 (H lives only
- * there), else nothing.  Backward needs dZ (T*r elements), H again when
- * recompute = 1, and the fp32 partial sums of dA and dB. */
+/* Workspace bytes for phase 0 (cola_fwd), 1 (cola_bwd) or 2 (cola_infer);
+ * 0 on an invalid descriptor or phase.  Forward needs T*r elements when
+ * recompute = 1 (H lives only there), else nothing.  Backward needs dZ (T*r
+ * elements), H again when recompute = 1, and the fp32 partial sums of dA and
+ * dB.  Inference needs T*r elements for H whatever recompute says.  Weights
+ * whose row length is not a multiple of 8 (bf16) add a padded copy. */
 size_t cola_workspace_bytes(const cola_desc* desc, int phase);
 
 /* Forward (Eq. main-fwd): Z = X A^T, H = sigma(Z), Y = H B^T.
@@ -124,6 +126,16 @@ int cola_bwd(const cola_desc* desc,
              const void* A, const void* B,
              void* dX, float* dA, float* dB,
              void* ws, size_t ws_bytes, cola_stream_t stream);
+
+/* Inference forward (Eq. main-fwd with nothing kept for a backward pass; the
+ * paper's inference comparison, App. "Inference Efficiency"):
+ *   Y = sigma(X A^T) B^T
+ * H lives only in the workspace (phase 2) and Z is never stored.  Y is
+ * bitwise the Y of cola_fwd on the same inputs.  desc->recompute is ignored;
+ * X, A, B, Y as in cola_fwd.  T = 0 enqueues nothing. */
+int cola_infer(const cola_desc* desc,
+               const void* X, const void* A, const void* B, void* Y,
+               void* ws, size_t ws_bytes, cola_stream_t stream);
 
 /* ------------------------------------------------------------------------
  * Grouped projections that read the same input (Sec. 3.2 applied to every
@@ -165,14 +177,22 @@ typedef struct {
     int64_t ldz;                      /* row pitch of Z_all and H_all, 0 = R */
 } cola_group_desc;
 
-/* Workspace bytes for phase 0 (forward) or 1 (backward); 0 on an invalid
- * descriptor. */
+/* Workspace bytes for phase 0 (forward), 1 (backward) or 2 (inference); 0
+ * on an invalid descriptor or phase. */
 size_t cola_group_workspace_bytes(const cola_group_desc* desc, int phase);
 
 int cola_group_fwd(const cola_group_desc* desc,
                    const void* X, const void* A_all, const void* const* B,
                    void* const* Y, void* Z_all, void* H_all,
                    void* ws, size_t ws_bytes, cola_stream_t stream);
+
+/* Inference forward of the group (cola_infer per projection, with the
+ * shared-input GEMM run once): Y_p = sigma(X A_p^T) B_p^T, H_all only in
+ * the workspace (phase 2), no Z.  desc->recompute and desc->ldz are ignored;
+ * each Y_p is bitwise that of cola_group_fwd. */
+int cola_group_infer(const cola_group_desc* desc,
+                     const void* X, const void* A_all, const void* const* B,
+                     void* const* Y, void* ws, size_t ws_bytes, cola_stream_t stream);
 
 /* dX is overwritten with sum_p dZ_p A_p; dA_all and every dB_p are
  * overwritten (fp32).  T = 0 writes dA_all = 0 and dB_p = 0. */
@@ -213,7 +233,8 @@ typedef enum {
     COLA_KC_DENSE_DX = 8,  /* dX = dY W                                */
     COLA_KC_DENSE_DW = 9,  /* dW = dY^T X                              */
     COLA_KC_FILL = 10,     /* zero fill (empty batches)                */
-    COLA_KC_COUNT = 11
+    COLA_KC_INFER_H = 11,  /* H = sigma(X A^T), Z not kept (inference) */
+    COLA_KC_COUNT = 12
 } cola_kernel_class;
 
 /* Per-class totals since the last reset: launches, elapsed milliseconds,

@@ -21,7 +21,7 @@ ACTS = {"identity": ACT_IDENTITY, "silu": ACT_SILU, "gelu": ACT_GELU}
 OK, ERR_INVALID_ARG, ERR_BAD_SHAPE, ERR_WORKSPACE, ERR_HIP, ERR_UNSUPPORTED = range(6)
 
 KERNEL_CLASSES = ("fwd_z_sigma", "fwd_y", "bwd_dz", "bwd_dx", "bwd_da", "bwd_db",
-                  "reduce_splits", "dense_fwd", "dense_dx", "dense_dw", "fill_zero")
+                  "reduce_splits", "dense_fwd", "dense_dx", "dense_dw", "fill_zero", "infer_h")
 
 
 class ColaError(RuntimeError):
@@ -71,6 +71,8 @@ EXPORTS = {
     "cola_group_fwd": ([ctypes.POINTER(GroupDesc), _P, _P, _P, _P, _P, _P, _P, _SZ, _P], ctypes.c_int),
     "cola_group_bwd": ([ctypes.POINTER(GroupDesc), _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _SZ, _P],
                        ctypes.c_int),
+    "cola_infer": ([ctypes.POINTER(ColaDesc), _P, _P, _P, _P, _P, _SZ, _P], ctypes.c_int),
+    "cola_group_infer": ([ctypes.POINTER(GroupDesc), _P, _P, _P, _P, _P, _SZ, _P], ctypes.c_int),
     "cola_timing_enable": ([ctypes.c_int], ctypes.c_int),
     "cola_timing_reset": ([], ctypes.c_int),
     "cola_timing_read": ([ctypes.c_int, ctypes.POINTER(ctypes.c_int64), ctypes.POINTER(ctypes.c_double),
@@ -156,6 +158,16 @@ def group_fwd(d: GroupDesc, X, A_all, B, Y, Z_all, H_all, ws=None, ws_bytes=None
                                 _ptr(ws), ws_bytes, _stream(stream)))
 
 
+def group_infer(d: GroupDesc, X, A_all, B, Y, ws=None, ws_bytes=None, stream=None):
+    """Inference forward: Y_p = sigma(X A_p^T) B_p^T, nothing kept for a backward pass."""
+    if ws_bytes is None:
+        ws_bytes = ws.numel() * ws.element_size() if ws is not None else 0
+    pb, _kb = _ptr_array(B)
+    py, _ky = _ptr_array(Y)
+    _check(lib().cola_group_infer(ctypes.byref(d), _ptr(X), _ptr(A_all), pb, py, _ptr(ws), ws_bytes,
+                                  _stream(stream)))
+
+
 def group_bwd(d: GroupDesc, dY, X, Z_all, H_all, A_all, B, dX, dA_all, dB, ws=None, ws_bytes=None, stream=None):
     """dZ_p = (dY_p B_p) * sigma'(Z_p), dX = sum_p dZ_p A_p, dA_all = dZ_all^T X, dB_p = dY_p^T H_p."""
     if ws_bytes is None:
@@ -185,6 +197,14 @@ def fwd(d: ColaDesc, X, A, B, Y, Z, H, ws=None, ws_bytes=None, stream=None):
         ws_bytes = ws.numel() * ws.element_size() if ws is not None else 0
     _check(lib().cola_fwd(ctypes.byref(d), _ptr(X), _ptr(A), _ptr(B), _ptr(Y), _ptr(Z), _ptr(H),
                           _ptr(ws), ws_bytes, _stream(stream)))
+
+
+def infer(d: ColaDesc, X, A, B, Y, ws=None, ws_bytes=None, stream=None):
+    """Inference forward: Y = sigma(X A^T) B^T, nothing kept for a backward pass."""
+    if ws_bytes is None:
+        ws_bytes = ws.numel() * ws.element_size() if ws is not None else 0
+    _check(lib().cola_infer(ctypes.byref(d), _ptr(X), _ptr(A), _ptr(B), _ptr(Y), _ptr(ws), ws_bytes,
+                            _stream(stream)))
 
 
 def bwd(d: ColaDesc, dY, X, Z, H, A, B, dX, dA, dB, ws=None, ws_bytes=None, stream=None):

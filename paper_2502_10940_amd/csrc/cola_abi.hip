@@ -348,7 +348,7 @@ const char* cola_strerror(int status) {
 const char* cola_kernel_name(int kc) {
     static const char* names[COLA_KC_COUNT] = {
         "fwd_z_sigma", "fwd_y", "bwd_dz", "bwd_dx", "bwd_da", "bwd_db",
-        "reduce_splits", "dense_fwd", "dense_dx", "dense_dw", "fill_zero"};
+        "reduce_splits", "dense_fwd", "dense_dx", "dense_dw", "fill_zero", "infer_h"};
     if (kc < 0 || kc >= COLA_KC_COUNT) return "invalid";
     return names[kc];
 }
@@ -358,6 +358,7 @@ size_t cola_workspace_bytes(const cola_desc* desc, int phase) {
     if (check_desc(desc, &x) != COLA_OK) return 0;
     if (phase == 0) return fwd_ws(x, desc->recompute == 1);
     if (phase == 1) return plan_bwd(x, desc->recompute == 1).total;
+    if (phase == 2) return fwd_ws(x, true);     // inference: H in the workspace, as CoLA-M's forward
     return 0;
 }
 
@@ -709,8 +710,84 @@ size_t cola_group_workspace_bytes(const cola_group_desc* desc, int phase) {
     if (check_group(desc, &g) != COLA_OK) return 0;
     if (phase == 0) return plan_group_fwd(g, desc->recompute == 1).total;
     if (phase == 1) return plan_group_bwd(g, desc->recompute == 1).total;
+    if (phase == 2) return plan_group_fwd(g, true).total;
     return 0;
 }
+
+}  // extern "C"
+
+namespace {
+
+// Forward of a validated group with the pointers checked.  Z_all == NULL is
+// the inference forward: K1 stores only H (into the workspace), nothing is
+// kept for a backward pass.
+int group_forward(const GDims& g, int act, const void* X, const void* A_all, const void* const* B,
+                  void* const* Y, void* Z_all, void* H_all, bool h_in_ws, char* w, hipStream_t s) {
+    const GFwdPlan p = plan_group_fwd(g, h_in_ws);
+    char* Hbuf = h_in_ws ? w + p.off_h : reinterpret_cast<char*>(H_all);
+    const int64_t ldh = h_in_ws ? p.ldw : g.ldz;
+    const double es = (double)g.esize;
+
+    const void* Aw;
+    int64_t lda;
+    hipError_t e = use_weight(p.pa, A_all, g.R, g.d_in, w, &Aw, &lda, s);
+    if (e != hipSuccess) return hip_fail(e, "pack_rows");
+
+    // K1 for every projection at once: Z_all = X A_all^T, H_all = sigma(Z_all)
+    if (Z_all) {
+        GemmArgs k1 = make_args(TAG_FWD_Z, g.T, g.R, g.d_in, X, g.ldx, KMAJ, Aw, lda, KMAJ, Z_all, g.ldz, EPI_Z_H,
+                                act);
+        k1.aux = Hbuf;
+        k1.ldaux = ldh;
+        const double b1 = es * ((double)g.T * g.d_in + (double)g.R * g.d_in + 2.0 * g.T * g.R);
+        e = timed(COLA_KC_FWD_Z, gemm_flops(g.T, g.R, g.d_in), b1, s, [&] { return gemm(k1, g.bf16, s); });
+        if (e != hipSuccess) return hip_fail(e, "fwd_z_sigma");
+    } else {
+        GemmArgs k1 = make_args(TAG_INFER_H, g.T, g.R, g.d_in, X, g.ldx, KMAJ, Aw, lda, KMAJ, Hbuf, ldh, EPI_H, act);
+        const double b1 = es * ((double)g.T * g.d_in + (double)g.R * g.d_in + (double)g.T * g.R);
+        e = timed(COLA_KC_INFER_H, gemm_flops(g.T, g.R, g.d_in), b1, s, [&] { return gemm(k1, g.bf16, s); });
+        if (e != hipSuccess) return hip_fail(e, "infer_h");
+    }
+
+    // K2 per projection: Y_p = H_p B_p^T
+    for (int q = 0; q < g.n; ++q) {
+        const void* Bw;
+        int64_t ldb;
+        e = use_weight(p.pb[q], B[q], g.d_out[q], g.r[q], w, &Bw, &ldb, s);
+        if (e != hipSuccess) return hip_fail(e, "pack_rows");
+        GemmArgs k2 = make_args(TAG_FWD_Y, g.T, g.d_out[q], g.r[q], Hbuf + g.off[q] * g.esize, ldh, KMAJ, Bw,
+                                ldb, KMAJ, Y[q], g.ldy[q], EPI_STORE, act);
+        const double b2 = es * ((double)g.T * g.r[q] + (double)g.d_out[q] * g.r[q] + (double)g.T * g.d_out[q]);
+        e = timed(COLA_KC_FWD_Y, gemm_flops(g.T, g.d_out[q], g.r[q]), b2, s, [&] { return gemm(k2, g.bf16, s); });
+        if (e != hipSuccess) return hip_fail(e, "fwd_y");
+    }
+    return COLA_OK;
+}
+
+// The group of one projection that a single-layer descriptor describes.
+GDims single_group(const Dims& x) {
+    GDims g{};
+    g.T = x.T; g.d_in = x.d_in; g.ldx = x.ldx; g.ldz = x.ldz; g.R = x.r; g.n = 1;
+    g.r[0] = x.r; g.d_out[0] = x.d_out; g.ldy[0] = x.ldy; g.off[0] = 0;
+    g.bf16 = x.bf16; g.esize = x.esize;
+    return g;
+}
+
+int infer_checked(const GDims& g, int act, const void* X, const void* A_all, const void* const* B, void* const* Y,
+                  void* ws, size_t ws_bytes, cola_stream_t stream) {
+    if (g.T == 0) return COLA_OK;
+    if (!X || !A_all || !B || !Y) return COLA_ERR_INVALID_ARG;
+    for (int q = 0; q < g.n; ++q)
+        if (!B[q] || !Y[q]) return COLA_ERR_INVALID_ARG;
+    const size_t need = plan_group_fwd(g, true).total;
+    if (need > 0 && (!ws || ws_bytes < need)) return COLA_ERR_WORKSPACE;
+    return group_forward(g, act, X, A_all, B, Y, nullptr, nullptr, true, reinterpret_cast<char*>(ws),
+                         reinterpret_cast<hipStream_t>(stream));
+}
+
+}  // namespace
+
+extern "C" {
 
 int cola_group_fwd(const cola_group_desc* desc, const void* X, const void* A_all, const void* const* B,
                    void* const* Y, void* Z_all, void* H_all, void* ws, size_t ws_bytes, cola_stream_t stream) {
@@ -726,39 +803,30 @@ int cola_group_fwd(const cola_group_desc* desc, const void* X, const void* A_all
             if (!B[q] || !Y[q]) return COLA_ERR_INVALID_ARG;
         const GFwdPlan p = plan_group_fwd(g, recompute);
         if (p.total > 0 && (!ws || ws_bytes < p.total)) return COLA_ERR_WORKSPACE;
-        hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-        char* w = reinterpret_cast<char*>(ws);
-        char* Hbuf = recompute ? w + p.off_h : reinterpret_cast<char*>(H_all);
-        const int64_t ldh = recompute ? p.ldw : g.ldz;
-        const double es = (double)g.esize;
+        return group_forward(g, desc->act, X, A_all, B, Y, Z_all, H_all, recompute, reinterpret_cast<char*>(ws),
+                             reinterpret_cast<hipStream_t>(stream));
+    });
+}
 
-        const void* Aw;
-        int64_t lda;
-        hipError_t e = use_weight(p.pa, A_all, g.R, g.d_in, w, &Aw, &lda, s);
-        if (e != hipSuccess) return hip_fail(e, "pack_rows");
+int cola_group_infer(const cola_group_desc* desc, const void* X, const void* A_all, const void* const* B,
+                     void* const* Y, void* ws, size_t ws_bytes, cola_stream_t stream) {
+    return guarded([&]() -> int {
+        GDims g;
+        const int st = check_group(desc, &g);
+        if (st != COLA_OK) return st;
+        return infer_checked(g, desc->act, X, A_all, B, Y, ws, ws_bytes, stream);
+    });
+}
 
-        // K1 for every projection at once: Z_all = X A_all^T, H_all = sigma(Z_all)
-        GemmArgs k1 = make_args(TAG_FWD_Z, g.T, g.R, g.d_in, X, g.ldx, KMAJ, Aw, lda, KMAJ, Z_all, g.ldz, EPI_Z_H,
-                                desc->act);
-        k1.aux = Hbuf;
-        k1.ldaux = ldh;
-        const double b1 = es * ((double)g.T * g.d_in + (double)g.R * g.d_in + 2.0 * g.T * g.R);
-        e = timed(COLA_KC_FWD_Z, gemm_flops(g.T, g.R, g.d_in), b1, s, [&] { return gemm(k1, g.bf16, s); });
-        if (e != hipSuccess) return hip_fail(e, "fwd_z_sigma");
-
-        // K2 per projection: Y_p = H_p B_p^T
-        for (int q = 0; q < g.n; ++q) {
-            const void* Bw;
-            int64_t ldb;
-            e = use_weight(p.pb[q], B[q], g.d_out[q], g.r[q], w, &Bw, &ldb, s);
-            if (e != hipSuccess) return hip_fail(e, "pack_rows");
-            GemmArgs k2 = make_args(TAG_FWD_Y, g.T, g.d_out[q], g.r[q], Hbuf + g.off[q] * g.esize, ldh, KMAJ, Bw,
-                                    ldb, KMAJ, Y[q], g.ldy[q], EPI_STORE, desc->act);
-            const double b2 = es * ((double)g.T * g.r[q] + (double)g.d_out[q] * g.r[q] + (double)g.T * g.d_out[q]);
-            e = timed(COLA_KC_FWD_Y, gemm_flops(g.T, g.d_out[q], g.r[q]), b2, s, [&] { return gemm(k2, g.bf16, s); });
-            if (e != hipSuccess) return hip_fail(e, "fwd_y");
-        }
-        return COLA_OK;
+int cola_infer(const cola_desc* desc, const void* X, const void* A, const void* B, void* Y, void* ws,
+               size_t ws_bytes, cola_stream_t stream) {
+    return guarded([&]() -> int {
+        Dims x;
+        const int st = check_desc(desc, &x);
+        if (st != COLA_OK) return st;
+        const void* Bs[1] = {B};
+        void* Ys[1] = {Y};
+        return infer_checked(single_group(x), desc->act, X, A, Bs, Ys, ws, ws_bytes, stream);
     });
 }
 

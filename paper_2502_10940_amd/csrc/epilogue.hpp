@@ -144,6 +144,10 @@ __device__ __forceinline__ void epilogue4(const GemmArgs& a, int64_t gm, int64_t
                 out[e] = round_bf16(v[e]);
                 h[e] = act_sigma<true>(a.act, out[e]);
             }
+        } else if constexpr (EPI == EPI_H) {
+            // the H of EPI_Z_H: sigma of Z rounded to bf16
+#pragma unroll
+            for (int e = 0; e < 4; ++e) out[e] = act_sigma<true>(a.act, round_bf16(v[e]));
         } else if constexpr (EPI == EPI_DZ) {
             const float z[4] = {bf16_to_f32(zz[0] & 0xffffu), bf16_to_f32(zz[0] >> 16),
                                 bf16_to_f32(zz[1] & 0xffffu), bf16_to_f32(zz[1] >> 16)};
@@ -180,9 +184,11 @@ __device__ __forceinline__ void epilogue_block_impl(const GemmArgs& a, const f32
                                                     int64_t row0, int64_t col0, int lane, int split) {
     const int64_t lrow = 4 * (lane >> 5) + (lane & 3);     // this lane's row within a group of 8
     const int64_t lcol = 4 * ((lane & 31) >> 2);           // its first column within a tile
-    if constexpr (EPI == EPI_STORE) {
-        // round to bf16 first, then transpose 16-bit pairs (half the exchange work)
+    if constexpr (EPI == EPI_STORE || EPI == EPI_H) {
+        // round to bf16 first, then transpose 16-bit pairs (half the exchange
+        // work); sigma is elementwise, so EPI_H applies it before the transpose
         const QuadSel sel(lane);
+        auto f = [&](float v) { return EPI == EPI_H ? act_sigma<true>(a.act, round_bf16(v)) : v; };
 #pragma unroll
         for (int i = 0; i < TM; ++i)
 #pragma unroll
@@ -190,8 +196,8 @@ __device__ __forceinline__ void epilogue_block_impl(const GemmArgs& a, const f32
 #pragma unroll
                 for (int j = 0; j < TN; ++j) {
                     uint32_t q0, q1;
-                    transpose_bf16(sel, pack_bf16x2(acc[i][j][4 * g], acc[i][j][4 * g + 1]),
-                                   pack_bf16x2(acc[i][j][4 * g + 2], acc[i][j][4 * g + 3]), q0, q1);
+                    transpose_bf16(sel, pack_bf16x2(f(acc[i][j][4 * g]), f(acc[i][j][4 * g + 1])),
+                                   pack_bf16x2(f(acc[i][j][4 * g + 2]), f(acc[i][j][4 * g + 3])), q0, q1);
                     const int64_t gm = row0 + 32 * i + 8 * g + lrow;
                     const int64_t gn = col0 + 32 * j + lcol;
                     uint16_t* c = reinterpret_cast<uint16_t*>(a.c) + gm * a.ldc + gn;

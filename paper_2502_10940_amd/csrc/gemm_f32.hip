@@ -87,6 +87,8 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a) {
             } else if constexpr (EPI == EPI_Z_H) {
                 reinterpret_cast<float*>(a.c)[gm * a.ldc + gn] = v;
                 if (a.aux) reinterpret_cast<float*>(a.aux)[gm * a.ldaux + gn] = act_sigma<false>(a.act, v);
+            } else if constexpr (EPI == EPI_H) {
+                reinterpret_cast<float*>(a.c)[gm * a.ldc + gn] = act_sigma<false>(a.act, v);
             } else if constexpr (EPI == EPI_DZ) {
                 const float z = reinterpret_cast<const float*>(a.zin)[gm * a.ldzin + gn];
                 reinterpret_cast<float*>(a.c)[gm * a.ldc + gn] = v * act_sigma_prime<false>(a.act, z);
@@ -112,6 +114,9 @@ hipError_t launch_gemm_f32(const GemmArgs& a, hipStream_t s) {
     switch (a.epi) {
         case EPI_Z_H:
             if (pl == KMAJ && ql == KMAJ) return launch_t<KMAJ, KMAJ, EPI_Z_H>(a, s);
+            break;
+        case EPI_H:
+            if (pl == KMAJ && ql == KMAJ) return launch_t<KMAJ, KMAJ, EPI_H>(a, s);
             break;
         case EPI_STORE:
             if (pl == KMAJ && ql == KMAJ) return launch_t<KMAJ, KMAJ, EPI_STORE>(a, s);

@@ -235,7 +235,7 @@ __device__ __forceinline__ void wait_vm_at_most(int n) {
 template <int EPI>
 __device__ __forceinline__ int epilogue_ops(bool aux) {
     constexpr int G = 4 * TM * TN;
-    return EPI == EPI_STORE ? G
+    return EPI == EPI_STORE || EPI == EPI_H ? G
          : EPI == EPI_STORE_F32 ? G
          : EPI == EPI_Z_H ? (aux ? 2 * G : G)
          : (aux ? 3 * G : 2 * G);               // EPI_DZ: Z loads, dZ (and H) stores
@@ -448,6 +448,7 @@ hipError_t launch_w(const GemmArgs& a, hipStream_t s) {
 hipError_t launch_gemm_wide(const GemmArgs& a, hipStream_t s) {
     switch (a.tag) {
         case TAG_FWD_Z: return launch_w<KMAJ, KMAJ, EPI_Z_H, TAG_FWD_Z>(a, s);
+        case TAG_INFER_H: return launch_w<KMAJ, KMAJ, EPI_H, TAG_INFER_H>(a, s);
         case TAG_FWD_Y: return launch_w<KMAJ, KMAJ, EPI_STORE, TAG_FWD_Y>(a, s);
         case TAG_BWD_DZ: return launch_w<KMAJ, MNMAJ, EPI_DZ, TAG_BWD_DZ>(a, s);
         case TAG_BWD_DX: return launch_w<KMAJ, MNMAJ, EPI_STORE, TAG_BWD_DX>(a, s);

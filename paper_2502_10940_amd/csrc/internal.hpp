@@ -18,13 +18,14 @@ enum Epilogue : int {
     EPI_STORE_F32 = 1, // c = acc as fp32 (weight gradients, split-K partials)
     EPI_Z_H = 2,       // c = Z = round(acc); aux = H = round(sigma(Z))
     EPI_DZ = 3,        // c = dZ = round(acc * sigma'(Z)), Z read from zin; aux = H if non-NULL
+    EPI_H = 4,         // c = H = round(sigma(round(acc))): H of EPI_Z_H without storing Z (inference)
 };
 
 // Which step of the layer a GEMM is (same numbering as the kernel classes of
 // the public timing API).
 enum Tag : int {
     TAG_FWD_Z = 0, TAG_FWD_Y = 1, TAG_BWD_DZ = 2, TAG_BWD_DX = 3, TAG_BWD_DA = 4,
-    TAG_BWD_DB = 5, TAG_DENSE_FWD = 7, TAG_DENSE_DX = 8, TAG_DENSE_DW = 9
+    TAG_BWD_DB = 5, TAG_DENSE_FWD = 7, TAG_DENSE_DX = 8, TAG_DENSE_DW = 9, TAG_INFER_H = 11
 };
 
 struct GemmArgs {

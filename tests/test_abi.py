@@ -27,7 +27,8 @@ def test_header_declares_expected_calls():
     for n in ("cola_fwd", "cola_bwd", "cola_workspace_bytes", "cola_strerror", "cola_abi_version",
               "dense_fwd", "dense_bwd", "dense_workspace_bytes", "cola_timing_enable",
               "cola_timing_read", "cola_timing_reset", "cola_kernel_name",
-              "cola_group_fwd", "cola_group_bwd", "cola_group_workspace_bytes"):
+              "cola_group_fwd", "cola_group_bwd", "cola_group_workspace_bytes", "cola_infer",
+              "cola_group_infer"):
         assert n in names
 
 
@@ -132,7 +133,8 @@ def test_workspace_sizes():
         dm = cola.desc(1000, 96, 80, 24, dtype=dtype, recompute=True)
         assert cola.workspace_bytes(dm, 0) >= 1000 * 24 * es         # CoLA-M keeps H here
         assert cola.workspace_bytes(dm, 1) >= cola.workspace_bytes(d, 1) + 1000 * 24 * es
-        assert cola.workspace_bytes(d, 2) == 0
+        assert cola.workspace_bytes(d, 2) == cola.workspace_bytes(dm, 0)  # inference keeps H there too
+        assert cola.workspace_bytes(d, 3) == 0
     empty = cola.desc(0, 96, 80, 24)
     assert cola.workspace_bytes(empty, 0) == 0 and cola.workspace_bytes(empty, 1) == 0
 
@@ -249,3 +251,50 @@ def test_group_pointer_and_workspace_checks():
     # an empty batch enqueues nothing
     e = cola.group_desc(0, 32, [8, 16], [32, 24])
     assert group_fwd_status(e, X=None, A=None, B=None, Y=None, Z=None, H=None) == cola.OK
+
+
+def infer_status(d, X=FAKE, A=FAKE, B=FAKE, Y=FAKE, ws=None, ws_bytes=0):
+    p = ctypes.byref(d) if d is not None else None
+    return cola.lib().cola_infer(p, X, A, B, Y, ws, ws_bytes, None)
+
+
+def group_infer_status(d, X=FAKE, A=FAKE, B=FAKE, Y=FAKE, ws=None, ws_bytes=0, n=None):
+    n = d.n if (d is not None and n is None) else (n or 1)
+    arr = lambda v: None if v is None else ctypes.cast((ctypes.c_void_p * max(n, 1))(*([v] * max(n, 1))),
+                                                      ctypes.c_void_p)
+    p = ctypes.byref(d) if d is not None else None
+    return cola.lib().cola_group_infer(p, X, A, arr(B), arr(Y), ws, ws_bytes, None)
+
+
+def test_infer_checks():
+    d = cola.desc(64, 32, 48, 8)
+    # H lives in the workspace whatever recompute says: the CoLA-M forward's size
+    need = cola.workspace_bytes(d, 2)
+    assert need == cola.workspace_bytes(cola.desc(64, 32, 48, 8, recompute=True), 0) > 0
+    assert cola.workspace_bytes(d, 3) == 0
+    assert infer_status(None) == cola.ERR_INVALID_ARG
+    for kw in (dict(dtype=7), dict(act=3)):
+        assert infer_status(cola.desc(64, 32, 48, 8, **kw)) == cola.ERR_INVALID_ARG
+    assert infer_status(cola.desc(64, 0, 48, 8)) == cola.ERR_BAD_SHAPE
+    assert infer_status(cola.desc(64, 32, 48, 8, ldx=31)) == cola.ERR_BAD_SHAPE
+    for k in ("X", "A", "B", "Y"):
+        assert infer_status(d, **{k: None}) == cola.ERR_INVALID_ARG
+    assert infer_status(d) == cola.ERR_WORKSPACE
+    assert infer_status(d, ws=FAKE, ws_bytes=need - 1) == cola.ERR_WORKSPACE
+    assert infer_status(cola.desc(0, 32, 48, 8), X=None, A=None, B=None, Y=None) == cola.OK
+
+
+def test_group_infer_checks():
+    d = cola.group_desc(64, 32, [8, 16], [32, 24])
+    need = cola.group_workspace_bytes(d, 2)
+    assert need == cola.group_workspace_bytes(cola.group_desc(64, 32, [8, 16], [32, 24], recompute=True), 0)
+    assert cola.group_workspace_bytes(d, 3) == 0
+    assert group_infer_status(None) == cola.ERR_INVALID_ARG
+    assert group_infer_status(cola.group_desc(64, 32, [8, 0], [32, 32])) == cola.ERR_BAD_SHAPE
+    assert group_infer_status(cola.group_desc(64, 32, [8], [32], act=3)) == cola.ERR_INVALID_ARG
+    for k in ("X", "A", "B", "Y"):
+        assert group_infer_status(d, **{k: None}) == cola.ERR_INVALID_ARG
+    assert group_infer_status(d) == cola.ERR_WORKSPACE
+    assert group_infer_status(d, ws=FAKE, ws_bytes=need - 1) == cola.ERR_WORKSPACE
+    e = cola.group_desc(0, 32, [8, 16], [32, 24])
+    assert group_infer_status(e, X=None, A=None, B=None, Y=None) == cola.OK

@@ -162,3 +162,47 @@ def test_group_empty_batch_zeroes_weight_gradients():
     assert torch.count_nonzero(dA).item() == 0
     for b in dB:
         assert torch.count_nonzero(b).item() == 0
+
+
+@pytest.mark.parametrize("case", range(len(CASES)), ids=[c[0] for c in CASES])
+def test_group_infer(case):
+    """Inference forward of the group: each Y_p against the oracle, and bitwise
+    the Y_p of the training forward (the same kernels and sums; H is never
+    written out, Z not at all)."""
+    name, T, d_in, ranks, widths, dtype, act = CASES[case]
+    X, As, Bs, dYs = group_inputs(case, T, d_in, ranks, widths, dtype)
+    ref = oracle_group(X, As, Bs, dYs, act)
+    run = GroupRun(X, As, Bs, dYs, T, d_in, ranks, widths, dtype, act, False)
+    cola.group_fwd(run.desc, run.X, run.A_all, run.B, run.Y, run.Z, run.H, run.ws)
+    nanb = NAN_BITS[dtype]
+    Yi = [empty(T, w, dtype, nanb) for w in widths]
+    ws = torch.empty(max(cola.group_workspace_bytes(run.desc, 2), 1), dtype=torch.uint8, device=DEV)
+    cola.group_infer(run.desc, run.X, run.A_all, run.B, Yi, ws)
+    torch.cuda.synchronize()
+    check({"Y": [to_f64(y) for y in Yi]}, {"Y": ref["Y"]}, dtype, f"{name}/infer")
+    for p in range(len(ranks)):
+        assert torch.equal(Yi[p], run.Y[p]), f"{name}: inference Y[{p}] differs from the training forward"
+
+
+@pytest.mark.parametrize("case", [0, 2, 4], ids=[CASES[c][0] for c in (0, 2, 4)])
+def test_single_infer(case):
+    """cola_infer on each projection alone: oracle parity and bitwise the Y of
+    cola_fwd."""
+    name, T, d_in, ranks, widths, dtype, act = CASES[case]
+    X, As, Bs, dYs = group_inputs(case, T, d_in, ranks, widths, dtype)
+    ref = oracle_group(X, As, Bs, dYs, act)
+    Xd = to_device(X.store, dtype)
+    for p, (A, B) in enumerate(zip(As, Bs)):
+        r, w = ranks[p], widths[p]
+        d = cola.desc(T, d_in, w, r, dtype, act)
+        Ad, Bd = to_device(A.store, dtype), to_device(B.store, dtype)
+        Y = torch.empty((T, w), dtype=TORCH_DT[dtype], device=DEV)
+        Z = torch.empty((T, r), dtype=TORCH_DT[dtype], device=DEV)
+        H = torch.empty((T, r), dtype=TORCH_DT[dtype], device=DEV)
+        cola.fwd(d, Xd, Ad, Bd, Y, Z, H, torch.empty(max(cola.workspace_bytes(d, 0), 1), dtype=torch.uint8,
+                                                     device=DEV))
+        Yi = empty(T, w, dtype, NAN_BITS[dtype])
+        cola.infer(d, Xd, Ad, Bd, Yi, torch.empty(cola.workspace_bytes(d, 2), dtype=torch.uint8, device=DEV))
+        torch.cuda.synchronize()
+        check({"Y": to_f64(Yi)}, {"Y": ref["Y"][p]}, dtype, f"{name}/infer[{p}]")
+        assert torch.equal(Yi, Y)
