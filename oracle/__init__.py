@@ -42,6 +42,9 @@ def _load(path=None):
     lib.oracle_cola_fwd.argtypes = [i64, i64, i64, i64, c_int, d, d, d, d, d, d]
     lib.oracle_cola_bwd.argtypes = [i64, i64, i64, i64, c_int, d, d, d, d, d,
                                     d, d, d, d, d]
+    lib.oracle_cola_fwd_outer.argtypes = [i64, i64, i64, i64, c_int, c_int, d, d, d, d, d, d, d]
+    lib.oracle_cola_bwd_outer.argtypes = [i64, i64, i64, i64, c_int, c_int, d, d, d, d, d, d,
+                                          d, d, d, d, d, d]
     lib.oracle_dense_fwd.argtypes = [i64, i64, i64, d, d, d]
     lib.oracle_dense_bwd.argtypes = [i64, i64, i64, d, d, d, d, d]
     lib.oracle_cola_rows.argtypes = [i64, i64, i64, i64, c_int, d, d, d, d,
@@ -131,6 +134,36 @@ def cola_bwd(X, Z, A, B, dY, act="silu"):
     _load().oracle_cola_bwd(T, d_in, d_out, r, _act(act), _p(X), _p(Z), _p(A), _p(B),
                             _p(dY), _p(dZ), _p(dX), _p(dA), _p(dB), _p(scratch))
     return dZ, dX, dA, dB
+
+
+def cola_fwd_outer(X, A, B, act="silu", outer="silu"):
+    """The "both sigma" variant: Y = sigma_out(H B^T).  Returns (Z, H, P, Y),
+    P = H B^T the output before sigma_out."""
+    X = _f64(X); A = _f64(A); B = _f64(B)
+    T, d_in = X.shape
+    r = A.shape[0]
+    d_out = B.shape[0]
+    _f64(A, (r, d_in)); _f64(B, (d_out, r))
+    Z = np.empty((T, r)); H = np.empty((T, r)); P = np.empty((T, d_out)); Y = np.empty((T, d_out))
+    _load().oracle_cola_fwd_outer(T, d_in, d_out, r, _act(act), _act(outer), _p(X), _p(A), _p(B),
+                                  _p(Z), _p(H), _p(P), _p(Y))
+    return Z, H, P, Y
+
+
+def cola_bwd_outer(X, Z, P, A, B, dY, act="silu", outer="silu"):
+    """Gradients of the "both sigma" variant from the saved Z and P.
+    Returns (dP, dZ, dX, dA, dB), dP = dY * sigma_out'(P)."""
+    X = _f64(X); Z = _f64(Z); P = _f64(P); A = _f64(A); B = _f64(B); dY = _f64(dY)
+    T, d_in = X.shape
+    r = A.shape[0]
+    d_out = B.shape[0]
+    _f64(Z, (T, r)); _f64(P, (T, d_out)); _f64(dY, (T, d_out))
+    dP = np.empty((T, d_out)); dZ = np.empty((T, r)); dX = np.empty((T, d_in))
+    dA = np.empty((r, d_in)); dB = np.empty((d_out, r))
+    scratch = np.empty(2 * T * r + T * d_out)
+    _load().oracle_cola_bwd_outer(T, d_in, d_out, r, _act(act), _act(outer), _p(X), _p(Z), _p(P), _p(A),
+                                  _p(B), _p(dY), _p(dP), _p(dZ), _p(dX), _p(dA), _p(dB), _p(scratch))
+    return dP, dZ, dX, dA, dB
 
 
 def dense_fwd(X, W):

@@ -36,6 +36,10 @@
  * no fast-math; OpenMP splits only the outermost output-row loop, so each
  * output element is one sequential sum in fp64.
  *
+ * The "both sigma" variant of the ablation (an outer nonlinearity sigma_out
+ * on the layer output, App. ablation) is the composition of the layer with
+ * sigma_out; its backward is the chain rule through that composition.
+ *
  * Pins (tests/test_oracle_*.py): identity-sigma closed form against the
  * conventional low-rank product B A X (Sec. 3.3), central finite differences,
  * torch fp64 autograd, the Prop. 1 limit construction, the Lemma
@@ -185,6 +189,34 @@ void oracle_cola_bwd(int64_t T, int64_t d_in, int64_t d_out, int64_t r, int act,
     gemm_tn(r, d_in, T, dZ, X, dA);               /* dA[j][k] = sum_t dZ[t][j] X[t][k] */
     gemm_tn(d_out, r, T, dY, H, dB);              /* dB[o][j] = sum_t dY[t][o] H[t][j] */
     if (dZ_out) memcpy(dZ_out, dZ, (size_t)(T * r) * sizeof(double));
+}
+
+/* ------------------------------------------------------------------------ */
+/* "both sigma" variant (App. ablation, Table "ablation"): the nonlinearity */
+/* that followed the original linear layer is kept on top of the layer,      */
+/* Y = sigma_out(B sigma(A x)).  The layer output before sigma_out, P, is    */
+/* what the backward needs.                                                  */
+/* ------------------------------------------------------------------------ */
+
+/* Forward: Z, H as in oracle_cola_fwd, P = H B^T, Y = sigma_out(P). */
+void oracle_cola_fwd_outer(int64_t T, int64_t d_in, int64_t d_out, int64_t r, int act, int outer,
+                           const double* X, const double* A, const double* B,
+                           double* Z, double* H, double* P, double* Y) {
+    oracle_cola_fwd(T, d_in, d_out, r, act, X, A, B, Z, H, P);
+    for (int64_t i = 0; i < T * d_out; ++i) Y[i] = oracle_sigma(outer, P[i]);
+}
+
+/* Backward: the chain rule through sigma_out gives dP = dY * sigma_out'(P);
+ * the layer's own backward then runs on dP.  dP_out may be NULL. */
+void oracle_cola_bwd_outer(int64_t T, int64_t d_in, int64_t d_out, int64_t r, int act, int outer,
+                           const double* X, const double* Z, const double* P,
+                           const double* A, const double* B, const double* dY,
+                           double* dP_out, double* dZ_out, double* dX, double* dA, double* dB,
+                           double* scratch /* 2*T*r + T*d_out doubles */) {
+    double* dP = scratch + 2 * T * r;
+    for (int64_t i = 0; i < T * d_out; ++i) dP[i] = dY[i] * oracle_sigma_prime(outer, P[i]);
+    oracle_cola_bwd(T, d_in, d_out, r, act, X, Z, A, B, dP, dZ_out, dX, dA, dB, scratch);
+    if (dP_out) memcpy(dP_out, dP, (size_t)(T * d_out) * sizeof(double));
 }
 
 /* ------------------------------------------------------------------------ */

@@ -29,6 +29,12 @@ MUTANTS = {
     "gelu_cdf_wrong_sign": ("return 0.5 * erfc(-z * 0.70710678118654752440);",
                             "return 0.5 * erfc(z * 0.70710678118654752440);"),
     "gelu_pdf_wrong_scale": ("exp(-0.5 * z * z)", "exp(-z * z)"),
+    "outer_backward_drops_sigma_prime": ("dP[i] = dY[i] * oracle_sigma_prime(outer, P[i]);", "dP[i] = dY[i];"),
+    "outer_sigma_prime_of_Y": ("dP[i] = dY[i] * oracle_sigma_prime(outer, P[i]);",
+                               "dP[i] = dY[i] * oracle_sigma_prime(outer, oracle_sigma(outer, P[i]));"),
+    "outer_forward_skips_sigma": ("Y[i] = oracle_sigma(outer, P[i]);", "Y[i] = P[i];"),
+    "outer_uses_inner_act": ("dP[i] = dY[i] * oracle_sigma_prime(outer, P[i]);",
+                             "dP[i] = dY[i] * oracle_sigma_prime(act, P[i]);"),
     "mac_counter_fwd_only_one_gemm": ("static void gemm_nt(int64_t M, int64_t N, int64_t K,\n                    const double* P, const double* Q, double* C) {\n    g_mac_count += M * N * K;",
                                       "static void gemm_nt(int64_t M, int64_t N, int64_t K,\n                    const double* P, const double* Q, double* C) {\n    g_mac_count += M * N;"),
 }
@@ -51,6 +57,9 @@ def battery():
         ("lemma", pins.test_lemma_esigma_zero_construction, ()),
         ("sampled", pins.test_sampled_rows_and_columns_match_full, ()),
         ("flops", pins.test_layer_flop_count, ((3, 8, 5, 2),)),
+        ("outer_identity", pins.test_outer_identity_is_the_plain_layer, ("silu",)),
+        ("outer_fd", pins.test_outer_gradients_by_central_differences, ((3, 5, 4, 2), "identity", "silu")),
+        ("outer_torch", pins.test_outer_against_torch_fp64_autograd, ("silu", "gelu")),
     ]
     failed = []
     for name, fn, args in checks:

@@ -201,6 +201,64 @@ def test_against_torch_fp64_autograd(shape, act):
 
 
 # --------------------------------------------------------------------------
+# "both sigma" variant (App. ablation): Y = sigma_out(B sigma(A x))
+# --------------------------------------------------------------------------
+
+@pytest.mark.parametrize("act", ["silu", "gelu", "identity"])
+def test_outer_identity_is_the_plain_layer(act):
+    # sigma_out = identity must give the plain layer exactly: Y = P, dP = dY
+    X, A, B, dY = rand_layer(41, 23, 19, 13, 6)
+    Z0, H0, Y0 = oracle.cola_fwd(X, A, B, act=act)
+    dZ0, dX0, dA0, dB0 = oracle.cola_bwd(X, Z0, A, B, dY, act=act)
+    Z, H, P, Y = oracle.cola_fwd_outer(X, A, B, act=act, outer="identity")
+    dP, dZ, dX, dA, dB = oracle.cola_bwd_outer(X, Z, P, A, B, dY, act=act, outer="identity")
+    for a, b in ((Z, Z0), (H, H0), (P, Y0), (Y, Y0), (dP, dY), (dZ, dZ0), (dX, dX0), (dA, dA0),
+                 (dB, dB0)):
+        assert np.array_equal(a, b)
+
+
+@pytest.mark.parametrize("act,outer", [("silu", "silu"), ("gelu", "gelu"), ("identity", "silu")])
+@pytest.mark.parametrize("shape", [(1, 1, 1, 1), (3, 5, 4, 2), (6, 4, 3, 2)])
+def test_outer_gradients_by_central_differences(shape, act, outer):
+    T, d_in, d_out, r = shape
+    X, A, B, dY = rand_layer(51 + T, T, d_in, d_out, r, scale_a=0.9, scale_b=0.8)
+
+    def loss(X_, A_, B_):
+        return float(np.sum(dY * oracle.cola_fwd_outer(X_, A_, B_, act=act, outer=outer)[3]))
+
+    Z, _, P, _ = oracle.cola_fwd_outer(X, A, B, act=act, outer=outer)
+    _, _, dX, dA, dB = oracle.cola_bwd_outer(X, Z, P, A, B, dY, act=act, outer=outer)
+    h = 1e-5
+    for name, arr, grad in (("X", X, dX), ("A", A, dA), ("B", B, dB)):
+        fd = np.zeros_like(arr)
+        for idx in np.ndindex(arr.shape):
+            args_p = {"X": X, "A": A, "B": B}; args_p[name] = arr.copy(); args_p[name][idx] += h
+            args_m = {"X": X, "A": A, "B": B}; args_m[name] = arr.copy(); args_m[name][idx] -= h
+            fd[idx] = (loss(args_p["X"], args_p["A"], args_p["B"]) -
+                       loss(args_m["X"], args_m["A"], args_m["B"])) / (2 * h)
+        assert relerr(grad, fd) < 1e-7, name
+
+
+@pytest.mark.parametrize("act,outer", [("silu", "silu"), ("gelu", "gelu"), ("silu", "gelu")])
+def test_outer_against_torch_fp64_autograd(act, outer):
+    T, d_in, d_out, r = 29, 24, 40, 8
+    X, A, B, dY = rand_layer(61, T, d_in, d_out, r)
+    f = {"silu": torch.nn.functional.silu,
+         "gelu": lambda z: torch.nn.functional.gelu(z, approximate="none")}
+    tX = torch.tensor(X, requires_grad=True)
+    tA = torch.tensor(A, requires_grad=True)
+    tB = torch.tensor(B, requires_grad=True)
+    tP = f[act](tX @ tA.T) @ tB.T
+    tP.retain_grad()
+    tY = f[outer](tP)
+    tY.backward(torch.tensor(dY))
+    Z, H, P, Y = oracle.cola_fwd_outer(X, A, B, act=act, outer=outer)
+    dP, dZ, dX, dA, dB = oracle.cola_bwd_outer(X, Z, P, A, B, dY, act=act, outer=outer)
+    for ours, ref in ((P, tP), (Y, tY), (dP, tP.grad), (dX, tX.grad), (dA, tA.grad), (dB, tB.grad)):
+        assert relerr(ours, ref.detach().numpy()) < 1e-13
+
+
+# --------------------------------------------------------------------------
 # constructions from the paper's proofs
 # --------------------------------------------------------------------------
 
