@@ -98,11 +98,13 @@ int cola_abi_version(void);
 /* Text for a status code; for COLA_ERR_HIP the text of the last failure. */
 const char* cola_strerror(int status);
 
-/* Workspace bytes for phase 0 (cola_fwd), 1 (cola_bwd) or 2 (cola_infer);
- * 0 on an invalid descriptor or phase.  Forward needs T*r elements when
+/* Workspace bytes for phase 0 (cola_fwd, cola_fwd_outer), 1 (cola_bwd),
+ * 2 (cola_infer) or 3 (cola_bwd_outer); 0 on an invalid descriptor or phase.  Forward needs T*r elements when
  * recompute = 1 (H lives only there), else nothing.  Backward needs dZ (T*r
  * elements), H again when recompute = 1, and the fp32 partial sums of dA and
- * dB.  Inference needs T*r elements for H whatever recompute says.  Weights
+ * dB.  Inference needs T*r elements for H whatever recompute says.  The
+ * both-sigma backward needs the backward's workspace plus T*d_out elements
+ * for dP.  Weights
  * whose row length is not a multiple of 8 (bf16) add a padded copy. */
 size_t cola_workspace_bytes(const cola_desc* desc, int phase);
 
@@ -126,6 +128,28 @@ int cola_bwd(const cola_desc* desc,
              const void* A, const void* B,
              void* dX, float* dA, float* dB,
              void* ws, size_t ws_bytes, cola_stream_t stream);
+
+/* The "both sigma" variant of the ablation (App. ablation, Table
+ * "ablation"): the nonlinearity that followed the original linear layer is
+ * kept on top of the layer, Y = sigma_out(B sigma(A x)), sigma_out given by
+ * outer_act (a cola_act).
+ * Forward: as cola_fwd, and K2 stores both P = H B^T (the output before
+ * sigma_out, which the backward needs) and Y = sigma_out(P); P and Y are
+ * [T][ldy] in the storage dtype, Y computed from P rounded to that dtype.
+ * Backward: dP = dY (.) sigma_out'(P), rounded to the storage dtype, then the
+ * backward of cola_bwd with dP in place of dY.  Workspace: phase 0 forward,
+ * phase 3 backward.  Ownership, errors and the H/recompute rule as in
+ * cola_fwd / cola_bwd; an invalid outer_act is COLA_ERR_INVALID_ARG. */
+int cola_fwd_outer(const cola_desc* desc, int outer_act,
+                   const void* X, const void* A, const void* B,
+                   void* Y, void* P, void* Z, void* H,
+                   void* ws, size_t ws_bytes, cola_stream_t stream);
+
+int cola_bwd_outer(const cola_desc* desc, int outer_act,
+                   const void* dY, const void* P, const void* X, const void* Z, const void* H,
+                   const void* A, const void* B,
+                   void* dX, float* dA, float* dB,
+                   void* ws, size_t ws_bytes, cola_stream_t stream);
 
 /* Inference forward (Eq. main-fwd with nothing kept for a backward pass; the
  * paper's inference comparison, App. "Inference Efficiency"):
@@ -234,7 +258,8 @@ typedef enum {
     COLA_KC_DENSE_DW = 9,  /* dW = dY^T X                              */
     COLA_KC_FILL = 10,     /* zero fill (empty batches)                */
     COLA_KC_INFER_H = 11,  /* H = sigma(X A^T), Z not kept (inference) */
-    COLA_KC_COUNT = 12
+    COLA_KC_OUTER_GRAD = 12, /* dP = dY (.) sigma_out'(P), both-sigma variant */
+    COLA_KC_COUNT = 13
 } cola_kernel_class;
 
 /* Per-class totals since the last reset: launches, elapsed milliseconds,

@@ -21,7 +21,8 @@ ACTS = {"identity": ACT_IDENTITY, "silu": ACT_SILU, "gelu": ACT_GELU}
 OK, ERR_INVALID_ARG, ERR_BAD_SHAPE, ERR_WORKSPACE, ERR_HIP, ERR_UNSUPPORTED = range(6)
 
 KERNEL_CLASSES = ("fwd_z_sigma", "fwd_y", "bwd_dz", "bwd_dx", "bwd_da", "bwd_db",
-                  "reduce_splits", "dense_fwd", "dense_dx", "dense_dw", "fill_zero", "infer_h")
+                  "reduce_splits", "dense_fwd", "dense_dx", "dense_dw", "fill_zero", "infer_h",
+                  "outer_grad")
 
 
 class ColaError(RuntimeError):
@@ -72,6 +73,10 @@ EXPORTS = {
     "cola_group_bwd": ([ctypes.POINTER(GroupDesc), _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _SZ, _P],
                        ctypes.c_int),
     "cola_infer": ([ctypes.POINTER(ColaDesc), _P, _P, _P, _P, _P, _SZ, _P], ctypes.c_int),
+    "cola_fwd_outer": ([ctypes.POINTER(ColaDesc), ctypes.c_int, _P, _P, _P, _P, _P, _P, _P, _P, _SZ, _P],
+                       ctypes.c_int),
+    "cola_bwd_outer": ([ctypes.POINTER(ColaDesc), ctypes.c_int, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _SZ,
+                        _P], ctypes.c_int),
     "cola_group_infer": ([ctypes.POINTER(GroupDesc), _P, _P, _P, _P, _P, _SZ, _P], ctypes.c_int),
     "cola_timing_enable": ([ctypes.c_int], ctypes.c_int),
     "cola_timing_reset": ([], ctypes.c_int),
@@ -197,6 +202,24 @@ def fwd(d: ColaDesc, X, A, B, Y, Z, H, ws=None, ws_bytes=None, stream=None):
         ws_bytes = ws.numel() * ws.element_size() if ws is not None else 0
     _check(lib().cola_fwd(ctypes.byref(d), _ptr(X), _ptr(A), _ptr(B), _ptr(Y), _ptr(Z), _ptr(H),
                           _ptr(ws), ws_bytes, _stream(stream)))
+
+
+def fwd_outer(d: ColaDesc, outer, X, A, B, Y, P, Z, H, ws=None, ws_bytes=None, stream=None):
+    """Both-sigma variant: P = H B^T, Y = sigma_out(P) (outer: a sigma name or code)."""
+    if ws_bytes is None:
+        ws_bytes = ws.numel() * ws.element_size() if ws is not None else 0
+    _check(lib().cola_fwd_outer(ctypes.byref(d), ACTS[outer] if isinstance(outer, str) else int(outer), _ptr(X),
+                                _ptr(A), _ptr(B), _ptr(Y), _ptr(P), _ptr(Z), _ptr(H), _ptr(ws), ws_bytes,
+                                _stream(stream)))
+
+
+def bwd_outer(d: ColaDesc, outer, dY, P, X, Z, H, A, B, dX, dA, dB, ws=None, ws_bytes=None, stream=None):
+    """Both-sigma backward: dP = dY * sigma_out'(P), then the layer backward on dP."""
+    if ws_bytes is None:
+        ws_bytes = ws.numel() * ws.element_size() if ws is not None else 0
+    _check(lib().cola_bwd_outer(ctypes.byref(d), ACTS[outer] if isinstance(outer, str) else int(outer), _ptr(dY),
+                                _ptr(P), _ptr(X), _ptr(Z), _ptr(H), _ptr(A), _ptr(B), _ptr(dX), _ptr(dA), _ptr(dB),
+                                _ptr(ws), ws_bytes, _stream(stream)))
 
 
 def infer(d: ColaDesc, X, A, B, Y, ws=None, ws_bytes=None, stream=None):

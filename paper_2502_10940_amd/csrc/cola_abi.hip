@@ -119,11 +119,12 @@ struct Dims {
     size_t esize;
 };
 
+bool valid_act(int act) { return act == COLA_ACT_IDENTITY || act == COLA_ACT_SILU || act == COLA_ACT_GELU; }
+
 int check_desc(const cola_desc* d, Dims* out) {
     if (!d) return COLA_ERR_INVALID_ARG;
     if (d->dtype != COLA_F32 && d->dtype != COLA_BF16) return COLA_ERR_INVALID_ARG;
-    if (d->act != COLA_ACT_IDENTITY && d->act != COLA_ACT_SILU && d->act != COLA_ACT_GELU)
-        return COLA_ERR_INVALID_ARG;
+    if (!valid_act(d->act)) return COLA_ERR_INVALID_ARG;
     if (d->recompute != 0 && d->recompute != 1) return COLA_ERR_INVALID_ARG;
     if (d->T < 0 || d->d_in < 1 || d->d_out < 1 || d->r < 1) return COLA_ERR_BAD_SHAPE;
     if (d->T > kMaxDim || d->d_in > kMaxDim || d->d_out > kMaxDim || d->r > kMaxDim)
@@ -327,6 +328,116 @@ int guarded(F&& f) {
     }
 }
 
+// Forward of one validated layer with its pointers and workspace checked.
+// outer >= 0: the both-sigma variant (K2 stores P and Y = sigma_out(P)).
+int layer_forward(const Dims& x, int act, bool recompute, const void* X, const void* A, const void* B, void* Y,
+                  void* Z, void* H, int outer, void* P, char* w, hipStream_t s) {
+    const FwdPlan p = plan_fwd(x, recompute);
+    void* Hbuf = recompute ? (void*)(w + p.off_h) : H;
+    const int64_t ldh = recompute ? p.ldw : x.ldz;
+    const double es = (double)x.esize;
+    const void* Aw;
+    const void* Bw;
+    int64_t lda, ldb;
+    hipError_t e = use_weight(p.pa, A, x.r, x.d_in, w, &Aw, &lda, s);
+    if (e == hipSuccess) e = use_weight(p.pb, B, x.d_out, x.r, w, &Bw, &ldb, s);
+    if (e != hipSuccess) return hip_fail(e, "pack_rows");
+
+    // K1: Z = X A^T, H = sigma(Z)
+    GemmArgs k1 = make_args(TAG_FWD_Z, x.T, x.r, x.d_in, X, x.ldx, KMAJ, Aw, lda, KMAJ, Z, x.ldz, EPI_Z_H,
+                            act);
+    k1.aux = Hbuf;
+    k1.ldaux = ldh;
+    const double b1 = es * ((double)x.T * x.d_in + (double)x.r * x.d_in + 2.0 * x.T * x.r);
+    e = timed(COLA_KC_FWD_Z, gemm_flops(x.T, x.r, x.d_in), b1, s, [&] { return gemm(k1, x.bf16, s); });
+    if (e != hipSuccess) return hip_fail(e, "fwd_z_sigma");
+
+    // K2: Y = H B^T; with an outer sigma (outer >= 0) K2 stores P = H B^T
+    // and Y = sigma_out(P)
+    GemmArgs k2 = make_args(TAG_FWD_Y, x.T, x.d_out, x.r, Hbuf, ldh, KMAJ, Bw, ldb, KMAJ, Y, x.ldy, EPI_STORE,
+                            act);
+    if (outer >= 0) {
+        k2 = make_args(TAG_FWD_YP, x.T, x.d_out, x.r, Hbuf, ldh, KMAJ, Bw, ldb, KMAJ, P, x.ldy, EPI_Z_H, outer);
+        k2.aux = Y;
+        k2.ldaux = x.ldy;
+    }
+    const double b2 = es * ((double)x.T * x.r + (double)x.d_out * x.r + (double)x.T * x.d_out *
+                            (outer >= 0 ? 2.0 : 1.0));
+    e = timed(COLA_KC_FWD_Y, gemm_flops(x.T, x.d_out, x.r), b2, s, [&] { return gemm(k2, x.bf16, s); });
+    if (e != hipSuccess) return hip_fail(e, "fwd_y");
+    return COLA_OK;
+}
+
+// Backward of one validated layer with a non-empty batch, its pointers and
+// workspace checked; dY has row pitch ldy.
+int layer_backward(const Dims& x, int act, bool recompute, const void* dY, int64_t ldy, const void* X,
+                   const void* Z, const void* H, const void* A, const void* B, void* dX, float* dA, float* dB,
+                   char* w, hipStream_t s) {
+    const BwdPlan p = plan_bwd(x, recompute);
+    void* dZ = w + p.off_dz;
+    const void* Hbuf = recompute ? (const void*)(w + p.off_h) : H;
+    const int64_t ldh = recompute ? p.ldw : x.ldz;
+    const double es = (double)x.esize;
+    const void* Aw;
+    const void* Bw;
+    int64_t lda, ldb;
+    hipError_t e = use_weight(p.wa, A, x.r, x.d_in, w, &Aw, &lda, s);
+    if (e == hipSuccess) e = use_weight(p.wb, B, x.d_out, x.r, w, &Bw, &ldb, s);
+    if (e != hipSuccess) return hip_fail(e, "pack_rows");
+
+    // K3: dZ = (dY B) (.) sigma'(Z); CoLA-M regenerates H = sigma(Z) here
+    GemmArgs k3 = make_args(TAG_BWD_DZ, x.T, x.r, x.d_out, dY, ldy, KMAJ, Bw, ldb, MNMAJ, dZ, p.ldw, EPI_DZ,
+                            act);
+    k3.zin = Z;
+    k3.ldzin = x.ldz;
+    k3.aux = recompute ? (void*)(w + p.off_h) : nullptr;
+    k3.ldaux = p.ldw;
+    const double b3 = es * ((double)x.T * x.d_out + (double)x.d_out * x.r +
+                            (double)x.T * x.r * (recompute ? 3.0 : 2.0));
+    e = timed(COLA_KC_BWD_DZ, gemm_flops(x.T, x.r, x.d_out), b3, s, [&] { return gemm(k3, x.bf16, s); });
+    if (e != hipSuccess) return hip_fail(e, "bwd_dz");
+
+    // K4: dX = dZ A
+    GemmArgs k4 = make_args(TAG_BWD_DX, x.T, x.d_in, x.r, dZ, p.ldw, KMAJ, Aw, lda, MNMAJ, dX, x.ldx, EPI_STORE,
+                            act);
+    const double b4 = es * ((double)x.T * x.r + (double)x.r * x.d_in + (double)x.T * x.d_in);
+    e = timed(COLA_KC_BWD_DX, gemm_flops(x.T, x.d_in, x.r), b4, s, [&] { return gemm(k4, x.bf16, s); });
+    if (e != hipSuccess) return hip_fail(e, "bwd_dx");
+
+    // K5: dA = dZ^T X ; K6: dB = dY^T H  (+ K7 fixed-order reductions)
+    int st = wgrad(x.bf16, x.r, x.d_in, x.T, dZ, p.ldw, X, x.ldx, dA, p.sa,
+               reinterpret_cast<float*>(w + p.off_pa), COLA_KC_BWD_DA,
+               es * ((double)x.T * x.r + (double)x.T * x.d_in), s);
+    if (st != COLA_OK) return st;
+    st = wgrad(x.bf16, x.d_out, x.r, x.T, dY, ldy, Hbuf, ldh, dB, p.sb,
+               reinterpret_cast<float*>(w + p.off_pb), COLA_KC_BWD_DB,
+               es * ((double)x.T * x.d_out + (double)x.T * x.r), s);
+    return st;
+}
+
+// dA = dB = 0 for an empty batch (the token sums are empty).
+int zero_weight_grads(const Dims& x, float* dA, float* dB, hipStream_t s) {
+    hipError_t e = timed(COLA_KC_FILL, 0.0, 4.0 * x.r * x.d_in, s,
+                         [&] { return launch_fill_zero(dA, x.r * x.d_in, s); });
+    if (e == hipSuccess)
+        e = timed(COLA_KC_FILL, 0.0, 4.0 * x.d_out * x.r, s, [&] { return launch_fill_zero(dB, x.d_out * x.r, s); });
+    return e == hipSuccess ? COLA_OK : hip_fail(e, "fill_zero");
+}
+
+// Workspace of the both-sigma backward: the layer's, then dP = dY sigma_out'(P).
+struct OuterPlan {
+    int64_t ldg;
+    size_t off_g, total;
+};
+
+OuterPlan plan_outer_bwd(const Dims& x, bool recompute) {
+    OuterPlan o;
+    o.ldg = x.bf16 ? (x.d_out + 7) / 8 * 8 : (x.d_out + 3) / 4 * 4;
+    o.off_g = plan_bwd(x, recompute).total;
+    o.total = x.T == 0 ? 0 : o.off_g + align256((size_t)x.T * (size_t)o.ldg * x.esize);
+    return o;
+}
+
 }  // namespace
 
 extern "C" {
@@ -348,7 +459,7 @@ const char* cola_strerror(int status) {
 const char* cola_kernel_name(int kc) {
     static const char* names[COLA_KC_COUNT] = {
         "fwd_z_sigma", "fwd_y", "bwd_dz", "bwd_dx", "bwd_da", "bwd_db",
-        "reduce_splits", "dense_fwd", "dense_dx", "dense_dw", "fill_zero", "infer_h"};
+        "reduce_splits", "dense_fwd", "dense_dx", "dense_dw", "fill_zero", "infer_h", "outer_grad"};
     if (kc < 0 || kc >= COLA_KC_COUNT) return "invalid";
     return names[kc];
 }
@@ -359,6 +470,7 @@ size_t cola_workspace_bytes(const cola_desc* desc, int phase) {
     if (phase == 0) return fwd_ws(x, desc->recompute == 1);
     if (phase == 1) return plan_bwd(x, desc->recompute == 1).total;
     if (phase == 2) return fwd_ws(x, true);     // inference: H in the workspace, as CoLA-M's forward
+    if (phase == 3) return plan_outer_bwd(x, desc->recompute == 1).total;
     return 0;
 }
 
@@ -375,35 +487,26 @@ int cola_fwd(const cola_desc* desc, const void* X, const void* A, const void* B,
         if (!X || !A || !B || !Y || !Z) return COLA_ERR_INVALID_ARG;
         const FwdPlan p = plan_fwd(x, recompute);
         if (p.total > 0 && (!ws || ws_bytes < p.total)) return COLA_ERR_WORKSPACE;
-        hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-        char* w = reinterpret_cast<char*>(ws);
+        return layer_forward(x, desc->act, recompute, X, A, B, Y, Z, H, -1, nullptr, reinterpret_cast<char*>(ws),
+                             reinterpret_cast<hipStream_t>(stream));
+    });
+}
 
-        void* Hbuf = recompute ? (void*)(w + p.off_h) : H;
-        const int64_t ldh = recompute ? p.ldw : x.ldz;
-        const double es = (double)x.esize;
-        const void* Aw;
-        const void* Bw;
-        int64_t lda, ldb;
-        hipError_t e = use_weight(p.pa, A, x.r, x.d_in, w, &Aw, &lda, s);
-        if (e == hipSuccess) e = use_weight(p.pb, B, x.d_out, x.r, w, &Bw, &ldb, s);
-        if (e != hipSuccess) return hip_fail(e, "pack_rows");
-
-        // K1: Z = X A^T, H = sigma(Z)
-        GemmArgs k1 = make_args(TAG_FWD_Z, x.T, x.r, x.d_in, X, x.ldx, KMAJ, Aw, lda, KMAJ, Z, x.ldz, EPI_Z_H,
-                                desc->act);
-        k1.aux = Hbuf;
-        k1.ldaux = ldh;
-        const double b1 = es * ((double)x.T * x.d_in + (double)x.r * x.d_in + 2.0 * x.T * x.r);
-        e = timed(COLA_KC_FWD_Z, gemm_flops(x.T, x.r, x.d_in), b1, s, [&] { return gemm(k1, x.bf16, s); });
-        if (e != hipSuccess) return hip_fail(e, "fwd_z_sigma");
-
-        // K2: Y = H B^T
-        GemmArgs k2 = make_args(TAG_FWD_Y, x.T, x.d_out, x.r, Hbuf, ldh, KMAJ, Bw, ldb, KMAJ, Y, x.ldy, EPI_STORE,
-                                desc->act);
-        const double b2 = es * ((double)x.T * x.r + (double)x.d_out * x.r + (double)x.T * x.d_out);
-        e = timed(COLA_KC_FWD_Y, gemm_flops(x.T, x.d_out, x.r), b2, s, [&] { return gemm(k2, x.bf16, s); });
-        if (e != hipSuccess) return hip_fail(e, "fwd_y");
-        return COLA_OK;
+int cola_fwd_outer(const cola_desc* desc, int outer_act, const void* X, const void* A, const void* B, void* Y,
+                   void* P, void* Z, void* H, void* ws, size_t ws_bytes, cola_stream_t stream) {
+    return guarded([&]() -> int {
+        Dims x;
+        int st = check_desc(desc, &x);
+        if (st != COLA_OK) return st;
+        if (!valid_act(outer_act)) return COLA_ERR_INVALID_ARG;
+        const bool recompute = desc->recompute == 1;
+        if (recompute ? (H != nullptr) : (H == nullptr && x.T > 0)) return COLA_ERR_INVALID_ARG;
+        if (x.T == 0) return COLA_OK;
+        if (!X || !A || !B || !Y || !P || !Z) return COLA_ERR_INVALID_ARG;
+        const FwdPlan p = plan_fwd(x, recompute);
+        if (p.total > 0 && (!ws || ws_bytes < p.total)) return COLA_ERR_WORKSPACE;
+        return layer_forward(x, desc->act, recompute, X, A, B, Y, Z, H, outer_act, P, reinterpret_cast<char*>(ws),
+                             reinterpret_cast<hipStream_t>(stream));
     });
 }
 
@@ -418,59 +521,40 @@ int cola_bwd(const cola_desc* desc, const void* dY, const void* X, const void* Z
         if (recompute ? (H != nullptr) : (H == nullptr && x.T > 0)) return COLA_ERR_INVALID_ARG;
         if (!dA || !dB) return COLA_ERR_INVALID_ARG;
         hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-        if (x.T == 0) {
-            // empty batch: the token sums are empty, dA = dB = 0
-            hipError_t e = timed(COLA_KC_FILL, 0.0, 4.0 * x.r * x.d_in, s,
-                                 [&] { return launch_fill_zero(dA, x.r * x.d_in, s); });
-            if (e == hipSuccess)
-                e = timed(COLA_KC_FILL, 0.0, 4.0 * x.d_out * x.r, s,
-                          [&] { return launch_fill_zero(dB, x.d_out * x.r, s); });
-            return e == hipSuccess ? COLA_OK : hip_fail(e, "fill_zero");
-        }
+        if (x.T == 0) return zero_weight_grads(x, dA, dB, s);
         if (!dY || !X || !Z || !A || !B || !dX) return COLA_ERR_INVALID_ARG;
         const BwdPlan p = plan_bwd(x, recompute);
         if (!ws || ws_bytes < p.total) return COLA_ERR_WORKSPACE;
+        return layer_backward(x, desc->act, recompute, dY, x.ldy, X, Z, H, A, B, dX, dA, dB,
+                              reinterpret_cast<char*>(ws), s);
+    });
+}
 
-        char* w = reinterpret_cast<char*>(ws);
-        void* dZ = w + p.off_dz;
-        const void* Hbuf = recompute ? (const void*)(w + p.off_h) : H;
-        const int64_t ldh = recompute ? p.ldw : x.ldz;
-        const double es = (double)x.esize;
-        const void* Aw;
-        const void* Bw;
-        int64_t lda, ldb;
-        hipError_t e = use_weight(p.wa, A, x.r, x.d_in, w, &Aw, &lda, s);
-        if (e == hipSuccess) e = use_weight(p.wb, B, x.d_out, x.r, w, &Bw, &ldb, s);
-        if (e != hipSuccess) return hip_fail(e, "pack_rows");
-
-        // K3: dZ = (dY B) (.) sigma'(Z); CoLA-M regenerates H = sigma(Z) here
-        GemmArgs k3 = make_args(TAG_BWD_DZ, x.T, x.r, x.d_out, dY, x.ldy, KMAJ, Bw, ldb, MNMAJ, dZ, p.ldw, EPI_DZ,
-                                desc->act);
-        k3.zin = Z;
-        k3.ldzin = x.ldz;
-        k3.aux = recompute ? (void*)(w + p.off_h) : nullptr;
-        k3.ldaux = p.ldw;
-        const double b3 = es * ((double)x.T * x.d_out + (double)x.d_out * x.r +
-                                (double)x.T * x.r * (recompute ? 3.0 : 2.0));
-        e = timed(COLA_KC_BWD_DZ, gemm_flops(x.T, x.r, x.d_out), b3, s, [&] { return gemm(k3, x.bf16, s); });
-        if (e != hipSuccess) return hip_fail(e, "bwd_dz");
-
-        // K4: dX = dZ A
-        GemmArgs k4 = make_args(TAG_BWD_DX, x.T, x.d_in, x.r, dZ, p.ldw, KMAJ, Aw, lda, MNMAJ, dX, x.ldx, EPI_STORE,
-                                desc->act);
-        const double b4 = es * ((double)x.T * x.r + (double)x.r * x.d_in + (double)x.T * x.d_in);
-        e = timed(COLA_KC_BWD_DX, gemm_flops(x.T, x.d_in, x.r), b4, s, [&] { return gemm(k4, x.bf16, s); });
-        if (e != hipSuccess) return hip_fail(e, "bwd_dx");
-
-        // K5: dA = dZ^T X ; K6: dB = dY^T H  (+ K7 fixed-order reductions)
-        st = wgrad(x.bf16, x.r, x.d_in, x.T, dZ, p.ldw, X, x.ldx, dA, p.sa,
-                   reinterpret_cast<float*>(w + p.off_pa), COLA_KC_BWD_DA,
-                   es * ((double)x.T * x.r + (double)x.T * x.d_in), s);
+int cola_bwd_outer(const cola_desc* desc, int outer_act, const void* dY, const void* P, const void* X,
+                   const void* Z, const void* H, const void* A, const void* B, void* dX, float* dA, float* dB,
+                   void* ws, size_t ws_bytes, cola_stream_t stream) {
+    return guarded([&]() -> int {
+        Dims x;
+        int st = check_desc(desc, &x);
         if (st != COLA_OK) return st;
-        st = wgrad(x.bf16, x.d_out, x.r, x.T, dY, x.ldy, Hbuf, ldh, dB, p.sb,
-                   reinterpret_cast<float*>(w + p.off_pb), COLA_KC_BWD_DB,
-                   es * ((double)x.T * x.d_out + (double)x.T * x.r), s);
-        return st;
+        if (!valid_act(outer_act)) return COLA_ERR_INVALID_ARG;
+        const bool recompute = desc->recompute == 1;
+        if (recompute ? (H != nullptr) : (H == nullptr && x.T > 0)) return COLA_ERR_INVALID_ARG;
+        if (!dA || !dB) return COLA_ERR_INVALID_ARG;
+        hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+        if (x.T == 0) return zero_weight_grads(x, dA, dB, s);
+        if (!dY || !P || !X || !Z || !A || !B || !dX) return COLA_ERR_INVALID_ARG;
+        const OuterPlan o = plan_outer_bwd(x, recompute);
+        if (!ws || ws_bytes < o.total) return COLA_ERR_WORKSPACE;
+        char* w = reinterpret_cast<char*>(ws);
+        // dP = dY (.) sigma_out'(P), rounded to the storage dtype like dZ
+        void* dP = w + o.off_g;
+        const double bytes = (double)x.esize * 3.0 * (double)x.T * (double)x.d_out;
+        hipError_t e = timed(COLA_KC_OUTER_GRAD, 0.0, bytes, s, [&] {
+            return launch_outer_grad(x.bf16, dY, x.ldy, P, x.ldy, dP, o.ldg, x.T, x.d_out, outer_act, s);
+        });
+        if (e != hipSuccess) return hip_fail(e, "outer_grad");
+        return layer_backward(x, desc->act, recompute, dP, o.ldg, X, Z, H, A, B, dX, dA, dB, w, s);
     });
 }
 

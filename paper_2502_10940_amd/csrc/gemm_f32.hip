@@ -183,6 +183,62 @@ __global__ __launch_bounds__(256) void pack_rows_kernel(const uint16_t* __restri
     }
 }
 
+// dP = dY (.) sigma'(P) (the both-sigma variant's backward through its outer
+// sigma).  One thread per group of V consecutive elements of a row (V = 8 for
+// bf16, 4 for fp32: one 16-byte access per operand when every row start is
+// 16-byte aligned), grid-stride over the groups.  bf16 products are taken in
+// fp32 and rounded to nearest even.
+template <bool BF16>
+__global__ __launch_bounds__(256) void outer_grad_kernel(const void* __restrict__ dy, int64_t lddy,
+                                                         const void* __restrict__ p, int64_t ldp,
+                                                         void* __restrict__ out, int64_t ldo, int64_t T,
+                                                         int64_t n, int act, int vec) {
+    constexpr int V = BF16 ? 8 : 4;
+    const int64_t groups = (n + V - 1) / V;
+    const int64_t total = T * groups;
+    const int64_t step = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t g = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; g < total; g += step) {
+        const int64_t t = g / groups;
+        const int64_t c0 = (g - t * groups) * V;
+        const int valid = (int)(n - c0 < V ? n - c0 : V);
+        if constexpr (BF16) {
+            const uint16_t* a = reinterpret_cast<const uint16_t*>(dy) + t * lddy + c0;
+            const uint16_t* b = reinterpret_cast<const uint16_t*>(p) + t * ldp + c0;
+            uint16_t* o = reinterpret_cast<uint16_t*>(out) + t * ldo + c0;
+            if (vec && valid == V) {
+                const uint4 av = *reinterpret_cast<const uint4*>(a);
+                const uint4 bv = *reinterpret_cast<const uint4*>(b);
+                const uint32_t aw[4] = {av.x, av.y, av.z, av.w};
+                const uint32_t bw[4] = {bv.x, bv.y, bv.z, bv.w};
+                uint32_t ow[4];
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    const float lo = bf16_to_f32(aw[k] & 0xffffu) * act_sigma_prime<true>(act, bf16_to_f32(bw[k] & 0xffffu));
+                    const float hi = bf16_to_f32(aw[k] >> 16) * act_sigma_prime<true>(act, bf16_to_f32(bw[k] >> 16));
+                    ow[k] = pack_bf16x2(lo, hi);
+                }
+                *reinterpret_cast<uint4*>(o) = make_uint4(ow[0], ow[1], ow[2], ow[3]);
+            } else {
+                for (int e = 0; e < valid; ++e)
+                    o[e] = (uint16_t)f32_to_bf16(bf16_to_f32(a[e]) * act_sigma_prime<true>(act, bf16_to_f32(b[e])));
+            }
+        } else {
+            const float* a = reinterpret_cast<const float*>(dy) + t * lddy + c0;
+            const float* b = reinterpret_cast<const float*>(p) + t * ldp + c0;
+            float* o = reinterpret_cast<float*>(out) + t * ldo + c0;
+            if (vec && valid == V) {
+                const float4 av = *reinterpret_cast<const float4*>(a);
+                const float4 bv = *reinterpret_cast<const float4*>(b);
+                *reinterpret_cast<float4*>(o) =
+                    make_float4(av.x * act_sigma_prime<false>(act, bv.x), av.y * act_sigma_prime<false>(act, bv.y),
+                                av.z * act_sigma_prime<false>(act, bv.z), av.w * act_sigma_prime<false>(act, bv.w));
+            } else {
+                for (int e = 0; e < valid; ++e) o[e] = a[e] * act_sigma_prime<false>(act, b[e]);
+            }
+        }
+    }
+}
+
 unsigned grid_for(int64_t work) {
     int64_t g = (work + 255) / 256;
     if (g < 1) g = 1;
@@ -205,6 +261,22 @@ hipError_t launch_pack_rows(const void* src, int64_t rows, int64_t width, void* 
     if (rows <= 0) return hipSuccess;
     hipLaunchKernelGGL(pack_rows_kernel, dim3(grid_for(rows * ld)), dim3(256), 0, s,
                        reinterpret_cast<const uint16_t*>(src), rows, width, reinterpret_cast<uint16_t*>(dst), ld);
+    return hipGetLastError();
+}
+
+hipError_t launch_outer_grad(bool bf16, const void* dy, int64_t lddy, const void* p, int64_t ldp, void* out,
+                             int64_t ldo, int64_t T, int64_t n, int act, hipStream_t s) {
+    if (T <= 0 || n <= 0) return hipSuccess;
+    const int64_t V = bf16 ? 8 : 4;
+    auto al = [](const void* q) { return (reinterpret_cast<uintptr_t>(q) & 15u) == 0; };
+    const int vec = al(dy) && al(p) && al(out) && lddy % V == 0 && ldp % V == 0 && ldo % V == 0;
+    const unsigned grid = grid_for(T * ((n + V - 1) / V));
+    if (bf16)
+        hipLaunchKernelGGL(outer_grad_kernel<true>, dim3(grid), dim3(256), 0, s, dy, lddy, p, ldp, out, ldo, T, n,
+                           act, vec);
+    else
+        hipLaunchKernelGGL(outer_grad_kernel<false>, dim3(grid), dim3(256), 0, s, dy, lddy, p, ldp, out, ldo, T, n,
+                           act, vec);
     return hipGetLastError();
 }
 

@@ -25,7 +25,8 @@ enum Epilogue : int {
 // the public timing API).
 enum Tag : int {
     TAG_FWD_Z = 0, TAG_FWD_Y = 1, TAG_BWD_DZ = 2, TAG_BWD_DX = 3, TAG_BWD_DA = 4,
-    TAG_BWD_DB = 5, TAG_DENSE_FWD = 7, TAG_DENSE_DX = 8, TAG_DENSE_DW = 9, TAG_INFER_H = 11
+    TAG_BWD_DB = 5, TAG_DENSE_FWD = 7, TAG_DENSE_DX = 8, TAG_DENSE_DW = 9, TAG_INFER_H = 11,
+    TAG_FWD_YP = 12     // K2 of the both-sigma variant: EPI_Z_H storing P and sigma_out(P)
 };
 
 struct GemmArgs {
@@ -70,6 +71,11 @@ hipError_t launch_pack_rows(const void* src, int64_t rows, int64_t width, void* 
                             hipStream_t s);
 // out[i] = 0 for i < n (fp32 words).
 hipError_t launch_fill_zero(float* out, int64_t n, hipStream_t s);
+
+// out[t][o] = dy[t][o] * sigma_act'(p[t][o]) over T rows of n elements, in
+// the storage dtype (bf16 rounded to nearest even, or fp32).
+hipError_t launch_outer_grad(bool bf16, const void* dy, int64_t lddy, const void* p, int64_t ldp, void* out,
+                             int64_t ldo, int64_t T, int64_t n, int act, hipStream_t s);
 
 // K tile of the bf16 kernel: split-K chunks are multiples of it.
 constexpr int BF16_BK = 64;

@@ -28,7 +28,7 @@ def test_header_declares_expected_calls():
               "dense_fwd", "dense_bwd", "dense_workspace_bytes", "cola_timing_enable",
               "cola_timing_read", "cola_timing_reset", "cola_kernel_name",
               "cola_group_fwd", "cola_group_bwd", "cola_group_workspace_bytes", "cola_infer",
-              "cola_group_infer"):
+              "cola_group_infer", "cola_fwd_outer", "cola_bwd_outer"):
         assert n in names
 
 
@@ -134,7 +134,8 @@ def test_workspace_sizes():
         assert cola.workspace_bytes(dm, 0) >= 1000 * 24 * es         # CoLA-M keeps H here
         assert cola.workspace_bytes(dm, 1) >= cola.workspace_bytes(d, 1) + 1000 * 24 * es
         assert cola.workspace_bytes(d, 2) == cola.workspace_bytes(dm, 0)  # inference keeps H there too
-        assert cola.workspace_bytes(d, 3) == 0
+        assert cola.workspace_bytes(d, 3) >= cola.workspace_bytes(d, 1) + 1000 * 80 * es  # both-sigma: + dP
+        assert cola.workspace_bytes(d, 4) == 0
     empty = cola.desc(0, 96, 80, 24)
     assert cola.workspace_bytes(empty, 0) == 0 and cola.workspace_bytes(empty, 1) == 0
 
@@ -271,7 +272,7 @@ def test_infer_checks():
     # H lives in the workspace whatever recompute says: the CoLA-M forward's size
     need = cola.workspace_bytes(d, 2)
     assert need == cola.workspace_bytes(cola.desc(64, 32, 48, 8, recompute=True), 0) > 0
-    assert cola.workspace_bytes(d, 3) == 0
+    assert cola.workspace_bytes(d, 4) == 0
     assert infer_status(None) == cola.ERR_INVALID_ARG
     for kw in (dict(dtype=7), dict(act=3)):
         assert infer_status(cola.desc(64, 32, 48, 8, **kw)) == cola.ERR_INVALID_ARG
@@ -298,3 +299,40 @@ def test_group_infer_checks():
     assert group_infer_status(d, ws=FAKE, ws_bytes=need - 1) == cola.ERR_WORKSPACE
     e = cola.group_desc(0, 32, [8, 16], [32, 24])
     assert group_infer_status(e, X=None, A=None, B=None, Y=None) == cola.OK
+
+
+def fwd_outer_status(d, outer=1, X=FAKE, A=FAKE, B=FAKE, Y=FAKE, P=FAKE, Z=FAKE, H=FAKE, ws=None, ws_bytes=0):
+    p = ctypes.byref(d) if d is not None else None
+    return cola.lib().cola_fwd_outer(p, outer, X, A, B, Y, P, Z, H, ws, ws_bytes, None)
+
+
+def bwd_outer_status(d, outer=1, dY=FAKE, P=FAKE, X=FAKE, Z=FAKE, H=FAKE, A=FAKE, B=FAKE, dX=FAKE, dA=FAKE,
+                     dB=FAKE, ws=None, ws_bytes=0):
+    p = ctypes.byref(d) if d is not None else None
+    return cola.lib().cola_bwd_outer(p, outer, dY, P, X, Z, H, A, B, dX, dA, dB, ws, ws_bytes, None)
+
+
+def test_outer_checks():
+    d = cola.desc(64, 32, 48, 8)
+    assert fwd_outer_status(None) == cola.ERR_INVALID_ARG
+    assert bwd_outer_status(None) == cola.ERR_INVALID_ARG
+    for bad in (-1, 3, 99):
+        assert fwd_outer_status(d, outer=bad) == cola.ERR_INVALID_ARG
+        assert bwd_outer_status(d, outer=bad) == cola.ERR_INVALID_ARG
+    assert fwd_outer_status(cola.desc(64, 32, 48, 8, act=3)) == cola.ERR_INVALID_ARG
+    assert fwd_outer_status(cola.desc(64, 32, 48, 8, ldy=47)) == cola.ERR_BAD_SHAPE
+    for k in ("X", "A", "B", "Y", "P", "Z"):
+        assert fwd_outer_status(d, **{k: None}) == cola.ERR_INVALID_ARG
+    assert fwd_outer_status(d, H=None) == cola.ERR_INVALID_ARG                       # CoLA needs H
+    m = cola.desc(64, 32, 48, 8, recompute=True)
+    assert fwd_outer_status(m) == cola.ERR_INVALID_ARG                               # CoLA-M takes no H
+    assert fwd_outer_status(m, H=None) == cola.ERR_WORKSPACE
+    # backward: the layer's workspace plus T*d_out elements of dP
+    need = cola.workspace_bytes(d, 3)
+    assert need >= cola.workspace_bytes(d, 1) + 64 * 48 * 2
+    for k in ("dY", "P", "X", "Z", "A", "B", "dX", "dA", "dB"):
+        assert bwd_outer_status(d, ws=FAKE, ws_bytes=need, **{k: None}) == cola.ERR_INVALID_ARG
+    assert bwd_outer_status(d, ws=FAKE, ws_bytes=need - 1) == cola.ERR_WORKSPACE
+    e = cola.desc(0, 32, 48, 8)
+    assert cola.workspace_bytes(e, 3) == 0
+    assert fwd_outer_status(e, X=None, A=None, B=None, Y=None, P=None, Z=None) == cola.OK
