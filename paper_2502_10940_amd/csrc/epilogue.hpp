@@ -88,6 +88,32 @@ __device__ __forceinline__ void transpose_f32(int lane, const float x[4], float 
     y[3] = odd ? z3 : s1;
 }
 
+// Lanes l and l ^ 4 (quads q and q ^ 1 of a 16-lane DPP row) exchange one
+// dword: the lane with bit 2 clear receives its partner's v from lane l + 4
+// (row_shl:4), the other from lane l - 4 (row_shr:4).
+__device__ __forceinline__ uint32_t swap_pair(uint32_t v, bool odd) {
+    const uint32_t up = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x104, 0xF, 0xF, false);
+    const uint32_t dn = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x114, 0xF, 0xF, false);
+    return odd ? dn : up;
+}
+
+// Two horizontally adjacent 32 x 32 tiles (j, j + 1) after the quad
+// transposes: lane 4q + b holds columns 4q .. 4q+3 of tile j in a0, a1 and of
+// tile j + 1 in b0, b1.  Quad pairs (q, q ^ 1) trade halves so that the even
+// quad holds columns 8m .. 8m+7 of tile j and the odd one those of tile j + 1
+// (m = q / 2): 16 bytes per lane, and one store instruction writes 8 whole
+// rows of 128 contiguous bytes (the two tiles' 64 columns).  Returns the
+// column (relative to tile j) of the lane's first element.
+__device__ __forceinline__ int pair_tiles(int lane, uint32_t a0, uint32_t a1, uint32_t b0, uint32_t b1,
+                                          u32x4_t& out) {
+    const int q = (lane & 31) >> 2;
+    const bool odd = (q & 1) != 0;
+    const uint32_t r0 = swap_pair(odd ? a0 : b0, odd);
+    const uint32_t r1 = swap_pair(odd ? a1 : b1, odd);
+    out = odd ? u32x4_t{r0, r1, b0, b1} : u32x4_t{a0, a1, r0, r1};
+    return 32 * (q & 1) + 8 * (q >> 1);
+}
+
 // Four bf16 (q0 = columns 0,1, q1 = columns 2,3) to p: one 8-byte store when
 // vec, else the first `valid` elements one by one.
 __device__ __forceinline__ void store_bf16x4(uint16_t* p, uint32_t q0, uint32_t q1, bool vec, int valid) {
@@ -177,6 +203,56 @@ __device__ __forceinline__ u32x2_t z4(const GemmArgs& a, int64_t gm, int64_t gn)
         return *reinterpret_cast<const u32x2_t*>(reinterpret_cast<const uint16_t*>(a.zin) + gm * a.ldzin + gn);
     else
         return load_z4(a, gm, gn);
+}
+
+// Interior blocks with 16-byte aligned rows (bf16 outputs): the quad
+// transposes of tile pairs, then whole 128-byte row segments per store.
+// Bitwise the values of the 8-byte path (same roundings, same sigma).
+template <int EPI, int TM, int TN>
+__device__ __forceinline__ void epilogue_lines(const GemmArgs& a, const f32x16 (&acc)[TM][TN], int64_t row0,
+                                               int64_t col0, int lane) {
+    static_assert(TN % 2 == 0, "tile pairs");
+    static_assert(EPI == EPI_STORE || EPI == EPI_H || EPI == EPI_Z_H, "bf16 stores without an input");
+    const int64_t lrow = 4 * (lane >> 5) + (lane & 3);
+    const QuadSel sel(lane);
+    uint16_t* C = reinterpret_cast<uint16_t*>(a.c);
+    uint16_t* Hp = reinterpret_cast<uint16_t*>(a.aux);
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int g = 0; g < 4; ++g)
+#pragma unroll
+            for (int jp = 0; jp < TN / 2; ++jp) {
+                const int64_t gm = row0 + 32 * i + 8 * g + lrow;
+                uint32_t c[2][2], h[2][2];
+#pragma unroll
+                for (int t = 0; t < 2; ++t) {
+                    const f32x16& v = acc[i][2 * jp + t];
+                    float x[4];
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        x[e] = v[4 * g + e];
+                        if constexpr (EPI == EPI_H) x[e] = act_sigma<true>(a.act, round_bf16(x[e]));
+                    }
+                    transpose_bf16(sel, pack_bf16x2(x[0], x[1]), pack_bf16x2(x[2], x[3]), c[t][0], c[t][1]);
+                    if constexpr (EPI == EPI_Z_H) {
+                        float y[4];
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) y[e] = act_sigma<true>(a.act, round_bf16(x[e]));
+                        transpose_bf16(sel, pack_bf16x2(y[0], y[1]), pack_bf16x2(y[2], y[3]), h[t][0], h[t][1]);
+                    }
+                }
+                u32x4_t o;
+                const int dc = pair_tiles(lane, c[0][0], c[0][1], c[1][0], c[1][1], o);
+                const int64_t gn = col0 + 64 * jp + dc;
+                *reinterpret_cast<u32x4_t*>(C + gm * a.ldc + gn) = o;
+                if constexpr (EPI == EPI_Z_H) {
+                    if (Hp) {
+                        pair_tiles(lane, h[0][0], h[0][1], h[1][0], h[1][1], o);
+                        *reinterpret_cast<u32x4_t*>(Hp + gm * a.ldaux + gn) = o;
+                    }
+                }
+            }
 }
 
 template <int EPI, bool FAST, int TM, int TN>
@@ -272,6 +348,15 @@ __device__ __forceinline__ void epilogue_block(const GemmArgs& a, const f32x16 (
     }
     if constexpr (EPI == EPI_Z_H || EPI == EPI_DZ) fast = fast && (a.aux == nullptr || al(a.aux, a.ldaux, 4));
     if constexpr (EPI == EPI_DZ) fast = fast && al(a.zin, a.ldzin, 4);
+    if constexpr ((EPI == EPI_STORE || EPI == EPI_H || EPI == EPI_Z_H) && TN % 2 == 0) {
+        // 16-byte rows: whole 128-byte row segments per store
+        bool line = fast && al(a.c, a.ldc, 8);
+        if constexpr (EPI == EPI_Z_H) line = line && (a.aux == nullptr || al(a.aux, a.ldaux, 8));
+        if (line) {
+            epilogue_lines<EPI>(a, acc, row0, col0, lane);
+            return;
+        }
+    }
     if (fast) epilogue_block_impl<EPI, true>(a, acc, row0, col0, lane, split);
     else epilogue_block_impl<EPI, false>(a, acc, row0, col0, lane, split);
 }

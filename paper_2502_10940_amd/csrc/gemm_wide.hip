@@ -230,14 +230,18 @@ __device__ __forceinline__ void wait_vm_at_most(int n) {
     }
 }
 
-// Vector-memory operations one wave issues in the epilogue of a tile whose
-// every 4-column group takes the vector path (4 TM TN groups per lane).
+// Vector-memory operations one wave issues in the epilogue of an interior
+// tile with aligned outputs (4 TM TN groups of 4 columns per lane).  The bf16
+// stores without an input take the whole-line path there (one 16-byte store
+// per two groups, TN even).  An over-count would shorten a wait, so where the
+// path is not certain the smaller count is used.
 template <int EPI>
 __device__ __forceinline__ int epilogue_ops(bool aux) {
     constexpr int G = 4 * TM * TN;
-    return EPI == EPI_STORE || EPI == EPI_H ? G
+    static_assert(TN % 2 == 0, "whole-line epilogue");
+    return EPI == EPI_STORE || EPI == EPI_H ? G / 2
          : EPI == EPI_STORE_F32 ? G
-         : EPI == EPI_Z_H ? (aux ? 2 * G : G)
+         : EPI == EPI_Z_H ? (aux ? G : G / 2)
          : (aux ? 3 * G : 2 * G);               // EPI_DZ: Z loads, dZ (and H) stores
 }
 
