@@ -90,4 +90,30 @@ __device__ __forceinline__ void act_sigma_both(int act, float z, float& sig, flo
     }
 }
 
+// The same with the activation fixed at compile time (ACT = 0 identity,
+// 1 SiLU, 2 GeLU): the GEMM epilogues choose ACT once per block, so the
+// unrolled per-element code has no branches.
+template <int ACT, bool FAST>
+__device__ __forceinline__ float act_sigma_c(float z) {
+    if constexpr (ACT == 0) return z;
+    else if constexpr (ACT == 2) return z * normal_cdf<FAST>(z);
+    else return z * (FAST ? logistic_fast(z) : logistic_exact(z));
+}
+
+template <int ACT, bool FAST>
+__device__ __forceinline__ void act_sigma_both_c(float z, float& sig, float& sigp) {
+    if constexpr (ACT == 0) {
+        sig = z;
+        sigp = 1.0f;
+    } else if constexpr (ACT == 2) {
+        const float cdf = normal_cdf<FAST>(z);
+        sig = z * cdf;
+        sigp = cdf + z * normal_pdf<FAST>(z);
+    } else {
+        const float s = FAST ? logistic_fast(z) : logistic_exact(z);
+        sig = z * s;
+        sigp = s * (1.0f + z * (1.0f - s));
+    }
+}
+
 }  // namespace cola

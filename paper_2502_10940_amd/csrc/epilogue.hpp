@@ -142,8 +142,9 @@ __device__ __forceinline__ u32x2_t load_z4(const GemmArgs& a, int64_t gm, int64_
 
 // Epilogue of 4 consecutive columns (gn .. gn+3) of output row gm; zz: the
 // matching Z values (EPI_DZ only).  FAST: the 4 columns exist and every
-// pointer is aligned for one vector access (checked once per block).
-template <int EPI, bool FAST>
+// pointer is aligned for one vector access (checked once per block).  ACT:
+// the activation (a.act, fixed per instantiation).
+template <int EPI, bool FAST, int ACT>
 __device__ __forceinline__ void epilogue4(const GemmArgs& a, int64_t gm, int64_t gn, const float v[4], int split,
                                           u32x2_t zz = u32x2_t{0u, 0u}) {
     if (!FAST && (gm >= a.M || gn >= a.N)) return;
@@ -168,20 +169,20 @@ __device__ __forceinline__ void epilogue4(const GemmArgs& a, int64_t gm, int64_t
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
                 out[e] = round_bf16(v[e]);
-                h[e] = act_sigma<true>(a.act, out[e]);
+                h[e] = act_sigma_c<ACT, true>(out[e]);
             }
         } else if constexpr (EPI == EPI_H) {
             // the H of EPI_Z_H: sigma of Z rounded to bf16
 #pragma unroll
-            for (int e = 0; e < 4; ++e) out[e] = act_sigma<true>(a.act, round_bf16(v[e]));
+            for (int e = 0; e < 4; ++e) out[e] = act_sigma_c<ACT, true>(round_bf16(v[e]));
         } else if constexpr (EPI == EPI_DZ) {
             const float z[4] = {bf16_to_f32(zz[0] & 0xffffu), bf16_to_f32(zz[0] >> 16),
                                 bf16_to_f32(zz[1] & 0xffffu), bf16_to_f32(zz[1] >> 16)};
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
                 float sp;
-                act_sigma_both<true>(a.act, z[e], h[e], sp);
-                out[e] = a.act == 0 ? v[e] : v[e] * sp;
+                act_sigma_both_c<ACT, true>(z[e], h[e], sp);
+                out[e] = ACT == 0 ? v[e] : v[e] * sp;
             }
         }
         const bool vec = FAST || (valid == 4 && (reinterpret_cast<uintptr_t>(c) & 7u) == 0);
@@ -208,7 +209,7 @@ __device__ __forceinline__ u32x2_t z4(const GemmArgs& a, int64_t gm, int64_t gn)
 // Interior blocks with 16-byte aligned rows (bf16 outputs): the quad
 // transposes of tile pairs, then whole 128-byte row segments per store.
 // Bitwise the values of the 8-byte path (same roundings, same sigma).
-template <int EPI, int TM, int TN>
+template <int EPI, int ACT, int TM, int TN>
 __device__ __forceinline__ void epilogue_lines(const GemmArgs& a, const f32x16 (&acc)[TM][TN], int64_t row0,
                                                int64_t col0, int lane) {
     static_assert(TN % 2 == 0, "tile pairs");
@@ -232,13 +233,13 @@ __device__ __forceinline__ void epilogue_lines(const GemmArgs& a, const f32x16 (
 #pragma unroll
                     for (int e = 0; e < 4; ++e) {
                         x[e] = v[4 * g + e];
-                        if constexpr (EPI == EPI_H) x[e] = act_sigma<true>(a.act, round_bf16(x[e]));
+                        if constexpr (EPI == EPI_H) x[e] = act_sigma_c<ACT, true>(round_bf16(x[e]));
                     }
                     transpose_bf16(sel, pack_bf16x2(x[0], x[1]), pack_bf16x2(x[2], x[3]), c[t][0], c[t][1]);
                     if constexpr (EPI == EPI_Z_H) {
                         float y[4];
 #pragma unroll
-                        for (int e = 0; e < 4; ++e) y[e] = act_sigma<true>(a.act, round_bf16(x[e]));
+                        for (int e = 0; e < 4; ++e) y[e] = act_sigma_c<ACT, true>(round_bf16(x[e]));
                         transpose_bf16(sel, pack_bf16x2(y[0], y[1]), pack_bf16x2(y[2], y[3]), h[t][0], h[t][1]);
                     }
                 }
@@ -255,7 +256,7 @@ __device__ __forceinline__ void epilogue_lines(const GemmArgs& a, const f32x16 (
             }
 }
 
-template <int EPI, bool FAST, int TM, int TN>
+template <int EPI, bool FAST, int ACT, int TM, int TN>
 __device__ __forceinline__ void epilogue_block_impl(const GemmArgs& a, const f32x16 (&acc)[TM][TN],
                                                     int64_t row0, int64_t col0, int lane, int split) {
     const int64_t lrow = 4 * (lane >> 5) + (lane & 3);     // this lane's row within a group of 8
@@ -264,7 +265,7 @@ __device__ __forceinline__ void epilogue_block_impl(const GemmArgs& a, const f32
         // round to bf16 first, then transpose 16-bit pairs (half the exchange
         // work); sigma is elementwise, so EPI_H applies it before the transpose
         const QuadSel sel(lane);
-        auto f = [&](float v) { return EPI == EPI_H ? act_sigma<true>(a.act, round_bf16(v)) : v; };
+        auto f = [&](float v) { return EPI == EPI_H ? act_sigma_c<ACT, true>(round_bf16(v)) : v; };
 #pragma unroll
         for (int i = 0; i < TM; ++i)
 #pragma unroll
@@ -310,8 +311,8 @@ __device__ __forceinline__ void epilogue_block_impl(const GemmArgs& a, const f32
                                         acc[i][j][4 * g + 3]};
                     float y[4];
                     transpose_f32(lane, x, y);
-                    epilogue4<EPI, FAST>(a, row0 + 32 * i + 8 * g + lrow, col0 + 32 * j + lcol, y, split,
-                                         zb[i & 1][g][j]);
+                    epilogue4<EPI, FAST, ACT>(a, row0 + 32 * i + 8 * g + lrow, col0 + 32 * j + lcol, y, split,
+                                              zb[i & 1][g][j]);
                 }
         }
     } else {
@@ -325,16 +326,17 @@ __device__ __forceinline__ void epilogue_block_impl(const GemmArgs& a, const f32
                                         acc[i][j][4 * g + 3]};
                     float y[4];
                     transpose_f32(lane, x, y);
-                    epilogue4<EPI, FAST>(a, row0 + 32 * i + 8 * g + lrow, col0 + 32 * j + lcol, y, split);
+                    epilogue4<EPI, FAST, ACT>(a, row0 + 32 * i + 8 * g + lrow, col0 + 32 * j + lcol, y, split);
                 }
     }
 }
 
 // The whole epilogue of one wave's block of TM x TN MFMA tiles, whose first
-// output row and column are row0, col0.  Blocks wholly inside the output with
-// aligned pointers (the common case) take the unguarded vector path.
-template <int EPI, int TM, int TN>
-__device__ __forceinline__ void epilogue_block(const GemmArgs& a, const f32x16 (&acc)[TM][TN],
+// output row and column are row0, col0, for activation ACT.  Blocks wholly
+// inside the output with aligned pointers (the common case) take the
+// unguarded vector path.
+template <int EPI, int ACT, int TM, int TN>
+__device__ __forceinline__ void epilogue_block_act(const GemmArgs& a, const f32x16 (&acc)[TM][TN],
                                                int64_t row0, int64_t col0, int lane, int split) {
     auto al = [](const void* p, int64_t ld, int64_t elems) {   // rows of elems-element vectors
         return p != nullptr && (reinterpret_cast<uintptr_t>(p) % (2 * elems)) == 0 && ld % elems == 0;
@@ -353,12 +355,26 @@ __device__ __forceinline__ void epilogue_block(const GemmArgs& a, const f32x16 (
         bool line = fast && al(a.c, a.ldc, 8);
         if constexpr (EPI == EPI_Z_H) line = line && (a.aux == nullptr || al(a.aux, a.ldaux, 8));
         if (line) {
-            epilogue_lines<EPI>(a, acc, row0, col0, lane);
+            epilogue_lines<EPI, ACT>(a, acc, row0, col0, lane);
             return;
         }
     }
-    if (fast) epilogue_block_impl<EPI, true>(a, acc, row0, col0, lane, split);
-    else epilogue_block_impl<EPI, false>(a, acc, row0, col0, lane, split);
+    if (fast) epilogue_block_impl<EPI, true, ACT>(a, acc, row0, col0, lane, split);
+    else epilogue_block_impl<EPI, false, ACT>(a, acc, row0, col0, lane, split);
+}
+
+// The epilogue of a wave's block with the activation a.act chosen once here
+// (epilogues without sigma ignore it).
+template <int EPI, int TM, int TN>
+__device__ __forceinline__ void epilogue_block(const GemmArgs& a, const f32x16 (&acc)[TM][TN],
+                                               int64_t row0, int64_t col0, int lane, int split) {
+    if constexpr (EPI == EPI_STORE || EPI == EPI_STORE_F32) {
+        epilogue_block_act<EPI, 0>(a, acc, row0, col0, lane, split);
+    } else {
+        if (a.act == 0) epilogue_block_act<EPI, 0>(a, acc, row0, col0, lane, split);
+        else if (a.act == 2) epilogue_block_act<EPI, 2>(a, acc, row0, col0, lane, split);
+        else epilogue_block_act<EPI, 1>(a, acc, row0, col0, lane, split);
+    }
 }
 
 }  // namespace cola
