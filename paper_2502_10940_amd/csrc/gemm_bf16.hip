@@ -298,7 +298,7 @@ hipError_t launch_layout(const GemmArgs& a, hipStream_t s) {
 
 }  // namespace
 
-// The BIG family takes only operands with 16-byte aligned rows whose tile
+// The BIG and PP families take only operands with 16-byte aligned rows whose tile
 // offsets fit its 32-bit per-lane offsets.
 bool big_operands_ok(const GemmArgs& a) {
     auto al = [](const void* p, int64_t ld) {
@@ -315,24 +315,24 @@ int gemm_family(int64_t M, int64_t N, int tag) {
         if (!strcmp(e, "stream")) return (int)FAM_STREAM;
         if (!strcmp(e, "wide")) return (int)FAM_WIDE;
         if (!strcmp(e, "big")) return (int)FAM_BIG;
+        if (!strcmp(e, "pp")) return (int)FAM_PP;
         return -1;
     }();
-    if (forced == FAM_WIDE || forced == FAM_BIG) return bf16_wide_ok(M, N) ? forced : (int)FAM_STREAM;
+    if (forced == FAM_WIDE || forced == FAM_BIG || forced == FAM_PP) return bf16_wide_ok(M, N) ? forced : (int)FAM_STREAM;
     if (forced >= 0) return forced;
-    // The 256 x 256 family wins where K is long and its tiles fill the chip
-    // in one round (the forward projection to the rank, Z = X A^T: N = r,
-    // K = d_in); the streaming family's two workgroups per CU hide the
-    // epilogue of the short-K products and the split weight gradients better
-    // (measured per shape on MI355X).
-    const bool fwd_z = tag == TAG_FWD_Z || tag == TAG_INFER_H;
-    if (fwd_z && bf16_wide_ok(M, N) && ((M + 255) / 256) * ((N + 255) / 256) >= 256) return FAM_BIG;
-    return FAM_STREAM;
+    // 256 x 256 tiles in ping-pong wherever both output dimensions exceed one
+    // 128-wide tile (measured on MI355X: 1.1-1.5x the streaming family on
+    // the products of the layer, weight gradients included); the streaming
+    // family for skinny outputs.
+    (void)tag;
+    return bf16_wide_ok(M, N) ? (int)FAM_PP : (int)FAM_STREAM;
 }
 
 hipError_t launch_gemm_bf16(const GemmArgs& a, hipStream_t s) {
     switch (gemm_family(a.M, a.N, a.tag)) {
         case FAM_WIDE: return launch_gemm_wide(a, s);
         case FAM_BIG: return big_operands_ok(a) ? launch_gemm_big(a, s) : launch_gemm_stream(a, s);
+        case FAM_PP: return big_operands_ok(a) ? launch_gemm_pp(a, s) : launch_gemm_stream(a, s);
         case FAM_STREAM: return launch_gemm_stream(a, s);
         default: return launch_gemm_reg(a, s);
     }

@@ -34,16 +34,10 @@
 #include "internal.hpp"
 #include "device_math.hpp"
 #include "epilogue.hpp"
+#include "lds_tile.hpp"
 
 namespace cola {
 namespace {
-
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef short s16x4 __attribute__((ext_vector_type(4)));
-typedef short s16x8 __attribute__((ext_vector_type(8)));
-typedef const __attribute__((address_space(1))) void* gptr_t;
-typedef __attribute__((address_space(3))) void* lptr_t;
-typedef __attribute__((address_space(3))) s16x4* lptr4_t;
 
 constexpr int BM = 256;
 constexpr int BN = 256;
@@ -52,179 +46,6 @@ constexpr int WR = 128;          // rows of a wave's block
 constexpr int WC = 128;          // columns of a wave's block
 constexpr int TM = WR / 32;
 constexpr int TN = WC / 32;
-
-__device__ __forceinline__ int wave_id() { return __builtin_amdgcn_readfirstlane(threadIdx.x >> 6); }
-
-// Buffer descriptor of a wave-uniform base address (raw buffer, no range
-// check: every offset the kernel uses is in bounds by construction).
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc_of(const char* ubase) {
-    return __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(ubase), (short)0, 0x7fffffff, 0x00020000);
-}
-// 16 bytes per lane from base + voff (scalar descriptor, 32-bit per-lane
-// offset: buffer_load_dwordx4 ... lds) to LDS bytes [lds + 16 lane, +16).
-__device__ __forceinline__ void dtl16(__amdgpu_buffer_rsrc_t r, uint32_t voff, char* lds) {
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lptr_t)lds, 16, voff, 0, 0, 0);
-}
-
-__device__ __forceinline__ uint4 load8_guarded(const uint16_t* p, int valid) {
-    uint32_t w[4];
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-        const uint32_t lo = (2 * e < valid) ? p[2 * e] : 0u;
-        const uint32_t hi = (2 * e + 1 < valid) ? p[2 * e + 1] : 0u;
-        w[e] = lo | (hi << 16);
-    }
-    return make_uint4(w[0], w[1], w[2], w[3]);
-}
-
-template <int LAYOUT, int BK>
-struct BTile;
-
-// ---- k-contiguous operand: LDS [256 rows][BK k] ----
-template <int BK>
-struct BTile<KMAJ, BK> {
-    static constexpr int CR = BK / 8;                 // 16-byte chunks per row
-    static constexpr int RPI = 64 / CR;               // rows per 1 KB instruction
-    static constexpr int BYTES = 256 * BK * 2;
-    static constexpr int DPW = BYTES / 1024 / 4;      // direct-to-LDS instructions per wave
-    static constexpr int FRAG_READS = 1;              // LDS reads per fragment
-    static_assert(CR == 4 || CR == 8, "BK of 32 or 64");
-
-    // chunk c of row r sits at chunk c ^ swz(r): the 16 rows a quarter-wave
-    // reads cover all 64 banks once
-    __device__ static __forceinline__ int swz(int row) { return (row / (16 / CR)) & (CR - 1); }
-    __device__ static __forceinline__ int off(int row, int c) { return row * (2 * BK) + ((c ^ swz(row)) << 4); }
-
-    // Per-lane byte offset of instruction j, relative to the K tile's first
-    // element (row0, k0).  Rows past the edge re-read the last row.
-    __device__ static __forceinline__ uint32_t voff(int j, int64_t ld, int64_t row0, int64_t rows) {
-        const int lane = threadIdx.x & 63;
-        const int blk = DPW * wave_id() + j;
-        const int row = RPI * blk + lane / CR;
-        const int lc = (lane % CR) ^ swz(row);
-        const int64_t lrow = row0 + row < rows ? row : rows - 1 - row0;
-        return 2u * ((uint32_t)lrow * (uint32_t)ld + 8u * (uint32_t)lc);
-    }
-    __device__ static __forceinline__ const char* gbase(const uint16_t* base, int64_t ld, int64_t row0, int64_t k0) {
-        return reinterpret_cast<const char*>(base + row0 * ld + k0);
-    }
-
-    // Guarded register path (partial K tile): zeros past kend.
-    __device__ static __forceinline__ void load_store(char* lds, const uint16_t* base, int64_t ld, int64_t row0,
-                                                      int64_t rows, int64_t k0, int64_t kend) {
-#pragma unroll
-        for (int i = 0; i < 256 * CR / NT; ++i) {
-            const int id = threadIdx.x + NT * i;
-            const int64_t row = row0 + id / CR;
-            const int64_t k = k0 + 8 * (id % CR);
-            const int64_t valid = row < rows ? kend - k : 0;
-            const uint4 v = load8_guarded(base + (row < rows ? row : 0) * ld + (valid > 0 ? k : 0),
-                                          (int)(valid < 0 ? 0 : (valid > 8 ? 8 : valid)));
-            *reinterpret_cast<uint4*>(lds + off(id / CR, id % CR)) = v;
-        }
-    }
-
-    // 32 rows (row0 ..) x 16 k (16 s ..) fragment
-    __device__ static __forceinline__ bf16x8 frag(const char* lds, int row0, int s, int lane) {
-        return *reinterpret_cast<const bf16x8*>(lds + off(row0 + (lane & 31), 2 * s + (lane >> 5)));
-    }
-};
-
-// ---- m-contiguous operand: LDS [BK k][256 m] (512-byte rows) ----
-template <int BK>
-struct BTile<MNMAJ, BK> {
-    static constexpr int BYTES = BK * 256 * 2;
-    static constexpr int DPW = BYTES / 1024 / 4;
-    static constexpr int FRAG_READS = 2;
-
-    __device__ static __forceinline__ int off(int k, int c) { return k * 512 + ((c ^ ((k & 3) << 2)) << 4); }
-
-    // Instruction j fills k rows 2 blk, 2 blk + 1; chunks that start past the
-    // last column re-read the last chunk.
-    __device__ static __forceinline__ uint32_t voff(int j, int64_t ld, int64_t m0, int64_t rows) {
-        const int lane = threadIdx.x & 63;
-        const int64_t mlast = ((rows - 1) >> 3) << 3;
-        const int blk = DPW * wave_id() + j;
-        const int k = 2 * blk + (lane >> 5);
-        const int lc = (lane & 31) ^ ((k & 3) << 2);
-        const int64_t lm = m0 + 8 * lc <= mlast ? 8 * lc : mlast - m0;
-        return 2u * ((uint32_t)k * (uint32_t)ld + (uint32_t)lm);
-    }
-    __device__ static __forceinline__ const char* gbase(const uint16_t* base, int64_t ld, int64_t m0, int64_t k0) {
-        return reinterpret_cast<const char*>(base + k0 * ld + m0);
-    }
-
-    __device__ static __forceinline__ void load_store(char* lds, const uint16_t* base, int64_t ld, int64_t m0,
-                                                      int64_t rows, int64_t k0, int64_t kend) {
-#pragma unroll
-        for (int i = 0; i < BK * 32 / NT; ++i) {
-            const int id = threadIdx.x + NT * i;
-            const int64_t k = k0 + id / 32;
-            const int64_t m = m0 + 8 * (id % 32);
-            const int64_t valid = k < kend ? rows - m : 0;
-            const uint4 v = load8_guarded(base + (k < kend ? k : 0) * ld + (valid > 0 ? m : 0),
-                                          (int)(valid < 0 ? 0 : (valid > 8 ? 8 : valid)));
-            *reinterpret_cast<uint4*>(lds + off(id / 32, id % 32)) = v;
-        }
-    }
-
-    // 32 m (m0 ..) x 16 k (16 s ..) fragment via two transposing reads: in
-    // each 16-lane group, lanes 4q..4q+3 point at k row q of a 4 x 16 block
-    // (four consecutive m each) and lane i receives column m0 + i.
-    __device__ static __forceinline__ bf16x8 frag(const char* lds, int m0, int s, int lane) {
-        const int g = lane >> 4;
-        const int i = lane & 15;
-        const int m = m0 + 16 * (g & 1) + 4 * (i & 3);
-        const int k = 16 * s + 8 * (g >> 1) + (i >> 2);
-        const int byte = (m & 7) * 2;
-        const int c = m >> 3;
-        const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lptr4_t)(lds + off(k, c) + byte));
-        const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lptr4_t)(lds + off(k + 4, c) + byte));
-        const s16x8 s8 = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
-        return __builtin_bit_cast(bf16x8, s8);
-    }
-};
-
-// Scheduling hints: sched_group_barrier masks (MFMA, all VMEM, DS read).
-constexpr int SG_MFMA = 0x008;
-constexpr int SG_VMEM = 0x010;
-constexpr int SG_DSR = 0x100;
-
-// Scheduling pattern of M MFMAs with R LDS reads and V vector-memory
-// loads spread over them: after MFMA n come the reads and loads whose even
-// share falls there (floor((n+1) R / M) - floor(n R / M) of each), so that no
-// gap between two MFMAs holds more than a few instructions -- with one wave
-// per SIMD, a gap longer than an MFMA's 32 cycles idles the matrix pipe.
-template <int M, int R, int V, int N = 0>
-__device__ __forceinline__ void sched_spread() {
-    if constexpr (N < M) {
-        constexpr int r = (N + 1) * R / M - N * R / M;
-        constexpr int v = (N + 1) * V / M - N * V / M;
-        __builtin_amdgcn_sched_group_barrier(SG_MFMA, 1, 0);
-        if constexpr (r > 0) __builtin_amdgcn_sched_group_barrier(SG_DSR, r, 0);
-        if constexpr (v > 0) __builtin_amdgcn_sched_group_barrier(SG_VMEM, v, 0);
-        sched_spread<M, R, V, N + 1>();
-    }
-}
-
-__device__ __forceinline__ void barrier_lds() {
-    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
-}
-template <int N>
-__device__ __forceinline__ void wait_vm() {
-    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
-}
-template <class T, T V>
-using ic = std::integral_constant<T, V>;
-
-// f(ic<int, 0>), ..., f(ic<int, N - 1>): a loop whose index is a constant.
-template <int N, int I = 0, class F>
-__device__ __forceinline__ void static_for(F&& f) {
-    if constexpr (I < N) {
-        f(ic<int, I>{});
-        static_for<N, I + 1>(f);
-    }
-}
 
 // Coordinates of one output tile (and K range) of a persistent workgroup.
 struct BigTile {
@@ -301,9 +122,9 @@ __global__ __launch_bounds__(NT, 1) void gemm_big_kernel(GemmArgs a) {
     };
     auto offs_for = [&](const BigTile& t, Offs& o) {
 #pragma unroll
-        for (int j = 0; j < POPS; ++j) o.p[j] = TP::voff(j, a.ldp, t.m0, a.M);
+        for (int j = 0; j < POPS; ++j) o.p[j] = TP::voff(POPS * wave + j, a.ldp, t.m0, a.M);
 #pragma unroll
-        for (int j = 0; j < QOPS; ++j) o.q[j] = TQ::voff(j, a.ldq, t.n0, a.N);
+        for (int j = 0; j < QOPS; ++j) o.q[j] = TQ::voff(QOPS * wave + j, a.ldq, t.n0, a.N);
     };
     // K tile kt of a tile whose first K tile has global number g0 sits in P
     // slot (g0 + kt) % NP and Q slot (g0 + kt) % NQ.
@@ -470,8 +291,8 @@ __global__ __launch_bounds__(NT, 1) void gemm_big_kernel(GemmArgs a) {
             char* qs = qslot(g0 + nkf + NQ - 1);
             const int64_t k0 = cur.kbeg + (int64_t)nkf * BK;
             barrier_lds();
-            TP::load_store(ps, P, a.ldp, cur.m0, a.M, k0, cur.kend);
-            TQ::load_store(qs, Q, a.ldq, cur.n0, a.N, k0, cur.kend);
+            TP::template load_store<NT>(ps, P, a.ldp, cur.m0, a.M, k0, cur.kend);
+            TQ::template load_store<NT>(qs, Q, a.ldq, cur.n0, a.N, k0, cur.kend);
             barrier_lds();
 #pragma unroll
             for (int s = 0; s < NSUB; ++s) {

@@ -54,12 +54,14 @@ hipError_t launch_gemm_reg(const GemmArgs& a, hipStream_t s);
 hipError_t launch_gemm_stream(const GemmArgs& a, hipStream_t s);
 hipError_t launch_gemm_wide(const GemmArgs& a, hipStream_t s);
 //   BIG    -- 256 x 256 tiles, one wave per SIMD, software-pipelined K loop
+//   PP     -- 256 x 256 tiles, two wave groups per workgroup in ping-pong
 hipError_t launch_gemm_big(const GemmArgs& a, hipStream_t s);
+hipError_t launch_gemm_pp(const GemmArgs& a, hipStream_t s);
 
-enum Family : int { FAM_REG = 0, FAM_STREAM = 1, FAM_WIDE = 2, FAM_BIG = 3 };
+enum Family : int { FAM_REG = 0, FAM_STREAM = 1, FAM_WIDE = 2, FAM_BIG = 3, FAM_PP = 4 };
 // Family used for a GEMM (also used by the split planner).  The environment
-// variable COLA_GEMM_FAMILY (reg | stream | wide | big) overrides the default,
-// for tuning and comparisons.
+// variable COLA_GEMM_FAMILY (reg | stream | wide | big | pp) overrides the
+// default, for tuning and comparisons.
 int gemm_family(int64_t M, int64_t N, int tag);
 hipError_t launch_gemm_f32(const GemmArgs& a, hipStream_t s);
 
@@ -84,13 +86,13 @@ constexpr int BF16_BK = 64;
 // K tile of the fp32 kernel.
 constexpr int F32_BK = 16;
 
-// Tile geometry of the launchers (mirrored here for planning): the WIDE and
-// BIG families use 256 x 256 (only when M > 128 and N > 128), the others BM x 128
+// Tile geometry of the launchers (mirrored here for planning): the WIDE, BIG
+// and PP families use 256 x 256 (only when M > 128 and N > 128), the others BM x 128
 // with BM = 256 (128 when M <= 128); fp32 uses 64 x 64.
 inline bool bf16_wide_ok(int64_t M, int64_t N) { return M > 128 && N > 128; }
 inline int64_t gemm_tiles(bool bf16, int64_t M, int64_t N, int tag) {
     const int fam = bf16 ? gemm_family(M, N, tag) : -1;
-    const bool wide = fam == FAM_WIDE || fam == FAM_BIG;
+    const bool wide = fam == FAM_WIDE || fam == FAM_BIG || fam == FAM_PP;
     const int64_t tm = bf16 ? (M > 128 ? 256 : 128) : 64;
     const int64_t tn = bf16 ? (wide ? 256 : 128) : 64;
     return ((M + tm - 1) / tm) * ((N + tn - 1) / tn);
@@ -99,7 +101,7 @@ inline int64_t gemm_tiles(bool bf16, int64_t M, int64_t N, int tag) {
 inline int64_t gemm_slots(bool bf16, int64_t M, int64_t N, int tag) {
     if (!bf16) return 1024;
     const int fam = gemm_family(M, N, tag);
-    return fam == FAM_WIDE || fam == FAM_BIG ? 256 : 512;
+    return fam == FAM_WIDE || fam == FAM_BIG || fam == FAM_PP ? 256 : 512;
 }
 
 }  // namespace cola
