@@ -208,8 +208,234 @@ __global__ __launch_bounds__(NTHR, 1) void gemm_pp_kernel(GemmArgs a) {
     epilogue_block<EPI>(a, acc, m0 + grp * WR, n0 + wl * WC, lane, split);
 }
 
+// ---- persistent variant (every K range a whole number of K tiles, at
+// least two) ----
+//
+// One workgroup per CU walks its output tiles; the K tiles of all its tiles
+// form one stream with global numbers g (P slot g % 3, Q slot g % 2), so the
+// loads run ahead across tile boundaries exactly as inside a tile and the two
+// groups keep their phase offset.  After the last K tile of a tile each group
+// spends one phase on its epilogue (group 0's overlaps group 1's last compute
+// phase), clears its accumulators and goes on with the next tile's first K
+// tile: no prologue, no drain.
+
+struct PPTile {
+    int64_t m0, n0, kbeg;
+    int split, nk;
+};
+
+// Output tile i (0, 1, ...) of this workgroup; false past the last one.  With
+// a grid and a tile count that are multiples of 8, XCD x (blockIdx % 8) owns
+// the contiguous tile range [x T/8, (x+1) T/8), swept by its workgroups
+// together (n fastest), so tiles that share operand rows share an L2.
+template <int BK>
+__device__ __forceinline__ bool pp_tile_at(const GemmArgs& a, int64_t i, PPTile* t) {
+    const int64_t tiles_n = (a.N + BN - 1) / BN;
+    const int64_t tiles_m = (a.M + BM - 1) / BM;
+    const int64_t per_split = tiles_m * tiles_n;
+    const int64_t total = per_split * a.splits;
+    const int64_t G = gridDim.x;
+    int64_t idx;
+    if ((G & 7) == 0 && (total & 7) == 0) {
+        const int64_t j = (int64_t)(blockIdx.x >> 3) + i * (G >> 3);
+        if (j >= (total >> 3)) return false;
+        idx = (int64_t)(blockIdx.x & 7) * (total >> 3) + j;
+    } else {
+        idx = (int64_t)blockIdx.x + i * G;
+        if (idx >= total) return false;
+    }
+    t->split = (int)(idx / per_split);
+    const int64_t rem = idx - (int64_t)t->split * per_split;
+    t->m0 = (rem / tiles_n) * BM;
+    t->n0 = (rem % tiles_n) * BN;
+    t->kbeg = (int64_t)t->split * a.k_chunk;
+    t->nk = (int)((min(a.K, t->kbeg + a.k_chunk) - t->kbeg) / BK);
+    return true;
+}
+
+template <int BK, int PL, int QL, int EPI, int TAG>
+__global__ __launch_bounds__(NTHR, 1) void gemm_pp_persist_kernel(GemmArgs a) {
+    using TP = BTile<PL, BK>;
+    using TQ = BTile<QL, BK>;
+    constexpr int NSUB = BK / 16;
+    constexpr int POPS = TP::DPW;
+    constexpr int QOPS = TQ::DPW;
+    __shared__ __attribute__((aligned(1024))) char smem[NP * TP::BYTES + NQ * TQ::BYTES];
+    char* const pring = smem;
+    char* const qring = smem + NP * TP::BYTES;
+
+    const uint16_t* P = reinterpret_cast<const uint16_t*>(a.p);
+    const uint16_t* Q = reinterpret_cast<const uint16_t*>(a.q);
+    const int wave = wave_id();
+    const int lane = threadIdx.x & 63;
+    const int grp = wave >> 2;
+    const int wl = wave & 3;
+
+    // P (Q) part of K tile kt of tile t into the slot of global K tile g;
+    // the per-lane offsets are formed here (they depend on the tile only at
+    // the M / N edges)
+    // Interior tiles: each load's offset is a per-lane part that depends on
+    // the load only through its parity (two registers per wave, computed
+    // once) plus a wave-uniform part in the scalar offset operand, so a load
+    // costs no vector arithmetic.  Edge tiles form the clamped per-lane
+    // offsets at each issue (the lane goes through an empty asm statement so
+    // that they are not hoisted and kept live across the compute phase).
+    uint32_t lpart[2];
+#pragma unroll
+    for (int par = 0; par < 2; ++par)
+        lpart[par] = grp == 0 ? TQ::lane_part(par, a.ldq, lane) : TP::lane_part(par, a.ldp, lane);
+    auto issue_p = [&](const PPTile& t, int kt, int g) {
+        const __amdgpu_buffer_rsrc_t r = rsrc_of(TP::gbase(P, a.ldp, t.m0, t.kbeg + (int64_t)kt * BK));
+        char* slot = pring + (g % NP) * TP::BYTES;
+        if (TP::interior(t.m0, a.M)) {
+#pragma unroll
+            for (int j = 0; j < POPS; ++j)
+                dtl16s(r, lpart[j & 1], TP::uniform_part(POPS * wl + j, a.ldp), slot + 1024 * (POPS * wl + j));
+        } else {
+            int ln = lane;
+            asm volatile("" : "+v"(ln));
+#pragma unroll
+            for (int j = 0; j < POPS; ++j)
+                dtl16(r, TP::voff_l(POPS * wl + j, a.ldp, t.m0, a.M, ln), slot + 1024 * (POPS * wl + j));
+        }
+    };
+    auto issue_q = [&](const PPTile& t, int kt, int g) {
+        const __amdgpu_buffer_rsrc_t r = rsrc_of(TQ::gbase(Q, a.ldq, t.n0, t.kbeg + (int64_t)kt * BK));
+        char* slot = qring + (g % NQ) * TQ::BYTES;
+        if (TQ::interior(t.n0, a.N)) {
+#pragma unroll
+            for (int j = 0; j < QOPS; ++j)
+                dtl16s(r, lpart[j & 1], TQ::uniform_part(QOPS * wl + j, a.ldq), slot + 1024 * (QOPS * wl + j));
+        } else {
+            int ln = lane;
+            asm volatile("" : "+v"(ln));
+#pragma unroll
+            for (int j = 0; j < QOPS; ++j)
+                dtl16(r, TQ::voff_l(QOPS * wl + j, a.ldq, t.n0, a.N, ln), slot + 1024 * (QOPS * wl + j));
+        }
+    };
+
+    constexpr int NLP = PL == KMAJ ? NSUB : TM;
+    constexpr int NLQ = QL == KMAJ ? NSUB : TN;
+    uint32_t lp[NLP], lq[NLQ];
+#pragma unroll
+    for (int u = 0; u < NLP; ++u) lp[u] = TP::lane_off(PL == KMAJ ? u : (grp * WR) / 32 + u, lane);
+#pragma unroll
+    for (int u = 0; u < NLQ; ++u) lq[u] = TQ::lane_off(QL == KMAJ ? u : (wl * WC) / 32 + u, lane);
+    auto frag_p = [&](const char* ps, int i, int s) -> bf16x8 {
+        if constexpr (PL == KMAJ) return TP::frag_at(ps, grp * WR + 32 * i, lp[s]);
+        else return TP::frag_at(ps, s, lp[i]);
+    };
+    auto frag_q = [&](const char* qs, int j, int s) -> bf16x8 {
+        if constexpr (QL == KMAJ) return TQ::frag_at(qs, wl * WC + 32 * j, lq[s]);
+        else return TQ::frag_at(qs, s, lq[j]);
+    };
+
+    f32x16 acc[TM][TN];
+    auto clear = [&]() {
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int j = 0; j < TN; ++j)
+#pragma unroll
+                for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.0f;
+    };
+    bf16x8 fa[NSUB][TM], fb[NSUB][TN];
+    auto read_tile = [&](int g) {
+        const char* ps = pring + (g % NP) * TP::BYTES;
+        const char* qs = qring + (g % NQ) * TQ::BYTES;
+#pragma unroll
+        for (int s = 0; s < NSUB; ++s) {
+#pragma unroll
+            for (int i = 0; i < TM; ++i) fa[s][i] = frag_p(ps, i, s);
+#pragma unroll
+            for (int j = 0; j < TN; ++j) fb[s][j] = frag_q(qs, j, s);
+        }
+    };
+    auto compute_tile = [&]() {
+        __builtin_amdgcn_s_setprio(1);
+#pragma unroll
+        for (int s = 0; s < NSUB; ++s)
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+#pragma unroll
+                for (int j = 0; j < TN; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[s][i], fb[s][j], acc[i][j], 0, 0, 0);
+        __builtin_amdgcn_s_setprio(0);
+    };
+
+    PPTile cur, nxt;
+    if (!pp_tile_at<BK>(a, 0, &cur)) return;
+    bool more = pp_tile_at<BK>(a, 1, &nxt);
+
+    // prologue: P(0), P(1) by group 1, Q(0) by group 0 (every tile has at
+    // least two K tiles)
+    if (grp == 0) {
+        issue_q(cur, 0, 0);
+        wait_vm<0>();
+    } else {
+        issue_p(cur, 0, 0);
+        issue_p(cur, 1, 1);
+        wait_vm<POPS>();
+    }
+    barrier_lds();
+    clear();
+
+    // The phases of both groups, one barrier after each: for every tile, a
+    // memory and a compute phase per K tile, then the epilogue phase; group 1
+    // one phase behind group 0.  Group 0 issues Q(g + 1) in its memory phase
+    // of global K tile g and has it in by the end of its compute phase;
+    // group 1 issues P(g + 2) in its memory phase of g and has P(g + 1) in by
+    // the end of it.  The slots they fill (of g - 1) were read by both groups
+    // before: group 1 read them in its memory phase of g - 1, group 0 one
+    // phase earlier still.
+    if (grp == 1) barrier_lds();
+    int g = 0;
+    for (int64_t it = 0;; ++it) {
+        const int nk = cur.nk;
+        for (int kt = 0; kt < nk; ++kt, ++g) {
+            read_tile(g);
+            if (grp == 0) {
+                if (kt + 1 < nk) issue_q(cur, kt + 1, g + 1);
+                else if (more) issue_q(nxt, 0, g + 1);
+            } else {
+                bool issued = true;
+                if (kt + 2 < nk) issue_p(cur, kt + 2, g + 2);
+                else if (more) issue_p(nxt, kt + 2 - nk, g + 2);
+                else issued = false;
+                if (issued) wait_vm<POPS>();
+                else wait_vm<0>();
+            }
+            barrier_lds();                               // end of the memory phase
+            __builtin_amdgcn_sched_barrier(0);
+            compute_tile();
+            __builtin_amdgcn_sched_barrier(0);
+            if (grp == 0) wait_vm<0>();                  // Q(g + 1) in
+            barrier_lds();                               // end of the compute phase
+        }
+        // the epilogue's coordinates pass through an empty asm statement so
+        // that none of its address arithmetic is hoisted above the K loop
+        // (it would stay live across the loop and spill)
+        // (tile coordinates are wave-uniform and below 2^31: M, N < 2^31)
+        int em0 = __builtin_amdgcn_readfirstlane((int)(cur.m0 + grp * WR));
+        int en0 = __builtin_amdgcn_readfirstlane((int)(cur.n0 + wl * WC));
+        int esplit = __builtin_amdgcn_readfirstlane(cur.split);
+        asm volatile("" : "+s"(em0), "+s"(en0), "+s"(esplit));
+        epilogue_block<EPI>(a, acc, (int64_t)em0, (int64_t)en0, lane, esplit);
+        clear();
+        barrier_lds();                                   // end of the epilogue phase
+        if (!more) break;
+        cur = nxt;
+        more = pp_tile_at<BK>(a, it + 2, &nxt);
+    }
+    if (grp == 0) barrier_lds();
+}
+
 // K tile 64: whole 128-byte lines per load row.
 constexpr int kPPBK = 64;
+// Persistent grid: one workgroup per CU (256 on MI355X), a multiple of 8 when
+// possible so each XCD gets equal work.
+constexpr int64_t kPPGrid = 256;
 
 template <int PL, int QL, int EPI, int TAG>
 hipError_t launch_p(const GemmArgs& a, hipStream_t s) {
@@ -217,6 +443,17 @@ hipError_t launch_p(const GemmArgs& a, hipStream_t s) {
     const int64_t tiles = ((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN) * (int64_t)a.splits;
     if (tiles <= 0) return hipSuccess;
     if (tiles > 0x7fffffffLL) return hipErrorInvalidConfiguration;
+    // persistent when there are more tiles than CUs and every split is a whole
+    // number (at least two) of K tiles
+    const int64_t last = a.K - (int64_t)(a.splits - 1) * a.k_chunk;
+    const bool whole = a.K % kPPBK == 0 && a.k_chunk % kPPBK == 0 && a.k_chunk >= 2 * kPPBK && last >= 2 * kPPBK;
+    if (whole && tiles > kPPGrid) {
+        int64_t grid = kPPGrid;
+        if ((tiles & 7) == 0) grid &= ~int64_t(7);
+        hipLaunchKernelGGL((gemm_pp_persist_kernel<kPPBK, PL, QL, EPI, TAG>), dim3((unsigned)grid), dim3(NTHR), 0,
+                           s, a);
+        return hipGetLastError();
+    }
     hipLaunchKernelGGL((gemm_pp_kernel<kPPBK, PL, QL, EPI, TAG>), dim3((unsigned)tiles), dim3(NTHR), 0, s, a);
     return hipGetLastError();
 }

@@ -37,6 +37,11 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc_of(const char* ubase) {
 __device__ __forceinline__ void dtl16(__amdgpu_buffer_rsrc_t r, uint32_t voff, char* lds) {
     __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lptr_t)lds, 16, voff, 0, 0, 0);
 }
+// The same with a wave-uniform part of the offset in the instruction's scalar
+// offset operand.
+__device__ __forceinline__ void dtl16s(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff, char* lds) {
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lptr_t)lds, 16, voff, soff, 0, 0);
+}
 
 __device__ __forceinline__ uint4 load8_guarded(const uint16_t* p, int valid) {
     uint32_t w[4];
@@ -71,14 +76,32 @@ struct BTile<KMAJ, BK> {
     // instruction), relative to the K tile's first element (row0, k0).  Rows
     // past the edge re-read the last row.
     __device__ static __forceinline__ uint32_t voff(int blk, int64_t ld, int64_t row0, int64_t rows) {
-        const int lane = threadIdx.x & 63;
+        return voff_l(blk, ld, row0, rows, threadIdx.x & 63);
+    }
+    // the same for an explicit lane (32-bit arithmetic: the tile's rows
+    // past the edge are clamped to rows - 1 - row0, which fits an int)
+    __device__ static __forceinline__ uint32_t voff_l(int blk, int64_t ld, int64_t row0, int64_t rows, int lane) {
         const int row = RPI * blk + lane / CR;
         const int lc = (lane % CR) ^ swz(row);
-        const int64_t lrow = row0 + row < rows ? row : rows - 1 - row0;
+        const int64_t lim64 = rows - 1 - row0;
+        const int lim = lim64 < 255 ? (int)lim64 : 255;
+        const int lrow = row < lim ? row : lim;
         return 2u * ((uint32_t)lrow * (uint32_t)ld + 8u * (uint32_t)lc);
     }
     __device__ static __forceinline__ const char* gbase(const uint16_t* base, int64_t ld, int64_t row0, int64_t k0) {
         return reinterpret_cast<const char*>(base + row0 * ld + k0);
+    }
+
+    // voff of an interior tile (every row in range) split in two: a per-lane
+    // part that depends on the block only through its parity (the swizzle
+    // term repeats every two blocks) and a wave-uniform part.
+    __device__ static __forceinline__ bool interior(int64_t row0, int64_t rows) { return row0 + 256 <= rows; }
+    __device__ static __forceinline__ uint32_t lane_part(int par, int64_t ld, int lane) {
+        const int row = RPI * par + lane / CR;
+        return 2u * ((uint32_t)(lane / CR) * (uint32_t)ld + 8u * (uint32_t)((lane % CR) ^ swz(row)));
+    }
+    __device__ static __forceinline__ uint32_t uniform_part(int blk, int64_t ld) {
+        return 2u * (uint32_t)(RPI * blk) * (uint32_t)ld;
     }
 
     // Guarded register path (partial K tile), NTHR threads: zeros past kend.
@@ -127,15 +150,32 @@ struct BTile<MNMAJ, BK> {
     // 1 KB block blk fills k rows 2 blk, 2 blk + 1; chunks that start past
     // the last column re-read the last chunk.
     __device__ static __forceinline__ uint32_t voff(int blk, int64_t ld, int64_t m0, int64_t rows) {
-        const int lane = threadIdx.x & 63;
-        const int64_t mlast = ((rows - 1) >> 3) << 3;
+        return voff_l(blk, ld, m0, rows, threadIdx.x & 63);
+    }
+    __device__ static __forceinline__ uint32_t voff_l(int blk, int64_t ld, int64_t m0, int64_t rows, int lane) {
+        const int64_t lim64 = (((rows - 1) >> 3) << 3) - m0;       // last chunk, relative to m0
+        const int lim = lim64 < 255 * 8 ? (int)lim64 : 255 * 8;
         const int k = 2 * blk + (lane >> 5);
         const int lc = (lane & 31) ^ ((k & 3) << 2);
-        const int64_t lm = m0 + 8 * lc <= mlast ? 8 * lc : mlast - m0;
+        const int lm = 8 * lc <= lim ? 8 * lc : lim;
         return 2u * ((uint32_t)k * (uint32_t)ld + (uint32_t)lm);
     }
     __device__ static __forceinline__ const char* gbase(const uint16_t* base, int64_t ld, int64_t m0, int64_t k0) {
         return reinterpret_cast<const char*>(base + k0 * ld + m0);
+    }
+
+    // voff of an interior tile (all 256 columns in range, no chunk clamped)
+    // split in two: per lane (through the parity of the block, which fixes
+    // k & 3 of the lane's row) and wave-uniform.
+    __device__ static __forceinline__ bool interior(int64_t m0, int64_t rows) {
+        return m0 + 248 <= (((rows - 1) >> 3) << 3);
+    }
+    __device__ static __forceinline__ uint32_t lane_part(int par, int64_t ld, int lane) {
+        const int k = 2 * par + (lane >> 5);
+        return 2u * ((uint32_t)(lane >> 5) * (uint32_t)ld + 8u * (uint32_t)((lane & 31) ^ ((k & 3) << 2)));
+    }
+    __device__ static __forceinline__ uint32_t uniform_part(int blk, int64_t ld) {
+        return 2u * (uint32_t)(2 * blk) * (uint32_t)ld;
     }
 
     template <int NTHR>
