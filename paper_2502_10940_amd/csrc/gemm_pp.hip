@@ -9,7 +9,8 @@
 //    waves on a SIMD belong to different groups.
 //  * Each group alternates a memory phase (read the whole K tile's fragments
 //    from LDS into registers, issue its share of the direct-to-LDS loads)
-//    and a compute phase (the K tile's 32 MFMAs, at raised wave priority).
+//    and a compute phase (the K tile's 32 MFMAs, at raised wave priority
+//    when the Q operand fits in L2).
 //    Group 1 runs one phase behind group 0, and all eight waves meet at a
 //    barrier between phases, so on every SIMD one wave issues MFMAs while
 //    the other reads and loads: the matrix pipe never waits for LDS reads,
@@ -136,8 +137,13 @@ __global__ __launch_bounds__(NTHR, 1) void gemm_pp_kernel(GemmArgs a) {
             for (int j = 0; j < TN; ++j) fb[s][j] = frag_q(qs, j, s);
         }
     };
+    // Raised wave priority for the compute phase when the Q operand fits
+    // comfortably in an XCD's L2 (measured on MI355X: it helps there, and
+    // slows products whose Q operand misses in L2, whose memory phases need
+    // the issue slots).
+    const bool prio = (int64_t)a.N * a.K * 2 <= (int64_t)(3 << 20);
     auto compute_tile = [&]() {
-        __builtin_amdgcn_s_setprio(1);
+        if (prio) __builtin_amdgcn_s_setprio(1);
 #pragma unroll
         for (int s = 0; s < NSUB; ++s)
 #pragma unroll
@@ -145,7 +151,7 @@ __global__ __launch_bounds__(NTHR, 1) void gemm_pp_kernel(GemmArgs a) {
 #pragma unroll
                 for (int j = 0; j < TN; ++j)
                     acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[s][i], fb[s][j], acc[i][j], 0, 0, 0);
-        __builtin_amdgcn_s_setprio(0);
+        if (prio) __builtin_amdgcn_s_setprio(0);
     };
 
     // prologue: P(0), P(1) by group 1, Q(0) by group 0; K tile 0 complete
@@ -227,7 +233,12 @@ struct PPTile {
 // Output tile i (0, 1, ...) of this workgroup; false past the last one.  With
 // a grid and a tile count that are multiples of 8, XCD x (blockIdx % 8) owns
 // the contiguous tile range [x T/8, (x+1) T/8), swept by its workgroups
-// together (n fastest), so tiles that share operand rows share an L2.
+// together, so tiles that share operand rows share an L2.  When that range
+// is whole rows of tiles (one split), it is swept in column bands of
+// kBand tiles (n fastest within a band, then the next row): the Q rows of a
+// band (kBand x 256 rows, 2 MB for K = 512) stay in the XCD's 4 MB L2 while
+// the band's rows stream, instead of every row of tiles pulling all of Q.
+constexpr int64_t kBand = 8;
 template <int BK>
 __device__ __forceinline__ bool pp_tile_at(const GemmArgs& a, int64_t i, PPTile* t) {
     const int64_t tiles_n = (a.N + BN - 1) / BN;
@@ -237,9 +248,21 @@ __device__ __forceinline__ bool pp_tile_at(const GemmArgs& a, int64_t i, PPTile*
     const int64_t G = gridDim.x;
     int64_t idx;
     if ((G & 7) == 0 && (total & 7) == 0) {
+        const int64_t per_xcd = total >> 3;
         const int64_t j = (int64_t)(blockIdx.x >> 3) + i * (G >> 3);
-        if (j >= (total >> 3)) return false;
-        idx = (int64_t)(blockIdx.x & 7) * (total >> 3) + j;
+        if (j >= per_xcd) return false;
+        const int64_t x = blockIdx.x & 7;
+        if (a.splits == 1 && per_xcd % tiles_n == 0 && tiles_n > kBand) {
+            const int64_t rows = per_xcd / tiles_n;               // rows of tiles this XCD owns
+            const int64_t nbands = (tiles_n + kBand - 1) / kBand;
+            int64_t band = j / (rows * kBand);
+            if (band > nbands - 1) band = nbands - 1;
+            const int64_t off = j - band * rows * kBand;
+            const int64_t w = min(kBand, tiles_n - band * kBand);  // width of this band
+            idx = (x * rows + off / w) * tiles_n + band * kBand + off % w;
+        } else {
+            idx = x * per_xcd + j;
+        }
     } else {
         idx = (int64_t)blockIdx.x + i * G;
         if (idx >= total) return false;
@@ -352,8 +375,13 @@ __global__ __launch_bounds__(NTHR, 1) void gemm_pp_persist_kernel(GemmArgs a) {
             for (int j = 0; j < TN; ++j) fb[s][j] = frag_q(qs, j, s);
         }
     };
+    // Raised wave priority for the compute phase when the Q operand fits
+    // comfortably in an XCD's L2 (measured on MI355X: it helps there, and
+    // slows products whose Q operand misses in L2, whose memory phases need
+    // the issue slots).
+    const bool prio = (int64_t)a.N * a.K * 2 <= (int64_t)(3 << 20);
     auto compute_tile = [&]() {
-        __builtin_amdgcn_s_setprio(1);
+        if (prio) __builtin_amdgcn_s_setprio(1);
 #pragma unroll
         for (int s = 0; s < NSUB; ++s)
 #pragma unroll
@@ -361,7 +389,7 @@ __global__ __launch_bounds__(NTHR, 1) void gemm_pp_persist_kernel(GemmArgs a) {
 #pragma unroll
                 for (int j = 0; j < TN; ++j)
                     acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[s][i], fb[s][j], acc[i][j], 0, 0, 0);
-        __builtin_amdgcn_s_setprio(0);
+        if (prio) __builtin_amdgcn_s_setprio(0);
     };
 
     PPTile cur, nxt;
