@@ -223,7 +223,8 @@ __global__ __launch_bounds__(NTHR, 1) void gemm_pp_kernel(GemmArgs a) {
 // groups keep their phase offset.  After the last K tile of a tile each group
 // spends one phase on its epilogue (group 0's overlaps group 1's last compute
 // phase), clears its accumulators and goes on with the next tile's first K
-// tile: no prologue, no drain.
+// tile: no prologue, no drain.  (The first k step of each tile's first K
+// tile starts from zero accumulators, so nothing is cleared in between.)
 
 struct PPTile {
     int64_t m0, n0, kbeg;
@@ -355,14 +356,6 @@ __global__ __launch_bounds__(NTHR, 1) void gemm_pp_persist_kernel(GemmArgs a) {
     };
 
     f32x16 acc[TM][TN];
-    auto clear = [&]() {
-#pragma unroll
-        for (int i = 0; i < TM; ++i)
-#pragma unroll
-            for (int j = 0; j < TN; ++j)
-#pragma unroll
-                for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.0f;
-    };
     bf16x8 fa[NSUB][TM], fb[NSUB][TN];
     auto read_tile = [&](int g) {
         const char* ps = pring + (g % NP) * TP::BYTES;
@@ -380,15 +373,25 @@ __global__ __launch_bounds__(NTHR, 1) void gemm_pp_persist_kernel(GemmArgs a) {
     // slows products whose Q operand misses in L2, whose memory phases need
     // the issue slots).
     const bool prio = (int64_t)a.N * a.K * 2 <= (int64_t)(3 << 20);
-    auto compute_tile = [&]() {
+    // FIRST: the first K tile of an output tile, whose first k step starts
+    // from zero accumulators (no separate clearing after the epilogue)
+    auto compute_tile = [&](auto first) {
         if (prio) __builtin_amdgcn_s_setprio(1);
 #pragma unroll
         for (int s = 0; s < NSUB; ++s)
 #pragma unroll
             for (int i = 0; i < TM; ++i)
 #pragma unroll
-                for (int j = 0; j < TN; ++j)
+                for (int j = 0; j < TN; ++j) {
+                    if constexpr (decltype(first)::value) {
+                        if (s == 0) {
+                            const f32x16 zero = {};
+                            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[s][i], fb[s][j], zero, 0, 0, 0);
+                            continue;
+                        }
+                    }
                     acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[s][i], fb[s][j], acc[i][j], 0, 0, 0);
+                }
         if (prio) __builtin_amdgcn_s_setprio(0);
     };
 
@@ -407,7 +410,6 @@ __global__ __launch_bounds__(NTHR, 1) void gemm_pp_persist_kernel(GemmArgs a) {
         wait_vm<POPS>();
     }
     barrier_lds();
-    clear();
 
     // The phases of both groups, one barrier after each: for every tile, a
     // memory and a compute phase per K tile, then the epilogue phase; group 1
@@ -436,7 +438,8 @@ __global__ __launch_bounds__(NTHR, 1) void gemm_pp_persist_kernel(GemmArgs a) {
             }
             barrier_lds();                               // end of the memory phase
             __builtin_amdgcn_sched_barrier(0);
-            compute_tile();
+            if (kt == 0) compute_tile(ic<bool, true>{});
+            else compute_tile(ic<bool, false>{});
             __builtin_amdgcn_sched_barrier(0);
             if (grp == 0) wait_vm<0>();                  // Q(g + 1) in
             barrier_lds();                               // end of the compute phase
@@ -450,7 +453,6 @@ __global__ __launch_bounds__(NTHR, 1) void gemm_pp_persist_kernel(GemmArgs a) {
         int esplit = __builtin_amdgcn_readfirstlane(cur.split);
         asm volatile("" : "+s"(em0), "+s"(en0), "+s"(esplit));
         epilogue_block<EPI>(a, acc, (int64_t)em0, (int64_t)en0, lane, esplit);
-        clear();
         barrier_lds();                                   // end of the epilogue phase
         if (!more) break;
         cur = nxt;

@@ -40,6 +40,11 @@ CASES = [
     ("odd_rank_weight_repack_bf16", 200, 136, 144, 37, "bf16", "silu"),
     ("gelu_bf16", 600, 520, 264, 136, "bf16", "gelu"),
     ("gelu_f32", 256, 512, 512, 128, "f32", "gelu"),
+    # more output tiles than CUs with whole K tiles: the persistent 256 x 256
+    # kernel, ragged in M and N, its tiles swept in column bands of 8 + 4
+    # (24 x 12 tiles of Y = H B^T here, of dX = dZ A in the next case)
+    ("persistent_banded_wide_out_bf16", 6044, 300, 3000, 128, "bf16", "silu"),
+    ("persistent_banded_wide_in_bf16", 6044, 3000, 300, 128, "bf16", "silu"),
 ]
 
 
