@@ -44,6 +44,8 @@ def parse():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", type=int, default=4, help="1..5 (default 4: LLaMA-1B-shaped block)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--streams", type=int, default=2,
+                    help="HIP streams the independent projections are spread over (CoLA, CoLA-M steps)")
     ap.add_argument("--no-dense", action="store_true")
     ap.add_argument("--no-cola-m", action="store_true")
     ap.add_argument("--cpu-tokens", type=int, default=8192,
@@ -393,19 +395,45 @@ def main():
                  by["down"]]
     ws_need = max([p.ws_need for p in projs] + [u.ws_need for u in units if isinstance(u, Group)])
     ws = torch.empty(ws_need, dtype=torch.uint8, device="cuda:0")
+    # independent projections spread over several HIP streams (default
+    # priority), each with its own workspace: projection i runs its forward
+    # and backward on stream i % S, so one kernel's ramp-up overlaps another
+    # stream's drain.  The step still starts and ends on the current stream.
+    nstreams = max(1, args.streams)
+    streams = [None] + [torch.cuda.Stream() for _ in range(nstreams - 1)]
+    wss = [ws] + [torch.empty(ws_need, dtype=torch.uint8, device="cuda:0") for _ in range(nstreams - 1)]
     setup_s = time.time() - t0
 
-    def step_cola():
+    def spread(fwd, bwd):
+        if nstreams == 1:
+            for p in projs:
+                fwd(p, ws)
+            for p in reversed(projs):
+                bwd(p, ws)
+            return
+        main = torch.cuda.current_stream()
+        for st in streams[1:]:
+            st.wait_stream(main)
+        order = list(enumerate(projs))
+        for phase, seq in ((fwd, order), (bwd, order[::-1])):
+            for i, p in seq:
+                k = i % nstreams
+                with torch.cuda.stream(streams[k] if k else main):
+                    phase(p, wss[k])
+        for st in streams[1:]:
+            main.wait_stream(st)
+
+    def step_cola_1s():
         for p in projs:
             p.fwd(ws)
         for p in reversed(projs):
             p.bwd(ws)
 
+    def step_cola():
+        spread(lambda p, w: p.fwd(w), lambda p, w: p.bwd(w))
+
     def step_cola_m():
-        for p in projs:
-            p.fwd(ws, True)
-        for p in reversed(projs):
-            p.bwd(ws, True)
+        spread(lambda p, w: p.fwd(w, True), lambda p, w: p.bwd(w, True))
 
     def step_fused():
         for u in units:
@@ -439,7 +467,7 @@ def main():
         # the launch stream): per-kernel durations for the roofline and the table
         cola.timing_reset()
         cola.timing_enable(True)
-        res["cola_events"] = timed_steps(step_cola, args.steps, 0)
+        res["cola_events"] = timed_steps(step_cola_1s, args.steps, 0)
         cola.timing_enable(False)
         kernels = kernel_table(cola)
     # the headline mode: total time of exactly K steps / K; the others: median step
@@ -475,13 +503,15 @@ def main():
         "data": "synthetic",
         "config": {"workload": w["name"], "tokens": T, "d": w["d"], "ffn": w["ffn"], "rank": r,
                    "projections": [p.name for p in projs], "act": "silu", "mode": main_mode,
-                   "step": "fwd of all projections, then bwd in reverse order"},
+                   "step": "fwd of all projections, then bwd in reverse order",
+                   "streams": nstreams},
         "pct_of_bf16_mfma_peak": round(100.0 * value / peak, 2),
         "tokens_per_s": round(T / (ms / 1e3), 1),
     }
     if "cola_events" in res:
         out["cola_with_kernel_events"] = {"ms_per_step": round(res["cola_events"], 4),
-                                          "tflops": round(flops_cola / (res["cola_events"] * 1e9), 2)}
+                                          "tflops": round(flops_cola / (res["cola_events"] * 1e9), 2),
+                                          "streams": 1}
     if "cola_m" in res:
         out["cola_m"] = {"ms_per_step": round(res["cola_m"], 4),
                          "tflops": round(flops_cola / (res["cola_m"] * 1e9), 2),

@@ -377,4 +377,256 @@ __device__ __forceinline__ void epilogue_block(const GemmArgs& a, const f32x16 (
     }
 }
 
+// ---------------------------------------------------------------------------
+// Transposed accumulators.  A kernel that gives the MFMA the Q fragment as its
+// first operand holds the tiles of C^T: lane l, register v of tile (i, j) is
+// element (32 i + l % 32, 32 j + 8 (v / 4) + 4 (l / 32) + v % 4) of the
+// wave's block, so every group of four registers is four consecutive columns
+// of one row.  Two lane exchanges (no transposes) make the stores wide:
+//  1. v_permlane32_swap (lanes 32-63 of one register with lanes 0-31 of
+//     another) on the register groups 2p and 2p + 1 leaves lane l with the
+//     eight columns 16 p + 8 (l / 32) + 0..7 of row l % 32;
+//  2. v_permlane16_swap (lanes 16-31 / 48-63 of one register with lanes
+//     0-15 / 32-47 of another) on the pieces p = 0 and p = 1 leaves lane l
+//     with columns 16 ((l / 16) % 2) + 8 (l / 32) + 0..7 of row l % 16 (piece
+//     X) and of row 16 + l % 16 (piece Y).
+// One 16-byte store (bf16) per piece then writes 16 rows x 64 contiguous
+// bytes, which sustains the full store rate of a CU (as 8 rows x 128 bytes
+// does; 32 rows x 32 bytes is slower).  fp32 outputs take a third exchange
+// and two stores per piece, again 16 rows x 64 contiguous bytes each.  Same roundings and sigma as the epilogues above, so the values are
+// bitwise those of the other families.
+
+// x (lanes 32-63) <-> y (lanes 0-31)
+__device__ __forceinline__ void swap_halves(uint32_t& x, uint32_t& y) {
+    const auto r = __builtin_amdgcn_permlane32_swap(x, y, false, false);
+    x = r[0];
+    y = r[1];
+}
+// x (lanes 16-31, 48-63) <-> y (lanes 0-15, 32-47)
+__device__ __forceinline__ void swap_rows16(uint32_t& x, uint32_t& y) {
+    const auto r = __builtin_amdgcn_permlane16_swap(x, y, false, false);
+    x = r[0];
+    y = r[1];
+}
+
+// Eight bf16 (packed pairs w[0..3], lower column in the low half) to row gm,
+// columns gn .. gn+7 of a bf16 matrix; FAST: in bounds and 16-byte aligned.
+template <bool FAST>
+__device__ __forceinline__ void store_bf16x8(uint16_t* base, int64_t ld, int64_t M, int64_t N, int64_t gm,
+                                             int64_t gn, const uint32_t w[4]) {
+    uint16_t* p = base + gm * ld + gn;
+    if constexpr (FAST) {
+        *reinterpret_cast<u32x4_t*>(p) = u32x4_t{w[0], w[1], w[2], w[3]};
+    } else {
+        if (gm >= M) return;
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+            if (gn + e < N) p[e] = (uint16_t)((w[e >> 1] >> (16 * (e & 1))) & 0xffffu);
+    }
+}
+
+// Four fp32 (bit patterns) to row gm, columns gn .. gn+3; FAST as above.
+template <bool FAST>
+__device__ __forceinline__ void store_f32x4(float* base, int64_t ld, int64_t M, int64_t N, int64_t gm, int64_t gn,
+                                            const uint32_t* w) {
+    float* p = base + gm * ld + gn;
+    if constexpr (FAST) {
+        *reinterpret_cast<u32x4_t*>(p) = u32x4_t{w[0], w[1], w[2], w[3]};
+    } else {
+        if (gm >= M) return;
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+            if (gn + e < N) p[e] = __uint_as_float(w[e]);
+    }
+}
+
+// Eight bf16 of row gm, columns gn .. gn+7 (packed pairs); past the edges 0.
+template <bool FAST>
+__device__ __forceinline__ u32x4_t load_bf16x8(const uint16_t* base, int64_t ld, int64_t M, int64_t N, int64_t gm,
+                                               int64_t gn) {
+    const uint16_t* p = base + gm * ld + gn;
+    if constexpr (FAST) {
+        return *reinterpret_cast<const u32x4_t*>(p);
+    } else {
+        uint32_t e[8];
+#pragma unroll
+        for (int k = 0; k < 8; ++k) e[k] = (gm < M && gn + k < N) ? (uint32_t)p[k] : 0u;
+        return u32x4_t{e[0] | (e[1] << 16), e[2] | (e[3] << 16), e[4] | (e[5] << 16), e[6] | (e[7] << 16)};
+    }
+}
+
+template <int EPI, int ACT, bool FAST, int TM, int TN>
+__device__ __forceinline__ void epilogue_t_impl(const GemmArgs& a, const f32x16 (&acc)[TM][TN], int64_t row0,
+                                                int64_t col0, int lane, int split) {
+    // after exchange 1: row l % 32, columns 16 p + h1 ..
+    const int r1 = lane & 31;
+    const int h1 = 8 * (lane >> 5);
+    // after exchange 2: rows l % 16 (X) and 16 + l % 16 (Y), columns c2 ..
+    const int r2 = lane & 15;
+    const int c2 = 16 * ((lane >> 4) & 1) + 8 * (lane >> 5);
+    uint16_t* C = reinterpret_cast<uint16_t*>(a.c);
+    uint16_t* Hp = reinterpret_cast<uint16_t*>(a.aux);
+    const uint16_t* Zp = reinterpret_cast<const uint16_t*>(a.zin);
+    // EPI_DZ: Z (in the layout after exchange 1) of tile row i + 1 is loaded
+    // before the stores of tile row i (a wave's vector-memory operations
+    // complete in order, so a load issued after a store would also wait for
+    // that store)
+    u32x4_t zb[2][TN][2];
+    auto zload = [&](int i, u32x4_t (&z)[TN][2]) {
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+            for (int p = 0; p < 2; ++p)
+                z[j][p] = load_bf16x8<FAST>(Zp, a.ldzin, a.M, a.N, row0 + 32 * i + r1, col0 + 32 * j + 16 * p + h1);
+    };
+    if constexpr (EPI == EPI_DZ) zload(0, zb[0]);
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
+        if constexpr (EPI == EPI_DZ) {
+            if (i + 1 < TM) zload(i + 1, zb[(i + 1) & 1]);
+        }
+        const int64_t gx = row0 + 32 * i + r2;     // row of piece X (Y: gx + 16)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+            const f32x16& v = acc[i][j];
+            const int64_t gn = col0 + 32 * j + c2;
+            if constexpr (EPI == EPI_STORE_F32) {
+                uint32_t w[2][8];
+#pragma unroll
+                for (int p = 0; p < 2; ++p)
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        w[p][e] = __float_as_uint(v[8 * p + e]);
+                        w[p][4 + e] = __float_as_uint(v[8 * p + 4 + e]);
+                        swap_halves(w[p][e], w[p][4 + e]);
+                    }
+#pragma unroll
+                for (int e = 0; e < 8; ++e) swap_rows16(w[0][e], w[1][e]);
+                // exchange 3 (fp32 only): within each piece, lanes l and l + 16
+                // trade columns 4..7 and 16..19 of their eight, so that lane l
+                // holds columns 4 (l / 16) + 0..3 and 16 + 4 (l / 16) + 0..3:
+                // each 16-byte store then writes 16 rows x 64 contiguous bytes
+#pragma unroll
+                for (int p = 0; p < 2; ++p)
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) swap_rows16(w[p][e], w[p][4 + e]);
+                float* c = reinterpret_cast<float*>(a.c) + (int64_t)split * a.split_stride;
+                const int64_t gf = col0 + 32 * j + 4 * (lane >> 4);
+#pragma unroll
+                for (int p = 0; p < 2; ++p) {
+                    store_f32x4<FAST>(c, a.ldc, a.M, a.N, gx + 16 * p, gf, &w[p][0]);
+                    store_f32x4<FAST>(c, a.ldc, a.M, a.N, gx + 16 * p, gf + 16, &w[p][4]);
+                }
+            } else {
+                uint32_t o[2][4], h[2][4];
+#pragma unroll
+                for (int p = 0; p < 2; ++p) {
+                    if constexpr (EPI == EPI_DZ) {
+                        // exchange 1 on the fp32 values, then sigma' of the
+                        // matching Z
+                        uint32_t w[8];
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) {
+                            w[e] = __float_as_uint(v[8 * p + e]);
+                            w[4 + e] = __float_as_uint(v[8 * p + 4 + e]);
+                            swap_halves(w[e], w[4 + e]);
+                        }
+                        const u32x4_t z = zb[i & 1][j][p];
+#pragma unroll
+                        for (int q = 0; q < 4; ++q) {
+                            float ov[2], hv[2];
+#pragma unroll
+                            for (int e = 0; e < 2; ++e) {
+                                const float ze = bf16_to_f32(e == 0 ? (z[q] & 0xffffu) : (z[q] >> 16));
+                                float sp;
+                                act_sigma_both_c<ACT, true>(ze, hv[e], sp);
+                                const float x = __uint_as_float(w[2 * q + e]);
+                                ov[e] = ACT == 0 ? x : x * sp;
+                            }
+                            o[p][q] = pack_bf16x2(ov[0], ov[1]);
+                            h[p][q] = pack_bf16x2(hv[0], hv[1]);
+                        }
+                    } else {
+                        // elementwise: round and pack first, then exchange 1
+                        // on the packed pairs (half the exchanges)
+#pragma unroll
+                        for (int q = 0; q < 4; ++q) {
+                            const int r = 8 * p + 2 * q;        // registers r, r + 1
+                            const uint32_t zz = pack_bf16x2(v[r], v[r + 1]);
+                            if constexpr (EPI == EPI_STORE) {
+                                o[p][q] = zz;
+                            } else {
+                                // sigma of the rounded values
+                                const float z0 = __uint_as_float(zz << 16);
+                                const float z1 = __uint_as_float(zz & 0xffff0000u);
+                                const uint32_t hh =
+                                    pack_bf16x2(act_sigma_c<ACT, true>(z0), act_sigma_c<ACT, true>(z1));
+                                if constexpr (EPI == EPI_H) {
+                                    o[p][q] = hh;
+                                } else {
+                                    o[p][q] = zz;
+                                    h[p][q] = hh;
+                                }
+                            }
+                        }
+                        swap_halves(o[p][0], o[p][2]);
+                        swap_halves(o[p][1], o[p][3]);
+                        if constexpr (EPI == EPI_Z_H) {
+                            swap_halves(h[p][0], h[p][2]);
+                            swap_halves(h[p][1], h[p][3]);
+                        }
+                    }
+                }
+                // exchange 2, then one store per piece
+#pragma unroll
+                for (int q = 0; q < 4; ++q) swap_rows16(o[0][q], o[1][q]);
+                store_bf16x8<FAST>(C, a.ldc, a.M, a.N, gx, gn, o[0]);
+                store_bf16x8<FAST>(C, a.ldc, a.M, a.N, gx + 16, gn, o[1]);
+                if constexpr (EPI == EPI_Z_H || EPI == EPI_DZ) {
+                    if (Hp) {
+#pragma unroll
+                        for (int q = 0; q < 4; ++q) swap_rows16(h[0][q], h[1][q]);
+                        store_bf16x8<FAST>(Hp, a.ldaux, a.M, a.N, gx, gn, h[0]);
+                        store_bf16x8<FAST>(Hp, a.ldaux, a.M, a.N, gx + 16, gn, h[1]);
+                    }
+                }
+            }
+        }
+    }
+}
+
+// The epilogue of a wave's block of transposed accumulators (rows row0 ..,
+// columns col0 ..).  Blocks wholly inside the output with 16-byte aligned
+// rows take the unguarded vector path.
+template <int EPI, int ACT, int TM, int TN>
+__device__ __forceinline__ void epilogue_t_act(const GemmArgs& a, const f32x16 (&acc)[TM][TN], int64_t row0,
+                                               int64_t col0, int lane, int split) {
+    auto al = [](const void* p, int64_t ld, int64_t elems) {   // rows of elems-element vectors
+        return p != nullptr && (reinterpret_cast<uintptr_t>(p) % (2 * elems)) == 0 && ld % elems == 0;
+    };
+    bool fast = row0 + 32 * TM <= a.M && col0 + 32 * TN <= a.N;
+    if constexpr (EPI == EPI_STORE_F32) {
+        const float* c = reinterpret_cast<const float*>(a.c) + (int64_t)split * a.split_stride;
+        fast = fast && (reinterpret_cast<uintptr_t>(c) & 15u) == 0 && a.ldc % 4 == 0;
+    } else {
+        fast = fast && al(a.c, a.ldc, 8);
+    }
+    if constexpr (EPI == EPI_Z_H || EPI == EPI_DZ) fast = fast && (a.aux == nullptr || al(a.aux, a.ldaux, 8));
+    if constexpr (EPI == EPI_DZ) fast = fast && al(a.zin, a.ldzin, 8);
+    if (fast) epilogue_t_impl<EPI, ACT, true>(a, acc, row0, col0, lane, split);
+    else epilogue_t_impl<EPI, ACT, false>(a, acc, row0, col0, lane, split);
+}
+
+template <int EPI, int TM, int TN>
+__device__ __forceinline__ void epilogue_block_t(const GemmArgs& a, const f32x16 (&acc)[TM][TN], int64_t row0,
+                                                 int64_t col0, int lane, int split) {
+    if constexpr (EPI == EPI_STORE || EPI == EPI_STORE_F32) {
+        epilogue_t_act<EPI, 0>(a, acc, row0, col0, lane, split);
+    } else {
+        if (a.act == 0) epilogue_t_act<EPI, 0>(a, acc, row0, col0, lane, split);
+        else if (a.act == 2) epilogue_t_act<EPI, 2>(a, acc, row0, col0, lane, split);
+        else epilogue_t_act<EPI, 1>(a, acc, row0, col0, lane, split);
+    }
+}
+
 }  // namespace cola

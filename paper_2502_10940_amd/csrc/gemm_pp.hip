@@ -6,7 +6,10 @@
 //  * Group 0 (waves 0-3) owns rows 0-127 of the 256 x 256 tile, group 1
 //    (waves 4-7) rows 128-255; each wave a 128 x 64 block as 4 x 2 tiles of
 //    v_mfma_f32_32x32x16_bf16 (128 fp32 accumulators per lane).  The two
-//    waves on a SIMD belong to different groups.
+//    waves on a SIMD belong to different groups.  The Q fragment is the
+//    MFMA's first operand, so the accumulators hold C^T tiles: four
+//    consecutive columns of one row per register group, stored by the
+//    transposed epilogue of epilogue.hpp without any transposes.
 //  * Each group alternates a memory phase (read the whole K tile's fragments
 //    from LDS into registers, issue its share of the direct-to-LDS loads)
 //    and a compute phase (the K tile's 32 MFMAs, at raised wave priority
@@ -42,6 +45,9 @@ constexpr int TM = WR / 32;
 constexpr int TN = WC / 32;
 constexpr int NP = 3;            // P slots (two K tiles ahead)
 constexpr int NQ = 2;            // Q slots (one K tile ahead)
+// K tile of the persistent kernel and the launcher: 64, whole 128-byte lines
+// per load row.
+constexpr int kPPBK = 64;
 
 template <int BK, int PL, int QL, int EPI, int TAG>
 __global__ __launch_bounds__(NTHR, 1) void gemm_pp_kernel(GemmArgs a) {
@@ -150,7 +156,7 @@ __global__ __launch_bounds__(NTHR, 1) void gemm_pp_kernel(GemmArgs a) {
             for (int i = 0; i < TM; ++i)
 #pragma unroll
                 for (int j = 0; j < TN; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[s][i], fb[s][j], acc[i][j], 0, 0, 0);
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[s][j], fa[s][i], acc[i][j], 0, 0, 0);
         if (prio) __builtin_amdgcn_s_setprio(0);
     };
 
@@ -211,7 +217,7 @@ __global__ __launch_bounds__(NTHR, 1) void gemm_pp_kernel(GemmArgs a) {
         read_tile(pring, qring);
         compute_tile();
     }
-    epilogue_block<EPI>(a, acc, m0 + grp * WR, n0 + wl * WC, lane, split);
+    epilogue_block_t<EPI>(a, acc, m0 + grp * WR, n0 + wl * WC, lane, split);
 }
 
 // ---- persistent variant (every K range a whole number of K tiles, at
@@ -240,12 +246,47 @@ struct PPTile {
 // band (kBand x 256 rows, 2 MB for K = 512) stay in the XCD's 4 MB L2 while
 // the band's rows stream, instead of every row of tiles pulling all of Q.
 constexpr int64_t kBand = 8;
-template <int BK>
+
+// n / d for n, d < 2^21: one multiply by the hardware reciprocal (1 ulp) and
+// a correction of at most one either way.  The product is within 1/2 of
+// n / d (relative error below 1.5 * 2^-23, n / d < 2^21), so its truncation
+// is off by at most one.
+__device__ __forceinline__ int64_t fdiv21(int64_t n, int64_t d) {
+    const uint32_t un = (uint32_t)n, ud = (uint32_t)d;
+    uint32_t q = (uint32_t)((float)un * __builtin_amdgcn_rcpf((float)ud));
+    const int32_t r = (int32_t)(un - q * ud);
+    if (r < 0) --q;
+    else if ((uint32_t)r >= ud) ++q;
+    // the operands are wave-uniform: keep the quotient (and the tile
+    // coordinates made from it) in scalar registers
+    return (int64_t)(uint32_t)__builtin_amdgcn_readfirstlane((int)q);
+}
+
+// Output tile i (0, 1, ...) of this workgroup; false past the last one.  With
+// a grid and a tile count that are multiples of 8, XCD x (blockIdx % 8) owns
+// the contiguous tile range [x T/8, (x+1) T/8), swept by its workgroups
+// together, so tiles that share operand rows share an L2.  When that range
+// is whole rows of tiles (one split), it is swept in column bands of
+// kBand tiles (n fastest within a band, then the next row): the Q rows of a
+// band (kBand x 256 rows, 2 MB for K = 512) stay in the XCD's 4 MB L2 while
+// the band's rows stream, instead of every row of tiles pulling all of Q.
+// Every dividend and divisor here is at most the tile count; below 2^21
+// tiles (any realistic launch) the divisions take the short path, so the
+// walk costs a few dozen instructions per tile instead of several
+// thousand cycles of 64-bit division.
 __device__ __forceinline__ bool pp_tile_at(const GemmArgs& a, int64_t i, PPTile* t) {
-    const int64_t tiles_n = (a.N + BN - 1) / BN;
-    const int64_t tiles_m = (a.M + BM - 1) / BM;
+    // the launch constants pass through an empty asm statement so that the
+    // walk is recomputed at each call rather than hoisted out of the tile
+    // loop (its loop-invariant part would stay live in registers and spill)
+    int64_t M = a.M, N = a.N, K = a.K, kc = a.k_chunk;
+    int splits = a.splits;
+    asm volatile("" : "+s"(M), "+s"(N), "+s"(K), "+s"(kc), "+s"(splits));
+    const int64_t tiles_n = (N + BN - 1) / BN;             // shifts (BN, BM powers of two)
+    const int64_t tiles_m = (M + BM - 1) / BM;
     const int64_t per_split = tiles_m * tiles_n;
-    const int64_t total = per_split * a.splits;
+    const int64_t total = per_split * splits;
+    const bool fast = total < (int64_t(1) << 21);
+    auto dv = [fast](int64_t n, int64_t d) { return fast ? fdiv21(n, d) : n / d; };
     const int64_t G = gridDim.x;
     int64_t idx;
     if ((G & 7) == 0 && (total & 7) == 0) {
@@ -253,14 +294,15 @@ __device__ __forceinline__ bool pp_tile_at(const GemmArgs& a, int64_t i, PPTile*
         const int64_t j = (int64_t)(blockIdx.x >> 3) + i * (G >> 3);
         if (j >= per_xcd) return false;
         const int64_t x = blockIdx.x & 7;
-        if (a.splits == 1 && per_xcd % tiles_n == 0 && tiles_n > kBand) {
-            const int64_t rows = per_xcd / tiles_n;               // rows of tiles this XCD owns
+        const int64_t rows = dv(per_xcd, tiles_n);            // rows of tiles this XCD owns
+        if (splits == 1 && rows * tiles_n == per_xcd && tiles_n > kBand) {
             const int64_t nbands = (tiles_n + kBand - 1) / kBand;
-            int64_t band = j / (rows * kBand);
+            int64_t band = dv(j, rows * kBand);
             if (band > nbands - 1) band = nbands - 1;
             const int64_t off = j - band * rows * kBand;
             const int64_t w = min(kBand, tiles_n - band * kBand);  // width of this band
-            idx = (x * rows + off / w) * tiles_n + band * kBand + off % w;
+            const int64_t r = w == kBand ? off / kBand : dv(off, w);
+            idx = (x * rows + r) * tiles_n + band * kBand + (off - r * w);
         } else {
             idx = x * per_xcd + j;
         }
@@ -268,12 +310,13 @@ __device__ __forceinline__ bool pp_tile_at(const GemmArgs& a, int64_t i, PPTile*
         idx = (int64_t)blockIdx.x + i * G;
         if (idx >= total) return false;
     }
-    t->split = (int)(idx / per_split);
+    t->split = (int)dv(idx, per_split);
     const int64_t rem = idx - (int64_t)t->split * per_split;
-    t->m0 = (rem / tiles_n) * BM;
-    t->n0 = (rem % tiles_n) * BN;
-    t->kbeg = (int64_t)t->split * a.k_chunk;
-    t->nk = (int)((min(a.K, t->kbeg + a.k_chunk) - t->kbeg) / BK);
+    const int64_t tm = dv(rem, tiles_n);
+    t->m0 = tm * BM;
+    t->n0 = (rem - tm * tiles_n) * BN;
+    t->kbeg = (int64_t)t->split * kc;
+    t->nk = (int)((min(K, t->kbeg + kc) - t->kbeg) / kPPBK);
     return true;
 }
 
@@ -386,18 +429,18 @@ __global__ __launch_bounds__(NTHR, 1) void gemm_pp_persist_kernel(GemmArgs a) {
                     if constexpr (decltype(first)::value) {
                         if (s == 0) {
                             const f32x16 zero = {};
-                            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[s][i], fb[s][j], zero, 0, 0, 0);
+                            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[s][j], fa[s][i], zero, 0, 0, 0);
                             continue;
                         }
                     }
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[s][i], fb[s][j], acc[i][j], 0, 0, 0);
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[s][j], fa[s][i], acc[i][j], 0, 0, 0);
                 }
         if (prio) __builtin_amdgcn_s_setprio(0);
     };
 
     PPTile cur, nxt;
-    if (!pp_tile_at<BK>(a, 0, &cur)) return;
-    bool more = pp_tile_at<BK>(a, 1, &nxt);
+    if (!pp_tile_at(a, 0, &cur)) return;
+    bool more = pp_tile_at(a, 1, &nxt);
 
     // prologue: P(0), P(1) by group 1, Q(0) by group 0 (every tile has at
     // least two K tiles)
@@ -452,17 +495,15 @@ __global__ __launch_bounds__(NTHR, 1) void gemm_pp_persist_kernel(GemmArgs a) {
         int en0 = __builtin_amdgcn_readfirstlane((int)(cur.n0 + wl * WC));
         int esplit = __builtin_amdgcn_readfirstlane(cur.split);
         asm volatile("" : "+s"(em0), "+s"(en0), "+s"(esplit));
-        epilogue_block<EPI>(a, acc, (int64_t)em0, (int64_t)en0, lane, esplit);
+        epilogue_block_t<EPI>(a, acc, (int64_t)em0, (int64_t)en0, lane, esplit);
         barrier_lds();                                   // end of the epilogue phase
         if (!more) break;
         cur = nxt;
-        more = pp_tile_at<BK>(a, it + 2, &nxt);
+        more = pp_tile_at(a, it + 2, &nxt);
     }
     if (grp == 0) barrier_lds();
 }
 
-// K tile 64: whole 128-byte lines per load row.
-constexpr int kPPBK = 64;
 // Persistent grid: one workgroup per CU (256 on MI355X), a multiple of 8 when
 // possible so each XCD gets equal work.
 constexpr int64_t kPPGrid = 256;
