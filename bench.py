@@ -45,7 +45,7 @@ def parse():
     ap.add_argument("--workload", type=int, default=4, help="1..5 (default 4: LLaMA-1B-shaped block)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--streams", type=int, default=2,
-                    help="HIP streams the independent projections are spread over (CoLA, CoLA-M steps)")
+                    help="HIP streams the independent projections (or groups) of every step are spread over")
     ap.add_argument("--no-dense", action="store_true")
     ap.add_argument("--no-cola-m", action="store_true")
     ap.add_argument("--cpu-tokens", type=int, default=8192,
@@ -404,22 +404,22 @@ def main():
     wss = [ws] + [torch.empty(ws_need, dtype=torch.uint8, device="cuda:0") for _ in range(nstreams - 1)]
     setup_s = time.time() - t0
 
-    def spread(fwd, bwd):
-        if nstreams == 1:
-            for p in projs:
-                fwd(p, ws)
-            for p in reversed(projs):
-                bwd(p, ws)
-            return
+    def spread(items, fwd, bwd=None):
+        """fwd over items in order, then bwd in reverse order; item i on
+        stream i % S with that stream's workspace."""
         main = torch.cuda.current_stream()
         for st in streams[1:]:
             st.wait_stream(main)
-        order = list(enumerate(projs))
-        for phase, seq in ((fwd, order), (bwd, order[::-1])):
+        order = list(enumerate(items))
+        phases = [(fwd, order)] + ([(bwd, order[::-1])] if bwd is not None else [])
+        for phase, seq in phases:
             for i, p in seq:
                 k = i % nstreams
-                with torch.cuda.stream(streams[k] if k else main):
-                    phase(p, wss[k])
+                if k == 0:
+                    phase(p, wss[0])
+                else:
+                    with torch.cuda.stream(streams[k]):
+                        phase(p, wss[k])
         for st in streams[1:]:
             main.wait_stream(st)
 
@@ -430,28 +430,22 @@ def main():
             p.bwd(ws)
 
     def step_cola():
-        spread(lambda p, w: p.fwd(w), lambda p, w: p.bwd(w))
+        spread(projs, lambda p, w: p.fwd(w), lambda p, w: p.bwd(w))
 
     def step_cola_m():
-        spread(lambda p, w: p.fwd(w, True), lambda p, w: p.bwd(w, True))
+        spread(projs, lambda p, w: p.fwd(w, True), lambda p, w: p.bwd(w, True))
 
     def step_fused():
-        for u in units:
-            u.fwd(ws)
-        for u in reversed(units):
-            u.bwd(ws)
+        spread(units, lambda u, w: u.fwd(w), lambda u, w: u.bwd(w))
 
     def step_dense():
-        for p in projs:
-            p.dense_step(ws)
+        spread(projs, lambda p, w: p.dense_step(w))
 
     def step_infer():
-        for u in units:
-            u.infer(ws)
+        spread(units, lambda u, w: u.infer(w))
 
     def step_dense_infer():
-        for p in projs:
-            p.dense_fwd(ws)
+        spread(projs, lambda p, w: p.dense_fwd(w))
 
     flops_cola = sum(algo_flops_cola(T, p.d_in, p.d_out, r) for p in projs)
     flops_dense = sum(algo_flops_dense(T, p.d_in, p.d_out) for p in projs)
