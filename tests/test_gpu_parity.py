@@ -45,6 +45,14 @@ CASES = [
     # (24 x 12 tiles of Y = H B^T here, of dX = dZ A in the next case)
     ("persistent_banded_wide_out_bf16", 6044, 300, 3000, 128, "bf16", "silu"),
     ("persistent_banded_wide_in_bf16", 6044, 3000, 300, 128, "bf16", "silu"),
+    # 256 x 256 family with unaligned output rows: dX [T][301] and Y [T][263]
+    # (bf16, rows not a whole number of 16-byte chunks), dA [136][301] (fp32,
+    # rows not a whole number of 4 floats): the guarded stores of the
+    # transposed epilogue
+    ("odd_width_rank136_bf16", 600, 301, 263, 136, "bf16", "silu"),
+    # odd rank above 128: Z, H [T][137] written by the sigma epilogue and Z
+    # read by the dZ epilogue through the guarded paths
+    ("odd_rank137_bf16", 500, 264, 300, 137, "bf16", "silu"),
 ]
 
 
