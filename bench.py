@@ -396,25 +396,43 @@ def main():
     ws_need = max([p.ws_need for p in projs] + [u.ws_need for u in units if isinstance(u, Group)])
     ws = torch.empty(ws_need, dtype=torch.uint8, device="cuda:0")
     # independent projections spread over several HIP streams (default
-    # priority), each with its own workspace: projection i runs its forward
-    # and backward on stream i % S, so one kernel's ramp-up overlaps another
-    # stream's drain.  The step still starts and ends on the current stream.
+    # priority), each with its own workspace, balanced by work: a projection
+    # runs its forward and backward on one stream, and one kernel's ramp-up
+    # overlaps another stream's drain.  The step still starts and ends on the
+    # current stream.
     nstreams = max(1, args.streams)
     streams = [None] + [torch.cuda.Stream() for _ in range(nstreams - 1)]
     wss = [ws] + [torch.empty(ws_need, dtype=torch.uint8, device="cuda:0") for _ in range(nstreams - 1)]
     setup_s = time.time() - t0
 
-    def spread(items, fwd, bwd=None):
-        """fwd over items in order, then bwd in reverse order; item i on
-        stream i % S with that stream's workspace."""
+    def work(item, dense=False):
+        """relative work of a projection (or of a group's members)"""
+        if isinstance(item, Group):
+            return sum(work(m, dense) for m in item.m)
+        return item.T * (item.d_in * item.d_out if dense else item.r * (item.d_in + item.d_out))
+
+    def assign(items, dense=False):
+        """stream of each item: largest first, each to the least-loaded stream"""
+        load = [0.0] * nstreams
+        out = [0] * len(items)
+        for i in sorted(range(len(items)), key=lambda i: -work(items[i], dense)):
+            k = min(range(nstreams), key=lambda k: load[k])
+            out[i] = k
+            load[k] += work(items[i], dense)
+        return out
+
+    def spread(items, fwd, bwd=None, dense=False):
+        """fwd over items in order, then bwd in reverse order; each item on
+        the stream `assign` gives it, with that stream's workspace."""
         main = torch.cuda.current_stream()
         for st in streams[1:]:
             st.wait_stream(main)
+        where = assign(items, dense)
         order = list(enumerate(items))
         phases = [(fwd, order)] + ([(bwd, order[::-1])] if bwd is not None else [])
         for phase, seq in phases:
             for i, p in seq:
-                k = i % nstreams
+                k = where[i]
                 if k == 0:
                     phase(p, wss[0])
                 else:
@@ -439,13 +457,13 @@ def main():
         spread(units, lambda u, w: u.fwd(w), lambda u, w: u.bwd(w))
 
     def step_dense():
-        spread(projs, lambda p, w: p.dense_step(w))
+        spread(projs, lambda p, w: p.dense_step(w), dense=True)
 
     def step_infer():
         spread(units, lambda u, w: u.infer(w))
 
     def step_dense_infer():
-        spread(projs, lambda p, w: p.dense_fwd(w))
+        spread(projs, lambda p, w: p.dense_fwd(w), dense=True)
 
     flops_cola = sum(algo_flops_cola(T, p.d_in, p.d_out, r) for p in projs)
     flops_dense = sum(algo_flops_dense(T, p.d_in, p.d_out) for p in projs)
