@@ -266,7 +266,10 @@ typedef enum {
     COLA_KC_FILL = 10,     /* zero fill (empty batches)                */
     COLA_KC_INFER_H = 11,  /* H = sigma(X A^T), Z not kept (inference) */
     COLA_KC_OUTER_GRAD = 12, /* dP = dY (.) sigma_out'(P), both-sigma variant */
-    COLA_KC_COUNT = 13
+    COLA_KC_BWD_DADB = 13, /* dA and dB in one launch (bf16, both outputs
+                              wider than 128): the two token-split weight
+                              gradients share the launch and the split    */
+    COLA_KC_COUNT = 14
 } cola_kernel_class;
 
 /* Per-class totals since the last reset: launches, elapsed milliseconds,

@@ -22,7 +22,7 @@ OK, ERR_INVALID_ARG, ERR_BAD_SHAPE, ERR_WORKSPACE, ERR_HIP, ERR_UNSUPPORTED = ra
 
 KERNEL_CLASSES = ("fwd_z_sigma", "fwd_y", "bwd_dz", "bwd_dx", "bwd_da", "bwd_db",
                   "reduce_splits", "dense_fwd", "dense_dx", "dense_dw", "fill_zero", "infer_h",
-                  "outer_grad")
+                  "outer_grad", "bwd_da_db")
 
 
 class ColaError(RuntimeError):

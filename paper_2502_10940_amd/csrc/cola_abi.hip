@@ -9,11 +9,14 @@
 //              K4  dX = dZ A
 //              K5  dA partials = dZ^T X             (split over tokens)
 //              K6  dB partials = dY^T H             (split over tokens)
+//                  (bf16 with both outputs wider than 128: K5 and K6 in one
+//                  launch, one split of T for both)
 //              K7  dA, dB = fixed-order sums of the partials
 //   dense    : Y = X W^T ; dX = dY W ; dW = dY^T X (split over tokens + K7)
 #include <mutex>
 #include <new>
 #include <stdio.h>
+#include <stdlib.h>
 #include <string.h>
 #include <vector>
 
@@ -161,14 +164,14 @@ struct Split {
 // and slots is the number of workgroups the chip runs at once -- a split that
 // leaves a few workgroups for a second round costs a whole round -- plus
 // writing and re-reading the S fp32 partials at about 4 TB/s.
-Split plan_split(bool bf16, int64_t M, int64_t N, int64_t K, int tag) {
+// Split of K for `tiles` output tiles (workgroups) on `slots` resident
+// workgroups, whose fp32 partials total `elems` values per split.
+Split plan_split_tiles(bool bf16, int64_t tiles, int64_t slots, int64_t K, double elems) {
     const int64_t bk = bf16 ? BF16_BK : F32_BK;
-    const int64_t tiles = gemm_tiles(bf16, M, N, tag);
-    const int64_t slots = gemm_slots(bf16, M, N, tag);
     const int64_t ktiles = (K + bk - 1) / bk;
     if (ktiles < 1) return Split{1, bk};                       // empty batch: nothing to split
     const double step_us = 2.0;
-    const double partial_us_per_split = (double)M * (double)N * 8.0 / 4.0e6;
+    const double partial_us_per_split = elems * 8.0 / 4.0e6;
     int64_t maxs = ktiles / 4;
     if (maxs < 1) maxs = 1;
     if (maxs > 64) maxs = 64;
@@ -191,6 +194,28 @@ Split plan_split(bool bf16, int64_t M, int64_t N, int64_t K, int tag) {
     s.splits = (int)((K + s.k_chunk - 1) / s.k_chunk);
     if (s.splits < 1) s.splits = 1;
     return s;
+}
+
+Split plan_split(bool bf16, int64_t M, int64_t N, int64_t K, int tag) {
+    return plan_split_tiles(bf16, gemm_tiles(bf16, M, N, tag), gemm_slots(bf16, M, N, tag), K,
+                            (double)M * (double)N);
+}
+
+// The two weight gradients of a layer in one launch (bf16, both in the PP
+// family): their tiles share the slots and one split of K = T.
+// COLA_WGRAD_PAIR=0 launches them one by one (tuning, comparisons).
+bool pair_wgrads(bool bf16, int64_t r, int64_t d_in, int64_t d_out) {
+    static const bool off = [] {
+        const char* e = getenv("COLA_WGRAD_PAIR");
+        return e != nullptr && e[0] == '0';
+    }();
+    return !off && bf16 && gemm_family(r, d_in, TAG_BWD_DA) == FAM_PP &&
+           gemm_family(d_out, r, TAG_BWD_DB) == FAM_PP;
+}
+Split plan_split_pair(int64_t r, int64_t d_in, int64_t d_out, int64_t T) {
+    const int64_t tiles = gemm_tiles(true, r, d_in, TAG_BWD_DA) + gemm_tiles(true, d_out, r, TAG_BWD_DB);
+    return plan_split_tiles(true, tiles, gemm_slots(true, r, d_in, TAG_BWD_DA), T,
+                            (double)r * (double)d_in + (double)d_out * (double)r);
 }
 
 // Row pitch (elements) of a buffer the library lays out itself: a whole
@@ -253,7 +278,8 @@ FwdPlan plan_fwd(const Dims& x, bool recompute) {
 struct BwdPlan {
     int64_t ldw;          // pitch of dZ (and recomputed H) in the workspace
     size_t off_dz, off_h, off_pa, off_pb, total;
-    Split sa, sb;
+    Split sa, sb;         // the same split for both when pair
+    bool pair;            // dA and dB in one launch
     Pack wa, wb;          // repacked A and B
 };
 
@@ -261,8 +287,13 @@ BwdPlan plan_bwd(const Dims& x, bool recompute) {
     BwdPlan p;
     p.ldw = line_pitch(x.bf16, x.r);
     const size_t zbytes = align256((size_t)x.T * (size_t)p.ldw * x.esize);
-    p.sa = plan_split(x.bf16, x.r, x.d_in, x.T, TAG_BWD_DA);
-    p.sb = plan_split(x.bf16, x.d_out, x.r, x.T, TAG_BWD_DB);
+    p.pair = pair_wgrads(x.bf16, x.r, x.d_in, x.d_out);
+    if (p.pair) {
+        p.sa = p.sb = plan_split_pair(x.r, x.d_in, x.d_out, x.T);
+    } else {
+        p.sa = plan_split(x.bf16, x.r, x.d_in, x.T, TAG_BWD_DA);
+        p.sb = plan_split(x.bf16, x.d_out, x.r, x.T, TAG_BWD_DB);
+    }
     p.off_dz = 0;
     p.off_h = zbytes;
     p.off_pa = p.off_h + (recompute ? zbytes : 0);
@@ -319,6 +350,40 @@ int wgrad(bool bf16, int64_t M, int64_t N, int64_t T, const void* P, int64_t ldp
         e = timed(COLA_KC_REDUCE, 0.0, rb, s,
                   [&] { return launch_reduce_splits(partials, sp.splits, M * N, C, M * N, s); });
         if (e != hipSuccess) return hip_fail(e, "reduce");
+    }
+    return COLA_OK;
+}
+
+// Both weight gradients of a layer, C0[M0][N0] = sum_t P0[t][m] Q0[t][n] and
+// C1 likewise, in one launch with one split of K = T (bf16 PP family), then
+// the fixed-order reductions of their partials.
+int wgrad_pair(int64_t T, const Split& sp, int64_t M0, int64_t N0, const void* P0, int64_t ldp0, const void* Q0,
+               int64_t ldq0, float* C0, float* part0, int64_t M1, int64_t N1, const void* P1, int64_t ldp1,
+               const void* Q1, int64_t ldq1, float* C1, float* part1, double bytes_in, hipStream_t s) {
+    GemmArgs a0 = make_args(TAG_BWD_DA, M0, N0, T, P0, ldp0, MNMAJ, Q0, ldq0, MNMAJ, C0, N0, EPI_STORE_F32, 0);
+    GemmArgs a1 = make_args(TAG_BWD_DB, M1, N1, T, P1, ldp1, MNMAJ, Q1, ldq1, MNMAJ, C1, N1, EPI_STORE_F32, 0);
+    for (GemmArgs* a : {&a0, &a1}) {
+        a->splits = sp.splits;
+        a->k_chunk = sp.k_chunk;
+    }
+    if (sp.splits > 1) {
+        a0.c = part0;
+        a0.split_stride = M0 * N0;
+        a1.c = part1;
+        a1.split_stride = M1 * N1;
+    }
+    const double elems = (double)M0 * (double)N0 + (double)M1 * (double)N1;
+    const double out_bytes = elems * 4.0 * (sp.splits > 1 ? sp.splits : 1);
+    hipError_t e = timed(COLA_KC_BWD_DADB, gemm_flops(M0, N0, T) + gemm_flops(M1, N1, T), bytes_in + out_bytes, s,
+                         [&] { return launch_gemm_bf16_pair(a0, a1, s); });
+    if (e != hipSuccess) return hip_fail(e, cola_kernel_name(COLA_KC_BWD_DADB));
+    if (sp.splits > 1) {
+        struct { const float* part; float* out; int64_t n; } red[2] = {{part0, C0, M0 * N0}, {part1, C1, M1 * N1}};
+        for (const auto& r : red) {
+            e = timed(COLA_KC_REDUCE, 0.0, (double)r.n * 4.0 * (sp.splits + 1), s,
+                      [&] { return launch_reduce_splits(r.part, sp.splits, r.n, r.out, r.n, s); });
+            if (e != hipSuccess) return hip_fail(e, "reduce");
+        }
     }
     return COLA_OK;
 }
@@ -412,7 +477,14 @@ int layer_backward(const Dims& x, int act, bool recompute, const void* dY, int64
     e = timed(COLA_KC_BWD_DX, gemm_flops(x.T, x.d_in, x.r), b4, s, [&] { return gemm(k4, x.bf16, s); });
     if (e != hipSuccess) return hip_fail(e, "bwd_dx");
 
-    // K5: dA = dZ^T X ; K6: dB = dY^T H  (+ K7 fixed-order reductions)
+    // K5: dA = dZ^T X ; K6: dB = dY^T H  (+ K7 fixed-order reductions);
+    // one launch for both when they share the PP family
+    if (p.pair)
+        return wgrad_pair(x.T, p.sa, x.r, x.d_in, dZ, p.ldw, X, x.ldx, dA, reinterpret_cast<float*>(w + p.off_pa),
+                          x.d_out, x.r, dY, ldy, Hbuf, ldh, dB, reinterpret_cast<float*>(w + p.off_pb),
+                          es * ((double)x.T * x.r + (double)x.T * x.d_in + (double)x.T * x.d_out +
+                                (double)x.T * x.r),
+                          s);
     int st = wgrad(x.bf16, x.r, x.d_in, x.T, dZ, p.ldw, X, x.ldx, dA, p.sa,
                reinterpret_cast<float*>(w + p.off_pa), COLA_KC_BWD_DA,
                es * ((double)x.T * x.r + (double)x.T * x.d_in), s);
@@ -467,7 +539,8 @@ const char* cola_strerror(int status) {
 const char* cola_kernel_name(int kc) {
     static const char* names[COLA_KC_COUNT] = {
         "fwd_z_sigma", "fwd_y", "bwd_dz", "bwd_dx", "bwd_da", "bwd_db",
-        "reduce_splits", "dense_fwd", "dense_dx", "dense_dw", "fill_zero", "infer_h", "outer_grad"};
+        "reduce_splits", "dense_fwd", "dense_dx", "dense_dw", "fill_zero", "infer_h", "outer_grad",
+        "bwd_da_db"};
     if (kc < 0 || kc >= COLA_KC_COUNT) return "invalid";
     return names[kc];
 }

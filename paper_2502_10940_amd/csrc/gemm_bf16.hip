@@ -328,6 +328,14 @@ int gemm_family(int64_t M, int64_t N, int tag) {
     return bf16_wide_ok(M, N) ? (int)FAM_PP : (int)FAM_STREAM;
 }
 
+hipError_t launch_gemm_bf16_pair(const GemmArgs& a0, const GemmArgs& a1, hipStream_t s) {
+    const bool pp = gemm_family(a0.M, a0.N, a0.tag) == FAM_PP && gemm_family(a1.M, a1.N, a1.tag) == FAM_PP &&
+                    big_operands_ok(a0) && big_operands_ok(a1);
+    if (pp) return launch_gemm_pp_pair(a0, a1, s);
+    hipError_t e = launch_gemm_bf16(a0, s);
+    return e == hipSuccess ? launch_gemm_bf16(a1, s) : e;
+}
+
 hipError_t launch_gemm_bf16(const GemmArgs& a, hipStream_t s) {
     switch (gemm_family(a.M, a.N, a.tag)) {
         case FAM_WIDE: return launch_gemm_wide(a, s);

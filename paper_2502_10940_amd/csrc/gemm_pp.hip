@@ -49,21 +49,34 @@ constexpr int NQ = 2;            // Q slots (one K tile ahead)
 // per load row.
 constexpr int kPPBK = 64;
 
-template <int BK, int PL, int QL, int EPI, int TAG>
-__global__ __launch_bounds__(NTHR, 1) void gemm_pp_kernel(GemmArgs a) {
+// LDS of one workgroup: NP P slots and NQ Q slots.
+template <int PL, int QL, int BK>
+constexpr int pp_smem_bytes() {
+    return NP * BTile<PL, BK>::BYTES + NQ * BTile<QL, BK>::BYTES;
+}
+
+// Block number with an XCD-aware renumbering (the hardware hands block b to
+// XCD b % 8): with a grid that is a multiple of 8, XCD x gets the contiguous
+// range [x G/8, (x+1) G/8) of output tiles.
+__device__ __forceinline__ int64_t xcd_block() {
+    const int64_t nb = gridDim.x;
+    int64_t b = blockIdx.x;
+    if ((nb & 7) == 0) b = (b & 7) * (nb >> 3) + (b >> 3);
+    return b;
+}
+
+// One output tile (tile and split number b of the product a) of one
+// workgroup, with the rings in smem.
+template <int BK, int PL, int QL, int EPI>
+__device__ __forceinline__ void pp_one_tile(const GemmArgs& a, int64_t b, char* smem) {
     using TP = BTile<PL, BK>;
     using TQ = BTile<QL, BK>;
     constexpr int NSUB = BK / 16;                 // 16-deep k steps per K tile
     constexpr int POPS = TP::DPW;                 // loads per loader wave per P tile (4 loaders)
     constexpr int QOPS = TQ::DPW;
-    __shared__ __attribute__((aligned(1024))) char smem[NP * TP::BYTES + NQ * TQ::BYTES];
     char* const pring = smem;
     char* const qring = smem + NP * TP::BYTES;
 
-    // output tile: XCD-aware renumbering (hardware hands block b to XCD b % 8)
-    const int64_t nb = gridDim.x;
-    int64_t b = blockIdx.x;
-    if ((nb & 7) == 0) b = (b & 7) * (nb >> 3) + (b >> 3);
     const int64_t tiles_n = (a.N + BN - 1) / BN;
     const int64_t tiles_m = (a.M + BM - 1) / BM;
     const int64_t per_split = tiles_m * tiles_n;
@@ -218,6 +231,25 @@ __global__ __launch_bounds__(NTHR, 1) void gemm_pp_kernel(GemmArgs a) {
         compute_tile();
     }
     epilogue_block_t<EPI>(a, acc, m0 + grp * WR, n0 + wl * WC, lane, split);
+}
+
+// One workgroup per output tile (and split).
+template <int BK, int PL, int QL, int EPI, int TAG>
+__global__ __launch_bounds__(NTHR, 1) void gemm_pp_kernel(GemmArgs a) {
+    __shared__ __attribute__((aligned(1024))) char smem[pp_smem_bytes<PL, QL, BK>()];
+    pp_one_tile<BK, PL, QL, EPI>(a, xcd_block(), smem);
+}
+
+// Two products of the same kind in one grid: blocks [0, nb0) are the tiles
+// and splits of a0, the rest those of a1 (the two weight gradients of a
+// layer, which share K = T: one launch, one set of partials per split for
+// both, and their tiles together fill the CUs).
+template <int BK, int PL, int QL, int EPI, int TAG>
+__global__ __launch_bounds__(NTHR, 1) void gemm_pp_pair_kernel(GemmArgs a0, GemmArgs a1, int64_t nb0) {
+    __shared__ __attribute__((aligned(1024))) char smem[pp_smem_bytes<PL, QL, BK>()];
+    const int64_t b = xcd_block();
+    if (b < nb0) pp_one_tile<BK, PL, QL, EPI>(a0, b, smem);
+    else pp_one_tile<BK, PL, QL, EPI>(a1, b - nb0, smem);
 }
 
 // ---- persistent variant (every K range a whole number of K tiles, at
@@ -530,6 +562,20 @@ hipError_t launch_p(const GemmArgs& a, hipStream_t s) {
 }
 
 }  // namespace
+
+hipError_t launch_gemm_pp_pair(const GemmArgs& a0, const GemmArgs& a1, hipStream_t s) {
+    for (const GemmArgs* a : {&a0, &a1})
+        if (a->p_layout != MNMAJ || a->q_layout != MNMAJ || a->epi != EPI_STORE_F32) return hipErrorInvalidValue;
+    auto blocks = [](const GemmArgs& a) {
+        return ((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN) * (int64_t)a.splits;
+    };
+    const int64_t nb0 = blocks(a0), nb1 = blocks(a1);
+    if (nb0 + nb1 <= 0) return hipSuccess;
+    if (nb0 + nb1 > 0x7fffffffLL) return hipErrorInvalidConfiguration;
+    hipLaunchKernelGGL((gemm_pp_pair_kernel<kPPBK, MNMAJ, MNMAJ, EPI_STORE_F32, TAG_BWD_DA>),
+                       dim3((unsigned)(nb0 + nb1)), dim3(NTHR), 0, s, a0, a1, nb0);
+    return hipGetLastError();
+}
 
 hipError_t launch_gemm_pp(const GemmArgs& a, hipStream_t s) {
     switch (a.tag) {

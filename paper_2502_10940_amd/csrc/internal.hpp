@@ -57,6 +57,12 @@ hipError_t launch_gemm_wide(const GemmArgs& a, hipStream_t s);
 //   PP     -- 256 x 256 tiles, two wave groups per workgroup in ping-pong
 hipError_t launch_gemm_big(const GemmArgs& a, hipStream_t s);
 hipError_t launch_gemm_pp(const GemmArgs& a, hipStream_t s);
+// Two weight-gradient products (both operands m-contiguous, fp32 output) in
+// one PP grid: a0's tiles and splits, then a1's.  Operands as for PP.
+hipError_t launch_gemm_pp_pair(const GemmArgs& a0, const GemmArgs& a1, hipStream_t s);
+// a0 and a1 in one launch when both go to the PP family with operands it
+// takes (else one launch each, as launch_gemm_bf16).
+hipError_t launch_gemm_bf16_pair(const GemmArgs& a0, const GemmArgs& a1, hipStream_t s);
 
 enum Family : int { FAM_REG = 0, FAM_STREAM = 1, FAM_WIDE = 2, FAM_BIG = 3, FAM_PP = 4 };
 // Family used for a GEMM (also used by the split planner).  The environment
