@@ -114,7 +114,8 @@ def traffic_summary(fetch_csv, write_csv, copy_fetch_csv, copy_write_csv):
             m = re.search(r"gemm_\w+_kernel<[^>]*, (\d+)>", name)
             if not m:
                 continue
-            cls = KERNEL_TAGS.get(int(m.group(1)))
+            # the launch of both weight gradients carries the dA tag
+            cls = "bwd_da_db" if "pair_kernel" in name else KERNEL_TAGS.get(int(m.group(1)))
             per.setdefault(cls, {}).setdefault(key, []).append(v * 1024.0 * scale)
     h = kernel_source_hash()
     out = {"_note": "HBM bytes per launch from rocprofv3 FETCH_SIZE + WRITE_SIZE, scaled by a "
