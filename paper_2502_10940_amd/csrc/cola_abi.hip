@@ -204,12 +204,15 @@ Split plan_split(bool bf16, int64_t M, int64_t N, int64_t K, int tag) {
 // The two weight gradients of a layer in one launch (bf16, both in the PP
 // family): their tiles share the slots and one split of K = T.
 // COLA_WGRAD_PAIR=0 launches them one by one (tuning, comparisons).
-bool pair_wgrads(bool bf16, int64_t r, int64_t d_in, int64_t d_out) {
+bool wgrad_pairing_on() {
     static const bool off = [] {
         const char* e = getenv("COLA_WGRAD_PAIR");
         return e != nullptr && e[0] == '0';
     }();
-    return !off && bf16 && gemm_family(r, d_in, TAG_BWD_DA) == FAM_PP &&
+    return !off;
+}
+bool pair_wgrads(bool bf16, int64_t r, int64_t d_in, int64_t d_out) {
+    return wgrad_pairing_on() && bf16 && gemm_family(r, d_in, TAG_BWD_DA) == FAM_PP &&
            gemm_family(d_out, r, TAG_BWD_DB) == FAM_PP;
 }
 Split plan_split_pair(int64_t r, int64_t d_in, int64_t d_out, int64_t T) {
@@ -831,14 +834,34 @@ GFwdPlan plan_group_fwd(const GDims& g, bool recompute) {
     return p;
 }
 
-// Workspace: [dZ_all] [H_all (CoLA-M)] [dA partials] [dB partials, reused
-// projection after projection] [repacked A_all] [repacked B_p ...]
+// The weight gradients of a group are the products w = 0 (dA_all, R x d_in)
+// and w = 1 + p (dB_p, d_out_p x r_p), all over K = T.  They run in pairs
+// (0, 1), (2, 3), ...: one launch with one split for a pair whose members
+// both go to the PP family (bf16, both output dimensions above 128), else one
+// launch each.  Workspace: [dZ_all] [H_all (CoLA-M)] [partials of the first
+// member of a pair] [of the second], both reused pair after pair,
+// [repacked A_all] [repacked B_p ...].
 struct GBwdPlan {
     int64_t ldw;
-    size_t off_dz, off_h, off_pa, off_pb, total;
-    Split sa, sb[COLA_GROUP_MAX];
+    size_t off_dz, off_h, off_p0, off_p1, total;
+    int nw;                                // 1 + number of projections
+    Split sp[COLA_GROUP_MAX + 1];          // split of each product (shared within a launched pair)
+    bool paired[COLA_GROUP_MAX + 1];       // pair starting at an even w launched together
     Pack wa, wb[COLA_GROUP_MAX];
 };
+
+// Shape (M, N) and kernel tag of weight-gradient product w of a group.
+void group_wgrad_shape(const GDims& g, int w, int64_t* M, int64_t* N, int* tag) {
+    if (w == 0) {
+        *M = g.R;
+        *N = g.d_in;
+        *tag = TAG_BWD_DA;
+    } else {
+        *M = g.d_out[w - 1];
+        *N = g.r[w - 1];
+        *tag = TAG_BWD_DB;
+    }
+}
 
 GBwdPlan plan_group_bwd(const GDims& g, bool recompute) {
     GBwdPlan p;
@@ -846,17 +869,31 @@ GBwdPlan plan_group_bwd(const GDims& g, bool recompute) {
     const size_t zbytes = align256((size_t)g.T * (size_t)p.ldw * g.esize);
     p.off_dz = 0;
     p.off_h = zbytes;
-    p.off_pa = p.off_h + (recompute ? zbytes : 0);
-    p.sa = plan_split(g.bf16, g.R, g.d_in, g.T, TAG_BWD_DA);
-    const size_t pa = p.sa.splits > 1 ? align256((size_t)p.sa.splits * (size_t)(g.R * g.d_in) * 4) : 0;
-    p.off_pb = p.off_pa + pa;
-    size_t pb = 0;
-    for (int q = 0; q < g.n; ++q) {
-        p.sb[q] = plan_split(g.bf16, g.d_out[q], g.r[q], g.T, TAG_BWD_DB);
-        const size_t b = p.sb[q].splits > 1 ? align256((size_t)p.sb[q].splits * (size_t)(g.d_out[q] * g.r[q]) * 4) : 0;
-        if (b > pb) pb = b;
+    p.off_p0 = p.off_h + (recompute ? zbytes : 0);
+    p.nw = g.n + 1;
+    size_t pb[2] = {0, 0};
+    for (int w0 = 0; w0 < p.nw; w0 += 2) {
+        int64_t M[2], N[2];
+        int tag[2];
+        const int cnt = w0 + 1 < p.nw ? 2 : 1;
+        for (int k = 0; k < cnt; ++k) group_wgrad_shape(g, w0 + k, &M[k], &N[k], &tag[k]);
+        p.paired[w0] = cnt == 2 && wgrad_pairing_on() && g.bf16 && gemm_family(M[0], N[0], tag[0]) == FAM_PP &&
+                       gemm_family(M[1], N[1], tag[1]) == FAM_PP;
+        if (p.paired[w0]) {
+            const int64_t tiles = gemm_tiles(true, M[0], N[0], tag[0]) + gemm_tiles(true, M[1], N[1], tag[1]);
+            p.sp[w0] = p.sp[w0 + 1] = plan_split_tiles(true, tiles, gemm_slots(true, M[0], N[0], tag[0]), g.T,
+                                                       (double)M[0] * N[0] + (double)M[1] * N[1]);
+        } else {
+            for (int k = 0; k < cnt; ++k) p.sp[w0 + k] = plan_split(g.bf16, M[k], N[k], g.T, tag[k]);
+        }
+        for (int k = 0; k < cnt; ++k) {
+            const Split& sp = p.sp[w0 + k];
+            const size_t b = sp.splits > 1 ? align256((size_t)sp.splits * (size_t)(M[k] * N[k]) * 4) : 0;
+            if (b > pb[k]) pb[k] = b;
+        }
     }
-    p.wa = plan_pack(g.bf16, g.R, g.d_in, p.off_pb + pb);
+    p.off_p1 = p.off_p0 + pb[0];
+    p.wa = plan_pack(g.bf16, g.R, g.d_in, p.off_p1 + pb[1]);
     size_t next = p.wa.off + p.wa.bytes;
     for (int q = 0; q < g.n; ++q) {
         p.wb[q] = plan_pack(g.bf16, g.d_out[q], g.r[q], next);
@@ -1058,17 +1095,37 @@ int cola_group_bwd(const cola_group_desc* desc, const void* const* dY, const voi
         e = timed(COLA_KC_BWD_DX, gemm_flops(g.T, g.d_in, g.R), b4, s, [&] { return gemm(k4, g.bf16, s); });
         if (e != hipSuccess) return hip_fail(e, "bwd_dx");
 
-        // K5 for every projection at once: dA_all = dZ_all^T X
-        st = wgrad(g.bf16, g.R, g.d_in, g.T, dZ, p.ldw, X, g.ldx, dA_all, p.sa,
-                   reinterpret_cast<float*>(w + p.off_pa), COLA_KC_BWD_DA,
-                   es * ((double)g.T * g.R + (double)g.T * g.d_in), s);
-        if (st != COLA_OK) return st;
-        // K6 per projection: dB_p = dY_p^T H_p
-        for (int q = 0; q < g.n; ++q) {
-            st = wgrad(g.bf16, g.d_out[q], g.r[q], g.T, dY[q], g.ldy[q], Hbuf + g.off[q] * g.esize, ldh, dB[q],
-                       p.sb[q], reinterpret_cast<float*>(w + p.off_pb), COLA_KC_BWD_DB,
-                       es * ((double)g.T * g.d_out[q] + (double)g.T * g.r[q]), s);
-            if (st != COLA_OK) return st;
+        // K5 for every projection at once, dA_all = dZ_all^T X (product 0),
+        // and K6 per projection, dB_p = dY_p^T H_p (product 1 + p), in pairs
+        struct Prod {
+            int64_t M, N;
+            const void *P, *Q;
+            int64_t ldp, ldq;
+            float* C;
+            int kc;
+        };
+        Prod pr[COLA_GROUP_MAX + 1];
+        pr[0] = Prod{g.R, g.d_in, dZ, X, p.ldw, g.ldx, dA_all, COLA_KC_BWD_DA};
+        for (int q = 0; q < g.n; ++q)
+            pr[q + 1] = Prod{g.d_out[q], g.r[q], dY[q], Hbuf + g.off[q] * g.esize, g.ldy[q], ldh, dB[q],
+                             COLA_KC_BWD_DB};
+        float* part[2] = {reinterpret_cast<float*>(w + p.off_p0), reinterpret_cast<float*>(w + p.off_p1)};
+        auto in_bytes = [&](const Prod& a) { return es * ((double)g.T * a.M + (double)g.T * a.N); };
+        for (int w0 = 0; w0 < p.nw; w0 += 2) {
+            const int cnt = w0 + 1 < p.nw ? 2 : 1;
+            if (p.paired[w0]) {
+                const Prod &a = pr[w0], &b = pr[w0 + 1];
+                st = wgrad_pair(g.T, p.sp[w0], a.M, a.N, a.P, a.ldp, a.Q, a.ldq, a.C, part[0], b.M, b.N, b.P, b.ldp,
+                                b.Q, b.ldq, b.C, part[1], in_bytes(a) + in_bytes(b), s);
+                if (st != COLA_OK) return st;
+                continue;
+            }
+            for (int k = 0; k < cnt; ++k) {
+                const Prod& a = pr[w0 + k];
+                st = wgrad(g.bf16, a.M, a.N, g.T, a.P, a.ldp, a.Q, a.ldq, a.C, p.sp[w0 + k], part[k], a.kc,
+                           in_bytes(a), s);
+                if (st != COLA_OK) return st;
+            }
         }
         return COLA_OK;
     });

@@ -26,6 +26,8 @@ TOL = {"f32": 1e-5, "bf16": 1e-2}
 CASES = [
     ("qkv_bf16", 700, 520, [136, 136, 136], [264, 264, 264], "bf16", "silu"),
     ("gate_up_bf16", 513, 256, [64, 64], [688, 688], "bf16", "silu"),
+    # weight gradients dA_all with dB_gate in one launch, dB_up alone
+    ("gate_up_wide_bf16", 600, 264, [136, 136], [300, 300], "bf16", "silu"),
     ("ragged_odd_bf16", 333, 301, [37, 64, 9], [100, 1, 77], "bf16", "gelu"),
     ("single_f32", 130, 70, [20], [90], "f32", "silu"),
     ("pair_f32", 77, 130, [33, 8], [65, 40], "f32", "gelu"),
