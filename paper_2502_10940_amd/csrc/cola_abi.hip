@@ -381,12 +381,10 @@ int wgrad_pair(int64_t T, const Split& sp, int64_t M0, int64_t N0, const void* P
                          [&] { return launch_gemm_bf16_pair(a0, a1, s); });
     if (e != hipSuccess) return hip_fail(e, cola_kernel_name(COLA_KC_BWD_DADB));
     if (sp.splits > 1) {
-        struct { const float* part; float* out; int64_t n; } red[2] = {{part0, C0, M0 * N0}, {part1, C1, M1 * N1}};
-        for (const auto& r : red) {
-            e = timed(COLA_KC_REDUCE, 0.0, (double)r.n * 4.0 * (sp.splits + 1), s,
-                      [&] { return launch_reduce_splits(r.part, sp.splits, r.n, r.out, r.n, s); });
-            if (e != hipSuccess) return hip_fail(e, "reduce");
-        }
+        e = timed(COLA_KC_REDUCE, 0.0, elems * 4.0 * (sp.splits + 1), s, [&] {
+            return launch_reduce_splits2(part0, M0 * N0, C0, M0 * N0, part1, M1 * N1, C1, M1 * N1, sp.splits, s);
+        });
+        if (e != hipSuccess) return hip_fail(e, "reduce");
     }
     return COLA_OK;
 }

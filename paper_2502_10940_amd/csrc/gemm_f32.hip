@@ -139,14 +139,16 @@ hipError_t launch_gemm_f32(const GemmArgs& a, hipStream_t s) {
 // ---------------------------------------------------------------------------
 namespace {
 
-__global__ __launch_bounds__(256) void reduce_splits_kernel(const float* __restrict__ part, int splits,
-                                                            int64_t stride, float* __restrict__ out,
-                                                            int64_t n) {
+// out[i] = sum_k part[k * stride + i] over k = 0 .. splits-1 in that order,
+// by block blk of nblk blocks (grid-stride over float4 groups, scalar tail).
+__device__ __forceinline__ void reduce_splits_range(const float* __restrict__ part, int splits, int64_t stride,
+                                                    float* __restrict__ out, int64_t n, int64_t blk,
+                                                    int64_t nblk) {
     const int64_t n4 = n >> 2;
     const bool vec = ((stride & 3) == 0) && ((reinterpret_cast<uintptr_t>(part) & 15u) == 0) &&
                      ((reinterpret_cast<uintptr_t>(out) & 15u) == 0);
-    const int64_t step = (int64_t)gridDim.x * blockDim.x;
-    int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const int64_t step = nblk * blockDim.x;
+    int64_t i = blk * blockDim.x + threadIdx.x;
     if (vec) {
         for (; i < n4; i += step) {
             float4 s = reinterpret_cast<const float4*>(part)[i];
@@ -157,13 +159,30 @@ __global__ __launch_bounds__(256) void reduce_splits_kernel(const float* __restr
             reinterpret_cast<float4*>(out)[i] = s;
         }
         // scalar tail
-        i = n4 * 4 + (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+        i = n4 * 4 + blk * blockDim.x + threadIdx.x;
     }
     for (; i < n; i += step) {
         float s = part[i];
         for (int k = 1; k < splits; ++k) s += part[(int64_t)k * stride + i];
         out[i] = s;
     }
+}
+
+__global__ __launch_bounds__(256) void reduce_splits_kernel(const float* __restrict__ part, int splits,
+                                                            int64_t stride, float* __restrict__ out,
+                                                            int64_t n) {
+    reduce_splits_range(part, splits, stride, out, n, blockIdx.x, gridDim.x);
+}
+
+// Two reductions with the same split count in one launch: blocks [0, g0) sum
+// the partials of output 0, the rest those of output 1 (same order, so the
+// same bits as two launches).
+__global__ __launch_bounds__(256) void reduce_splits2_kernel(const float* __restrict__ p0, int64_t st0,
+                                                             float* __restrict__ o0, int64_t n0, int64_t g0,
+                                                             const float* __restrict__ p1, int64_t st1,
+                                                             float* __restrict__ o1, int64_t n1, int splits) {
+    if ((int64_t)blockIdx.x < g0) reduce_splits_range(p0, splits, st0, o0, n0, blockIdx.x, g0);
+    else reduce_splits_range(p1, splits, st1, o1, n1, (int64_t)blockIdx.x - g0, (int64_t)gridDim.x - g0);
 }
 
 __global__ __launch_bounds__(256) void fill_zero_kernel(float* __restrict__ out, int64_t n) {
@@ -247,6 +266,16 @@ unsigned grid_for(int64_t work) {
 }
 
 }  // namespace
+
+hipError_t launch_reduce_splits2(const float* p0, int64_t st0, float* o0, int64_t n0, const float* p1, int64_t st1,
+                                 float* o1, int64_t n1, int splits, hipStream_t s) {
+    if (n0 <= 0) return launch_reduce_splits(p1, splits, st1, o1, n1, s);
+    if (n1 <= 0) return launch_reduce_splits(p0, splits, st0, o0, n0, s);
+    const unsigned g0 = grid_for((n0 + 3) / 4), g1 = grid_for((n1 + 3) / 4);
+    hipLaunchKernelGGL(reduce_splits2_kernel, dim3(g0 + g1), dim3(256), 0, s, p0, st0, o0, n0, (int64_t)g0, p1, st1,
+                       o1, n1, splits);
+    return hipGetLastError();
+}
 
 hipError_t launch_reduce_splits(const float* part, int splits, int64_t stride, float* out, int64_t n,
                                 hipStream_t s) {

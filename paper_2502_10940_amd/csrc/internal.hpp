@@ -74,6 +74,9 @@ hipError_t launch_gemm_f32(const GemmArgs& a, hipStream_t s);
 // out[i] = sum_{s < splits} part[s * stride + i], s in increasing order (fp32).
 hipError_t launch_reduce_splits(const float* part, int splits, int64_t stride,
                                 float* out, int64_t n, hipStream_t s);
+// Both at once for two outputs with the same split count (one launch).
+hipError_t launch_reduce_splits2(const float* p0, int64_t st0, float* o0, int64_t n0, const float* p1, int64_t st1,
+                                 float* o1, int64_t n1, int splits, hipStream_t s);
 // dst[r][c] = src[r][c] for c < width, 0 for width <= c < ld (16-bit
 // elements; src rows are contiguous).  Gives weights with odd widths a
 // 16-byte aligned row pitch.
