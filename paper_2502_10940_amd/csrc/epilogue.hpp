@@ -286,9 +286,9 @@ __device__ __forceinline__ void epilogue_block_impl(const GemmArgs& a, const f32
                     }
                 }
     } else if constexpr (EPI == EPI_DZ) {
-        // Z for row tile i+1 is loaded before row tile i's stores: a wave's
-        // vector-memory operations complete in order, so a Z load issued
-        // after a store would also wait for that store.
+        // Z for row tile i+1 is loaded before row tile i's stores: loads and
+        // stores share one wait counter, so waiting for a Z load issued after
+        // a store would also wait for that store.
         u32x2_t zb[2][4][TN];
 #pragma unroll
         for (int g = 0; g < 4; ++g)
@@ -468,9 +468,9 @@ __device__ __forceinline__ void epilogue_t_impl(const GemmArgs& a, const f32x16 
     uint16_t* Hp = reinterpret_cast<uint16_t*>(a.aux);
     const uint16_t* Zp = reinterpret_cast<const uint16_t*>(a.zin);
     // EPI_DZ: Z (in the layout after exchange 1) of tile row i + 1 is loaded
-    // before the stores of tile row i (a wave's vector-memory operations
-    // complete in order, so a load issued after a store would also wait for
-    // that store)
+    // before the stores of tile row i (loads and stores share one wait
+    // counter, so waiting for a load issued after a store also waits for that
+    // store)
     u32x4_t zb[2][TN][2];
     auto zload = [&](int i, u32x4_t (&z)[TN][2]) {
 #pragma unroll
@@ -489,7 +489,6 @@ __device__ __forceinline__ void epilogue_t_impl(const GemmArgs& a, const f32x16 
 #pragma unroll
         for (int j = 0; j < TN; ++j) {
             const f32x16& v = acc[i][j];
-            const int64_t gn = col0 + 32 * j + c2;
             if constexpr (EPI == EPI_STORE_F32) {
                 uint32_t w[2][8];
 #pragma unroll
@@ -518,6 +517,7 @@ __device__ __forceinline__ void epilogue_t_impl(const GemmArgs& a, const f32x16 
                     store_f32x4<FAST>(c, a.ldc, a.M, a.N, gx + 16 * p, gf + 16, &w[p][4]);
                 }
             } else {
+                const int64_t gn = col0 + 32 * j + c2;
                 uint32_t o[2][4], h[2][4];
 #pragma unroll
                 for (int p = 0; p < 2; ++p) {
