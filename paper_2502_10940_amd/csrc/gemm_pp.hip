@@ -49,6 +49,19 @@ constexpr int NQ = 2;            // Q slots (one K tile ahead)
 // per load row.
 constexpr int kPPBK = 64;
 
+// Byte offset of the ring slot of K tile i (i >= 0) among N slots of BYTES.
+// It passes through an empty asm statement and a mask, so the compiler
+// neither turns it into a running difference across iterations nor loses
+// that it is small and non-negative: the constant parts of the fragment
+// addresses then fold into the LDS instructions' offset fields instead of
+// one VALU add per read.
+template <int N, int BYTES>
+__device__ __forceinline__ uint32_t slot_off(int i) {
+    uint32_t o = ((uint32_t)i % (uint32_t)N) * (uint32_t)BYTES;
+    asm volatile("" : "+s"(o));
+    return o & 0x3ffffu;
+}
+
 // LDS of one workgroup: NP P slots and NQ Q slots.
 template <int PL, int QL, int BK>
 constexpr int pp_smem_bytes() {
@@ -200,7 +213,7 @@ __device__ __forceinline__ void pp_one_tile(const GemmArgs& a, int64_t b, char* 
     // before b(2j+2).
     if (grp == 1) barrier_lds();
     for (int j = 0; j < nk; ++j) {
-        read_tile(pring + (j % NP) * TP::BYTES, qring + (j % NQ) * TQ::BYTES);
+        read_tile(pring + slot_off<NP, TP::BYTES>(j), qring + slot_off<NQ, TQ::BYTES>(j));
         if (grp == 0) {
             if (j + 1 < nk) issue_q(j + 1);
         } else {
@@ -433,8 +446,8 @@ __global__ __launch_bounds__(NTHR, 1) void gemm_pp_persist_kernel(GemmArgs a) {
     f32x16 acc[TM][TN];
     bf16x8 fa[NSUB][TM], fb[NSUB][TN];
     auto read_tile = [&](int g) {
-        const char* ps = pring + (g % NP) * TP::BYTES;
-        const char* qs = qring + (g % NQ) * TQ::BYTES;
+        const char* ps = pring + slot_off<NP, TP::BYTES>(g);
+        const char* qs = qring + slot_off<NQ, TQ::BYTES>(g);
 #pragma unroll
         for (int s = 0; s < NSUB; ++s) {
 #pragma unroll
