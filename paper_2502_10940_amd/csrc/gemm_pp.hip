@@ -62,6 +62,21 @@ __device__ __forceinline__ uint32_t slot_off(int i) {
     return o & 0x3ffffu;
 }
 
+// n / d for n, d < 2^21: one multiply by the hardware reciprocal (1 ulp) and
+// a correction of at most one either way.  The product is within 1/2 of
+// n / d (relative error below 1.5 * 2^-23, n / d < 2^21), so its truncation
+// is off by at most one.
+__device__ __forceinline__ int64_t fdiv21(int64_t n, int64_t d) {
+    const uint32_t un = (uint32_t)n, ud = (uint32_t)d;
+    uint32_t q = (uint32_t)((float)un * __builtin_amdgcn_rcpf((float)ud));
+    const int32_t r = (int32_t)(un - q * ud);
+    if (r < 0) --q;
+    else if ((uint32_t)r >= ud) ++q;
+    // the operands are wave-uniform: keep the quotient (and the tile
+    // coordinates made from it) in scalar registers
+    return (int64_t)(uint32_t)__builtin_amdgcn_readfirstlane((int)q);
+}
+
 // LDS of one workgroup: NP P slots and NQ Q slots.
 template <int PL, int QL, int BK>
 constexpr int pp_smem_bytes() {
@@ -93,10 +108,14 @@ __device__ __forceinline__ void pp_one_tile(const GemmArgs& a, int64_t b, char* 
     const int64_t tiles_n = (a.N + BN - 1) / BN;
     const int64_t tiles_m = (a.M + BM - 1) / BM;
     const int64_t per_split = tiles_m * tiles_n;
-    const int split = (int)(b / per_split);
+    // below 2^21 tiles the reciprocal division (a few instructions instead of
+    // a 64-bit division before the first load)
+    const bool fast = per_split * a.splits < (int64_t(1) << 21);
+    const int split = (int)(fast ? fdiv21(b, per_split) : b / per_split);
     const int64_t rem = b - (int64_t)split * per_split;
-    const int64_t m0 = (rem / tiles_n) * BM;
-    const int64_t n0 = (rem % tiles_n) * BN;
+    const int64_t tm = fast ? fdiv21(rem, tiles_n) : rem / tiles_n;
+    const int64_t m0 = tm * BM;
+    const int64_t n0 = (rem - tm * tiles_n) * BN;
     const int64_t kbeg = (int64_t)split * a.k_chunk;
     const int64_t kend = min(a.K, kbeg + a.k_chunk);
     const int nk = (int)((kend - kbeg) / BK);     // whole K tiles
@@ -292,20 +311,6 @@ struct PPTile {
 // the band's rows stream, instead of every row of tiles pulling all of Q.
 constexpr int64_t kBand = 8;
 
-// n / d for n, d < 2^21: one multiply by the hardware reciprocal (1 ulp) and
-// a correction of at most one either way.  The product is within 1/2 of
-// n / d (relative error below 1.5 * 2^-23, n / d < 2^21), so its truncation
-// is off by at most one.
-__device__ __forceinline__ int64_t fdiv21(int64_t n, int64_t d) {
-    const uint32_t un = (uint32_t)n, ud = (uint32_t)d;
-    uint32_t q = (uint32_t)((float)un * __builtin_amdgcn_rcpf((float)ud));
-    const int32_t r = (int32_t)(un - q * ud);
-    if (r < 0) --q;
-    else if ((uint32_t)r >= ud) ++q;
-    // the operands are wave-uniform: keep the quotient (and the tile
-    // coordinates made from it) in scalar registers
-    return (int64_t)(uint32_t)__builtin_amdgcn_readfirstlane((int)q);
-}
 
 // Output tile i (0, 1, ...) of this workgroup; false past the last one.  With
 // a grid and a tile count that are multiples of 8, XCD x (blockIdx % 8) owns
