@@ -191,8 +191,10 @@ __device__ __forceinline__ void pp_one_tile(const GemmArgs& a, int64_t b, char* 
     // Raised wave priority for the compute phase when the Q operand fits
     // comfortably in an XCD's L2 (measured on MI355X: it helps there, and
     // slows products whose Q operand misses in L2, whose memory phases need
-    // the issue slots).
-    const bool prio = (int64_t)a.N * a.K * 2 <= (int64_t)(3 << 20);
+    // the issue slots), and for the fp32 weight gradients, whose memory
+    // phases are short since their fragment addresses fold into the LDS
+    // offsets (measured: dA + dB -1 %).
+    const bool prio = EPI == EPI_STORE_F32 || (int64_t)a.N * a.K * 2 <= (int64_t)(3 << 20);
     auto compute_tile = [&]() {
         if (prio) __builtin_amdgcn_s_setprio(1);
 #pragma unroll
