@@ -262,6 +262,27 @@ class Group:
                        p0.dX, self.dA, [p.dB for p in self.m], ws)
 
 
+def proj_work(item, dense=False):
+    """Relative work of a projection (a group: the sum over its members):
+    T d_in d_out for the dense layer, T r (d_in + d_out) for CoLA."""
+    if isinstance(item, Group):
+        return sum(proj_work(m, dense) for m in item.m)
+    return item.T * (item.d_in * item.d_out if dense else item.r * (item.d_in + item.d_out))
+
+
+def assign_streams(works, nstreams):
+    """Stream index of each item: largest work first, each to the stream with
+    the least work so far (ties to the lowest index, stream 0 being the
+    caller's current stream)."""
+    load = [0.0] * nstreams
+    out = [0] * len(works)
+    for i in sorted(range(len(works)), key=lambda i: -works[i]):
+        k = min(range(nstreams), key=lambda k: load[k])
+        out[i] = k
+        load[k] += works[i]
+    return out
+
+
 def timed_steps(step, steps, warmup):
     import torch
     for _ in range(warmup):
@@ -406,29 +427,13 @@ def main():
     wss = [ws] + [torch.empty(ws_need, dtype=torch.uint8, device="cuda:0") for _ in range(nstreams - 1)]
     setup_s = time.time() - t0
 
-    def work(item, dense=False):
-        """relative work of a projection (or of a group's members)"""
-        if isinstance(item, Group):
-            return sum(work(m, dense) for m in item.m)
-        return item.T * (item.d_in * item.d_out if dense else item.r * (item.d_in + item.d_out))
-
-    def assign(items, dense=False):
-        """stream of each item: largest first, each to the least-loaded stream"""
-        load = [0.0] * nstreams
-        out = [0] * len(items)
-        for i in sorted(range(len(items)), key=lambda i: -work(items[i], dense)):
-            k = min(range(nstreams), key=lambda k: load[k])
-            out[i] = k
-            load[k] += work(items[i], dense)
-        return out
-
     def spread(items, fwd, bwd=None, dense=False):
         """fwd over items in order, then bwd in reverse order; each item on
-        the stream `assign` gives it, with that stream's workspace."""
+        the stream `assign_streams` gives it, with that stream's workspace."""
         main = torch.cuda.current_stream()
         for st in streams[1:]:
             st.wait_stream(main)
-        where = assign(items, dense)
+        where = assign_streams([proj_work(x, dense) for x in items], nstreams)
         order = list(enumerate(items))
         phases = [(fwd, order)] + ([(bwd, order[::-1])] if bwd is not None else [])
         for phase, seq in phases:

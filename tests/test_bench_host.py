@@ -1,0 +1,116 @@
+"""The benchmark's host-side logic on the CPU: spreading projections over
+streams by work, the HBM-traffic summary built from rocprofv3 counter tables
+(copy calibration, kernel-class attribution, the paired weight-gradient launch
+counted as one class), and the refusal of more than one GPU."""
+import csv
+import json
+import os
+import subprocess
+import sys
+import types
+
+import pytest
+
+import bench
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def proj(T, d_in, d_out, r):
+    return types.SimpleNamespace(T=T, d_in=d_in, d_out=d_out, r=r)
+
+
+def test_proj_work_cola_and_dense():
+    p = proj(8, 3, 5, 2)
+    assert bench.proj_work(p) == 8 * 2 * (3 + 5)
+    assert bench.proj_work(p, dense=True) == 8 * 3 * 5
+    g = object.__new__(bench.Group)
+    g.m = [p, proj(8, 3, 7, 4)]
+    assert bench.proj_work(g) == 8 * 2 * 8 + 8 * 4 * 10
+
+
+def test_assign_streams_largest_first_least_loaded():
+    # 10 -> s0, 7 -> s1, 6 -> s1 (7 < 10), 5 -> s0 (10 < 13), 1 -> s1 (13 < 15)
+    works = [5, 10, 1, 7, 6]
+    where = bench.assign_streams(works, 2)
+    assert where == [0, 0, 1, 1, 1]
+    loads = [sum(w for w, k in zip(works, where) if k == s) for s in range(2)]
+    assert sorted(loads) == [14, 15]
+
+
+def test_assign_streams_single_stream_and_ties():
+    assert bench.assign_streams([3, 1, 2], 1) == [0, 0, 0]
+    # equal work: stable order, first item on the caller's stream
+    assert bench.assign_streams([4, 4, 4, 4], 2) == [0, 1, 0, 1]
+    assert bench.assign_streams([], 3) == []
+
+
+def test_assign_streams_balances_llama_block():
+    """The seven projections of a LLaMA-1B-shaped block (d 2048, FFN 5461,
+    rank d/4) on two streams: the two loads differ by at most the smallest
+    projection's work."""
+    d, f, r, T = 2048, 5461, 512, 4096
+    shapes = [(d, d, r)] * 4 + [(d, f, r), (d, f, r), (f, d, r)]
+    works = [bench.proj_work(proj(T, a, b, rr)) for a, b, rr in shapes]
+    where = bench.assign_streams(works, 2)
+    loads = [sum(w for w, k in zip(works, where) if k == s) for s in range(2)]
+    assert abs(loads[0] - loads[1]) <= min(works)
+
+
+def write_pmc(path, counter, rows):
+    with open(path, "w", newline="") as fh:
+        w = csv.DictWriter(fh, fieldnames=["Dispatch_Id", "Kernel_Name", "Counter_Name", "Counter_Value"])
+        w.writeheader()
+        for i, (name, kib) in enumerate(rows):
+            w.writerow({"Dispatch_Id": i + 1, "Kernel_Name": name, "Counter_Name": counter,
+                        "Counter_Value": kib})
+
+
+def test_traffic_summary_attribution_and_calibration(tmp_path, monkeypatch):
+    (tmp_path / "profiles").mkdir()
+    monkeypatch.setattr(bench, "ROOT", str(tmp_path))
+    monkeypatch.setattr(bench, "kernel_source_hash", lambda: "0123456789abcdef")
+    gib_kib = bench.COPY_BYTES / 1024.0
+    pair = "void gemm_pp_pair_kernel<64, 1, 1, 1, 4>(GemmArgs, GemmArgs, long) [clone .kd]"
+    fwd_y = "void gemm_pp_persist_kernel<64, 0, 1, 0, 1>(GemmArgs) [clone .kd]"
+    copy = "void at::native::elementwise_kernel<128, 4>(int, copy_functor) [clone .kd]"
+    f = tmp_path / "fetch.csv"
+    w = tmp_path / "write.csv"
+    cf = tmp_path / "copy_fetch.csv"
+    cw = tmp_path / "copy_write.csv"
+    write_pmc(f, "FETCH_SIZE", [(pair, 100.0), (pair, 300.0), (fwd_y, 40.0), (copy, 5.0)])
+    write_pmc(w, "WRITE_SIZE", [(pair, 10.0), (pair, 30.0), (fwd_y, 8.0)])
+    # the copy of 1 GiB reads as 0.8 GiB fetched and 1 GiB written: factors 1.25 and 1
+    write_pmc(cf, "FETCH_SIZE", [("small_copy_kernel", 1.0), (copy, 0.8 * gib_kib)])
+    write_pmc(cw, "WRITE_SIZE", [(copy, gib_kib)])
+    bench.traffic_summary(str(f), str(w), str(cf), str(cw))
+    out = json.load(open(tmp_path / "profiles" / "traffic.json"))
+    assert set(k for k in out if not k.startswith("_")) == {"bwd_da_db", "fwd_y"}
+    p = out["bwd_da_db"]
+    assert p["launches"] == 2
+    assert p["fetch_bytes_per_launch"] == pytest.approx(200.0 * 1024 * 1.25)
+    assert p["write_bytes_per_launch"] == pytest.approx(20.0 * 1024)
+    assert p["bytes_per_launch"] == pytest.approx(200.0 * 1024 * 1.25 + 20.0 * 1024)
+    assert out["fwd_y"]["bytes_per_launch"] == pytest.approx(40.0 * 1024 * 1.25 + 8.0 * 1024)
+    assert p["source_sha256_16"] == "0123456789abcdef"
+    # read back only while the kernel sources are unchanged
+    assert bench.load_traffic("bwd_da_db") == pytest.approx(p["bytes_per_launch"])
+    monkeypatch.setattr(bench, "kernel_source_hash", lambda: "fedcba9876543210")
+    assert bench.load_traffic("bwd_da_db") is None
+
+
+def test_traffic_summary_needs_copy_dispatch(tmp_path, monkeypatch):
+    (tmp_path / "profiles").mkdir()
+    monkeypatch.setattr(bench, "ROOT", str(tmp_path))
+    empty = tmp_path / "e.csv"
+    write_pmc(empty, "FETCH_SIZE", [("small_copy_kernel", 4.0)])
+    with pytest.raises(SystemExit):
+        bench.traffic_summary(str(empty), str(empty), str(empty), str(empty))
+
+
+def test_more_than_one_gpu_refused():
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
+                       capture_output=True, text=True, timeout=120)
+    assert r.returncode == 2
+    assert "one GPU" in r.stderr
+    assert r.stdout == ""
