@@ -192,3 +192,41 @@ def test_identity_cola_equals_dense_with_merged_weight():
     cola.dense_fwd(d, run.X, W, Yd)
     torch.cuda.synchronize()
     assert relerr(to_f64(run.Y), to_f64(Yd)) <= 1e-5
+
+
+CHILD = r"""
+import sys, numpy as np
+sys.path[:0] = [sys.argv[1], sys.argv[2]]
+from paper_2502_10940_amd import inputs as I
+from layer_runner import LayerRun
+T, d_in, d_out, r = 1000, 768, 1376, 192
+ins = I.layer_inputs(160, 0, d_in, d_out, r, T, "bf16")
+out = LayerRun(ins, T, d_in, d_out, r, "bf16", "silu", False).run().outputs()
+np.savez(sys.argv[3], **out)
+print("child done", flush=True)
+"""
+
+
+def test_weight_gradients_unpaired_switch(tmp_path):
+    """COLA_WGRAD_PAIR=0 (read once per process) launches dA and dB one by one
+    instead of in one launch: both paths match the oracle and each other."""
+    import os
+    import subprocess
+    import sys
+    T, d_in, d_out, r = 1000, 768, 1376, 192
+    ins = I.layer_inputs(160, 0, d_in, d_out, r, T, "bf16")
+    ref = oracle_all(ins, "silu")
+    paired = LayerRun(ins, T, d_in, d_out, r, "bf16", "silu", False).run().outputs()
+    check(paired, ref, "bf16", "paired")
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    dst = str(tmp_path / "unpaired.npz")
+    env = dict(os.environ, COLA_WGRAD_PAIR="0")
+    res = subprocess.run([sys.executable, "-u", "-c", CHILD, root, os.path.join(root, "tests"), dst],
+                         env=env, capture_output=True, text=True, timeout=240)
+    assert res.returncode == 0, res.stdout[-2000:] + res.stderr[-2000:]
+    unpaired = dict(np.load(dst))
+    check(unpaired, ref, "bf16", "unpaired")
+    for k in ("dA", "dB"):
+        assert relerr(unpaired[k], paired[k]) <= 1e-5, k
+    for k in ("Z", "H", "Y", "dX"):
+        assert np.array_equal(unpaired[k], paired[k]), k
