@@ -230,3 +230,44 @@ def test_weight_gradients_unpaired_switch(tmp_path):
         assert relerr(unpaired[k], paired[k]) <= 1e-5, k
     for k in ("Z", "H", "Y", "dX"):
         assert np.array_equal(unpaired[k], paired[k]), k
+
+
+FAMILY_CHILD = r"""
+import sys, numpy as np
+sys.path[:0] = [sys.argv[1], sys.argv[2]]
+import test_gpu_parity as P
+from layer_runner import LayerRun
+for case in map(int, sys.argv[4].split(",")):
+    name, T, d_in, d_out, r, dtype, act = P.CASES[case]
+    ins = P.gen(case, T, d_in, d_out, r, dtype)
+    for rc in (False, True):
+        out = LayerRun(ins, T, d_in, d_out, r, dtype, act, rc).run().outputs()
+        np.savez(f"{sys.argv[3]}_{case}_{int(rc)}.npz", **out)
+    print("child done", name, flush=True)
+"""
+
+
+@pytest.mark.parametrize("family", ["big", "wide", "reg", "stream"])
+def test_forced_gemm_family(family, tmp_path):
+    """COLA_GEMM_FAMILY (read once per process) forces every bf16 product onto
+    one kernel family (the 256 x 256 ones only where both output dimensions
+    exceed 128): each family against the oracle on ragged tiles, unaligned
+    output rows and an odd rank above 128, CoLA and CoLA-M."""
+    import os
+    import subprocess
+    import sys
+    names = ("tiles_ragged_bf16", "odd_width_rank136_bf16", "odd_rank137_bf16")
+    cases = [i for i, c in enumerate(CASES) if c[0] in names]
+    assert len(cases) == len(names)
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    dst = str(tmp_path / family)
+    env = dict(os.environ, COLA_GEMM_FAMILY=family)
+    res = subprocess.run([sys.executable, "-u", "-c", FAMILY_CHILD, root, os.path.join(root, "tests"), dst,
+                          ",".join(map(str, cases))], env=env, capture_output=True, text=True, timeout=240)
+    assert res.returncode == 0, res.stdout[-2000:] + res.stderr[-2000:]
+    for case in cases:
+        name, T, d_in, d_out, r, dtype, act = CASES[case]
+        ref = oracle_all(gen(case, T, d_in, d_out, r, dtype), act)
+        for rc in (0, 1):
+            got = dict(np.load(f"{dst}_{case}_{rc}.npz"))
+            check(got, ref, dtype, f"{family}/{name}/recompute={rc}")
