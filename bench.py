@@ -140,7 +140,13 @@ def algo_flops_cola(T, d_in, d_out, r):
     return 6.0 * T * r * (d_in + d_out)
 
 
+def algo_flops_cola_fwd(T, d_in, d_out, r):
+    """forward only (inference): the two GEMMs of Eq. main-fwd, 2 T r d each."""
+    return 2.0 * T * r * (d_in + d_out)
+
+
 def algo_flops_dense(T, d_in, d_out):
+    """fwd + bwd of one dense layer: 3 GEMMs of 2 T d_in d_out each."""
     return 6.0 * T * d_in * d_out
 
 
@@ -552,7 +558,7 @@ def main():
             out["fused_block"]["speedup_vs_dense"] = round(res["dense"] / res["fused"], 3)
     if "infer" in res:
         # forward only, nothing kept for a backward pass; grouped as fused_block
-        fl = sum(2.0 * T * r * (p.d_in + p.d_out) for p in projs)
+        fl = sum(algo_flops_cola_fwd(T, p.d_in, p.d_out, r) for p in projs)
         out["inference"] = {"ms_per_step": round(res["infer"], 4),
                             "tflops": round(fl / (res["infer"] * 1e9), 2),
                             "tokens_per_s": round(T / (res["infer"] / 1e3), 1)}

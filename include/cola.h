@@ -58,7 +58,7 @@
 extern "C" {
 #endif
 
-#define COLA_ABI_VERSION 1
+#define COLA_ABI_VERSION 2
 
 /* A hipStream_t, kept opaque so this header needs no HIP headers. */
 typedef void* cola_stream_t;
@@ -247,6 +247,23 @@ int dense_fwd(const dense_desc* desc, const void* X, const void* W, void* Y,
               void* ws, size_t ws_bytes, cola_stream_t stream);
 int dense_bwd(const dense_desc* desc, const void* dY, const void* X, const void* W,
               void* dX, float* dW, void* ws, size_t ws_bytes, cola_stream_t stream);
+
+/* Tuning options, process-wide (every GPU and thread of the process), read
+ * at each call; for tuning, comparisons and tests, not needed for correct
+ * results.  Every setting gives results within the stated tolerances;
+ * settings differ at most in the last bits of fp32 sums.
+ *   COLA_OPT_STREAM_ONLY (default 0): 1 sends every bf16 product to the
+ *     streaming kernel family (BM x 128 tiles) instead of the 256 x 256
+ *     ping-pong family.
+ *   COLA_OPT_WGRAD_PAIR (default 1): 0 launches the two weight gradients of a
+ *     layer (and of a group) one by one instead of in one launch.
+ * Workspace sizes depend on the settings: size the workspace after setting
+ * them (a call whose workspace is too small returns COLA_ERR_WORKSPACE).
+ * cola_set_option returns COLA_ERR_INVALID_ARG for an unknown option or a
+ * value other than 0 or 1; cola_get_option returns the value, or -1. */
+typedef enum { COLA_OPT_STREAM_ONLY = 0, COLA_OPT_WGRAD_PAIR = 1 } cola_option;
+int cola_set_option(int option, int value);
+int cola_get_option(int option);
 
 /* Kernel timing (profiling aid).  While enabled, every kernel the library
  * launches is bracketed by two HIP events on its stream; reading sums the

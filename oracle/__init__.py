@@ -14,7 +14,7 @@ import os
 
 import numpy as np
 
-from .build import LIB, build
+from .build import LIB, SRC, build
 
 _lib = None
 _D = ctypes.POINTER(ctypes.c_double)
@@ -27,7 +27,8 @@ def _load(path=None):
         return _lib
     if path is None:
         path = LIB
-        if not os.path.exists(path):
+        # (re)build when missing or older than its source
+        if not os.path.exists(path) or os.path.getmtime(path) < os.path.getmtime(SRC):
             build()
     lib = ctypes.CDLL(path)
     i64, d, c_int = _I64, _D, ctypes.c_int
@@ -53,6 +54,8 @@ def _load(path=None):
     lib.oracle_cola_wgrad_cols.argtypes = [i64, i64, i64, i64, c_int, d, d, d, d,
                                            i64, ctypes.POINTER(ctypes.c_int64), d, d]
     lib.oracle_cola_wgrad_cols.restype = c_int
+    lib.oracle_dense_rows.argtypes = [i64, i64, i64, d, d, d, i64, ctypes.POINTER(ctypes.c_int64), d, d]
+    lib.oracle_dense_wgrad_rows.argtypes = [i64, i64, i64, d, d, i64, ctypes.POINTER(ctypes.c_int64), d]
     _lib = lib
     return lib
 
@@ -223,3 +226,34 @@ def cola_wgrad_cols(X, A, B, dY, cols, act="silu"):
     if rc != 0:
         raise MemoryError("oracle could not allocate its token columns")
     return dA, dB
+
+
+def dense_rows(X, W, dY, rows):
+    """Dense layer rows Y[t, :] and dX[t, :] for the selected tokens.
+    Returns (Y_rows [n][d_out], dX_rows [n][d_in])."""
+    X = _f64(X); W = _f64(W); dY = _f64(dY)
+    T, d_in = X.shape
+    d_out = W.shape[0]
+    _f64(W, (d_out, d_in)); _f64(dY, (T, d_out))
+    rows = np.ascontiguousarray(rows, dtype=np.int64)
+    if rows.size and (rows.min() < 0 or rows.max() >= T):
+        raise ValueError("row index out of range")
+    n = rows.size
+    Y = np.empty((n, d_out)); dX = np.empty((n, d_in))
+    _load().oracle_dense_rows(T, d_in, d_out, _p(X), _p(W), _p(dY), n,
+                              rows.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)), _p(Y), _p(dX))
+    return Y, dX
+
+
+def dense_wgrad_rows(X, dY, outs):
+    """Rows dW[o, :] = sum_t dY[t, o] X[t, :] for the selected output indices o."""
+    X = _f64(X); dY = _f64(dY)
+    T, d_in = X.shape
+    d_out = dY.shape[1]
+    outs = np.ascontiguousarray(outs, dtype=np.int64)
+    if outs.size and (outs.min() < 0 or outs.max() >= d_out):
+        raise ValueError("output index out of range")
+    dW = np.empty((outs.size, d_in))
+    _load().oracle_dense_wgrad_rows(T, d_in, d_out, _p(X), _p(dY), outs.size,
+                                    outs.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)), _p(dW))
+    return dW

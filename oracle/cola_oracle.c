@@ -239,6 +239,47 @@ void oracle_dense_bwd(int64_t T, int64_t d_in, int64_t d_out,
 /* sampled evaluation for shapes too large for the full oracle               */
 /* ------------------------------------------------------------------------ */
 
+/* Dense layer, per selected token t = rows[i]: the rows Y[t][:] and dX[t][:]
+ * from the definition on that token alone.  Outputs are [nrows][width]. */
+void oracle_dense_rows(int64_t T, int64_t d_in, int64_t d_out,
+                       const double* X, const double* W, const double* dY,
+                       int64_t nrows, const int64_t* rows, double* Yr, double* dXr) {
+    (void)T;
+    g_mac_count += nrows * (d_out * d_in + d_in * d_out);
+    #pragma omp parallel for schedule(dynamic)
+    for (int64_t i = 0; i < nrows; ++i) {
+        const double* x = X + rows[i] * d_in;
+        const double* dy = dY + rows[i] * d_out;
+        for (int64_t o = 0; o < d_out; ++o) {        /* Y[t][o] = sum_k X[t][k] W[o][k] */
+            double s = 0.0;
+            for (int64_t k = 0; k < d_in; ++k) s += x[k] * W[o * d_in + k];
+            Yr[i * d_out + o] = s;
+        }
+        for (int64_t k = 0; k < d_in; ++k) {         /* dX[t][k] = sum_o dY[t][o] W[o][k] */
+            double s = 0.0;
+            for (int64_t o = 0; o < d_out; ++o) s += dy[o] * W[o * d_in + k];
+            dXr[i * d_in + k] = s;
+        }
+    }
+}
+
+/* Dense weight gradient, per selected output index o = outs[i]: the row
+ * dW[o][:] = sum_t dY[t][o] X[t][:].  Output is [nouts][d_in]. */
+void oracle_dense_wgrad_rows(int64_t T, int64_t d_in, int64_t d_out,
+                             const double* X, const double* dY,
+                             int64_t nouts, const int64_t* outs, double* dWr) {
+    g_mac_count += nouts * d_in * T;
+    #pragma omp parallel for schedule(dynamic)
+    for (int64_t i = 0; i < nouts; ++i) {
+        const int64_t o = outs[i];
+        for (int64_t k = 0; k < d_in; ++k) {
+            double s = 0.0;
+            for (int64_t t = 0; t < T; ++t) s += dY[t * d_out + o] * X[t * d_in + k];
+            dWr[i * d_in + k] = s;
+        }
+    }
+}
+
 /* Per selected token t = rows[i]: Z, H, Y, dZ and dX rows, each computed from
  * the definition on that token alone (every output row of the layer depends
  * only on its own input row).  Outputs are [nrows][width]. */

@@ -19,12 +19,11 @@ LIB = os.path.join(PKG, "libcola.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 
-SOURCES = ["gemm_bf16.hip", "gemm_stream.hip", "gemm_wide.hip", "gemm_big.hip", "gemm_pp.hip", "gemm_f32.hip", "cola_abi.hip"]
+SOURCES = ["gemm_dispatch.hip", "gemm_stream.hip", "gemm_pp.hip", "gemm_f32.hip", "cola_abi.hip"]
 # Per-source extra flags.  The 256 x 256 kernel's epilogues run over 256
 # accumulators per lane: past the default limit the unroller stops and the
 # accumulators go to scratch memory.
-EXTRA = {"gemm_big.hip": ["-mllvm", "-pragma-unroll-threshold=500000"],
-         "gemm_pp.hip": ["-mllvm", "-pragma-unroll-threshold=500000"]}
+EXTRA = {"gemm_pp.hip": ["-mllvm", "-pragma-unroll-threshold=500000"]}
 FLAGS = ["-std=c++17", "-O3", "-fPIC", f"--offload-arch={ARCH}", "-I", INCLUDE, "-I", CSRC,
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
          "-Wall", "-Wno-unused-function"]

@@ -83,7 +83,11 @@ EXPORTS = {
     "cola_timing_read": ([ctypes.c_int, ctypes.POINTER(ctypes.c_int64), ctypes.POINTER(ctypes.c_double),
                           ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double)], ctypes.c_int),
     "cola_kernel_name": ([ctypes.c_int], ctypes.c_char_p),
+    "cola_set_option": ([ctypes.c_int, ctypes.c_int], ctypes.c_int),
+    "cola_get_option": ([ctypes.c_int], ctypes.c_int),
 }
+
+OPT_STREAM_ONLY, OPT_WGRAD_PAIR = 0, 1
 
 
 def lib():
@@ -113,6 +117,98 @@ def _ptr(x):
     if isinstance(x, int):
         return x
     return x.data_ptr()
+
+
+# ---------------------------------------------------------------------------
+# Host-side checks of tensors against a descriptor.  The C ABI sees only
+# pointers, so a tensor of the wrong dtype (dA allocated as bf16: the kernels
+# write fp32, twice the bytes), a non-contiguous view, or rows shorter than
+# the pitch would send the kernels outside their buffers; these checks refuse
+# such calls with ValueError before anything is enqueued.  Raw integer
+# pointers are passed through unchecked (the caller vouches for them).
+# ---------------------------------------------------------------------------
+
+def _torch_dtype(code):
+    import torch
+    return torch.bfloat16 if code == BF16 else torch.float32
+
+
+def _need(name, t, rows, width, ld, dtype):
+    """t must be a 2-D tensor of `dtype` holding `rows` rows of `width` used
+    elements with row pitch `ld` elements, its storage covering rows x ld
+    elements from its first element, on a GPU."""
+    if t is None or isinstance(t, int) or rows == 0:
+        return
+    import torch
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name}: expected a torch.Tensor or an integer device pointer")
+    if t.dtype != dtype:
+        raise ValueError(f"{name}: dtype {t.dtype}, the descriptor needs {dtype}")
+    if t.dim() != 2:
+        raise ValueError(f"{name}: expected a 2-D tensor, got shape {tuple(t.shape)}")
+    if t.shape[0] < rows or t.shape[1] < width:
+        raise ValueError(f"{name}: shape {tuple(t.shape)} is smaller than [{rows}][{width}]")
+    if t.stride(1) != 1 or (rows > 1 and t.stride(0) != ld):
+        raise ValueError(f"{name}: strides {t.stride()} do not match a row pitch of {ld} elements "
+                         "with contiguous rows")
+    avail = t.untyped_storage().nbytes() - t.storage_offset() * t.element_size()
+    if avail < rows * ld * t.element_size():
+        raise ValueError(f"{name}: storage holds {avail} bytes from the first element, "
+                         f"{rows} rows of pitch {ld} need {rows * ld * t.element_size()}")
+
+
+def _on_gpu(named):
+    """Every tensor of (name, tensor) pairs in GPU memory (checked after the
+    shapes, so that a CPU test sees the shape refusals first)."""
+    for name, t in named:
+        if t is None or isinstance(t, int):
+            continue
+        if t.device.type != "cuda":
+            raise ValueError(f"{name}: tensor is on {t.device}, the library needs GPU memory")
+
+
+def _need_ws(ws, ws_bytes):
+    if ws is None or isinstance(ws, int):
+        return
+    import torch
+    if not isinstance(ws, torch.Tensor):
+        raise TypeError("ws: expected a torch.Tensor or an integer device pointer")
+    if not ws.is_contiguous():
+        raise ValueError("ws: the workspace must be contiguous")
+    if ws_bytes > ws.numel() * ws.element_size():
+        raise ValueError(f"ws: ws_bytes {ws_bytes} exceeds the tensor's {ws.numel() * ws.element_size()} bytes")
+    _on_gpu([("ws", ws)])
+
+
+def _ws_bytes(ws, ws_bytes):
+    if ws_bytes is None:
+        ws_bytes = ws.numel() * ws.element_size() if ws is not None and not isinstance(ws, int) else 0
+    _need_ws(ws, ws_bytes)
+    return ws_bytes
+
+
+def _layer_dims(d):
+    ldx = d.ldx or d.d_in
+    ldy = d.ldy or d.d_out
+    ldz = d.ldz or d.r
+    return d.T, d.d_in, d.d_out, d.r, ldx, ldy, ldz, _torch_dtype(d.dtype)
+
+
+def _check_layer(d, **ts):
+    """Tensors of one layer call, by their names in include/cola.h."""
+    import torch
+    T, d_in, d_out, r, ldx, ldy, ldz, dt = _layer_dims(d)
+    shapes = {"X": (T, d_in, ldx, dt), "dX": (T, d_in, ldx, dt), "Y": (T, d_out, ldy, dt),
+              "dY": (T, d_out, ldy, dt), "P": (T, d_out, ldy, dt), "Z": (T, r, ldz, dt),
+              "H": (T, r, ldz, dt), "A": (r, d_in, d_in, dt), "B": (d_out, r, r, dt),
+              "dA": (r, d_in, d_in, torch.float32), "dB": (d_out, r, r, torch.float32)}
+    if d.dtype not in (F32, BF16) or min(T, d_in, d_out, r, ldx, ldy, ldz) < 0:
+        return                      # the library refuses the descriptor itself
+    for name, t in ts.items():
+        rows, width, ld, dtype = shapes[name]
+        _need(name, t, rows, width, ld, dtype)
+    if T > 0:
+        _on_gpu(ts.items())
 
 
 def _stream(stream):
@@ -149,14 +245,70 @@ def _ptr_array(xs):
     return ctypes.cast(arr, ctypes.c_void_p), arr      # keep arr alive with the cast
 
 
+def _check_group(d, X=None, A_all=None, Z_all=None, H_all=None, dX=None, dA_all=None, B=None, Y=None, dY=None,
+                 dB=None):
+    import torch
+    n = d.n
+    if not 1 <= n <= GROUP_MAX or d.dtype not in (F32, BF16) or d.T < 0:
+        return                      # the library refuses the descriptor itself
+    T, d_in = d.T, d.d_in
+    R = sum(d.r[p] for p in range(n))
+    ldx = d.ldx or d_in
+    ldz = d.ldz or R
+    dt = _torch_dtype(d.dtype)
+    _need("X", X, T, d_in, ldx, dt)
+    _need("dX", dX, T, d_in, ldx, dt)
+    _need("A_all", A_all, R, d_in, d_in, dt)
+    _need("dA_all", dA_all, R, d_in, d_in, torch.float32)
+    _need("Z_all", Z_all, T, R, ldz, dt)
+    _need("H_all", H_all, T, R, ldz, dt)
+    for key, lst in (("B", B), ("Y", Y), ("dY", dY), ("dB", dB)):
+        if lst is None:
+            continue
+        if len(lst) != n:
+            raise ValueError(f"{key}: {len(lst)} entries for {n} projections")
+        for p, t in enumerate(lst):
+            r, d_out = d.r[p], d.d_out[p]
+            ldy = d.ldy[p] or d_out
+            if key == "B":
+                _need(f"B[{p}]", t, d_out, r, r, dt)
+            elif key == "dB":
+                _need(f"dB[{p}]", t, d_out, r, r, torch.float32)
+            else:
+                _need(f"{key}[{p}]", t, T, d_out, ldy, dt)
+    if T > 0:
+        named = [("X", X), ("dX", dX), ("A_all", A_all), ("dA_all", dA_all), ("Z_all", Z_all), ("H_all", H_all)]
+        for key, lst in (("B", B), ("Y", Y), ("dY", dY), ("dB", dB)):
+            named += [(f"{key}[{p}]", t) for p, t in enumerate(lst or [])]
+        _on_gpu(named)
+
+
+def _check_dense(d, X=None, W=None, Y=None, dY=None, dX=None, dW=None):
+    import torch
+    T, d_in, d_out = d.T, d.d_in, d.d_out
+    if d.dtype not in (F32, BF16) or min(T, d_in, d_out, d.ldx, d.ldy) < 0:
+        return                      # the library refuses the descriptor itself
+    ldx = d.ldx or d_in
+    ldy = d.ldy or d_out
+    dt = _torch_dtype(d.dtype)
+    _need("X", X, T, d_in, ldx, dt)
+    _need("dX", dX, T, d_in, ldx, dt)
+    _need("Y", Y, T, d_out, ldy, dt)
+    _need("dY", dY, T, d_out, ldy, dt)
+    _need("W", W, d_out, d_in, d_in, dt)
+    _need("dW", dW, d_out, d_in, d_in, torch.float32)
+    if T > 0:
+        _on_gpu([("X", X), ("W", W), ("Y", Y), ("dY", dY), ("dX", dX), ("dW", dW)])
+
+
 def group_workspace_bytes(d: GroupDesc, phase: int) -> int:
     return int(lib().cola_group_workspace_bytes(ctypes.byref(d), phase))
 
 
 def group_fwd(d: GroupDesc, X, A_all, B, Y, Z_all, H_all, ws=None, ws_bytes=None, stream=None):
     """Z_all = X A_all^T, H_all = sigma(Z_all), Y_p = H_p B_p^T (B, Y: lists)."""
-    if ws_bytes is None:
-        ws_bytes = ws.numel() * ws.element_size() if ws is not None else 0
+    ws_bytes = _ws_bytes(ws, ws_bytes)
+    _check_group(d, X=X, A_all=A_all, Z_all=Z_all, H_all=H_all, B=B, Y=Y)
     pb, _kb = _ptr_array(B)
     py, _ky = _ptr_array(Y)
     _check(lib().cola_group_fwd(ctypes.byref(d), _ptr(X), _ptr(A_all), pb, py, _ptr(Z_all), _ptr(H_all),
@@ -165,8 +317,8 @@ def group_fwd(d: GroupDesc, X, A_all, B, Y, Z_all, H_all, ws=None, ws_bytes=None
 
 def group_infer(d: GroupDesc, X, A_all, B, Y, ws=None, ws_bytes=None, stream=None):
     """Inference forward: Y_p = sigma(X A_p^T) B_p^T, nothing kept for a backward pass."""
-    if ws_bytes is None:
-        ws_bytes = ws.numel() * ws.element_size() if ws is not None else 0
+    ws_bytes = _ws_bytes(ws, ws_bytes)
+    _check_group(d, X=X, A_all=A_all, B=B, Y=Y)
     pb, _kb = _ptr_array(B)
     py, _ky = _ptr_array(Y)
     _check(lib().cola_group_infer(ctypes.byref(d), _ptr(X), _ptr(A_all), pb, py, _ptr(ws), ws_bytes,
@@ -175,8 +327,8 @@ def group_infer(d: GroupDesc, X, A_all, B, Y, ws=None, ws_bytes=None, stream=Non
 
 def group_bwd(d: GroupDesc, dY, X, Z_all, H_all, A_all, B, dX, dA_all, dB, ws=None, ws_bytes=None, stream=None):
     """dZ_p = (dY_p B_p) * sigma'(Z_p), dX = sum_p dZ_p A_p, dA_all = dZ_all^T X, dB_p = dY_p^T H_p."""
-    if ws_bytes is None:
-        ws_bytes = ws.numel() * ws.element_size() if ws is not None else 0
+    ws_bytes = _ws_bytes(ws, ws_bytes)
+    _check_group(d, X=X, A_all=A_all, Z_all=Z_all, H_all=H_all, dX=dX, dA_all=dA_all, B=B, dY=dY, dB=dB)
     pdy, _k1 = _ptr_array(dY)
     pb, _k2 = _ptr_array(B)
     pdb, _k3 = _ptr_array(dB)
@@ -198,16 +350,16 @@ def dense_workspace_bytes(d: DenseDesc, phase: int) -> int:
 
 def fwd(d: ColaDesc, X, A, B, Y, Z, H, ws=None, ws_bytes=None, stream=None):
     """Z = X A^T, H = sigma(Z), Y = H B^T (H is None in CoLA-M mode)."""
-    if ws_bytes is None:
-        ws_bytes = ws.numel() * ws.element_size() if ws is not None else 0
+    ws_bytes = _ws_bytes(ws, ws_bytes)
+    _check_layer(d, X=X, A=A, B=B, Y=Y, Z=Z, H=H)
     _check(lib().cola_fwd(ctypes.byref(d), _ptr(X), _ptr(A), _ptr(B), _ptr(Y), _ptr(Z), _ptr(H),
                           _ptr(ws), ws_bytes, _stream(stream)))
 
 
 def fwd_outer(d: ColaDesc, outer, X, A, B, Y, P, Z, H, ws=None, ws_bytes=None, stream=None):
     """Both-sigma variant: P = H B^T, Y = sigma_out(P) (outer: a sigma name or code)."""
-    if ws_bytes is None:
-        ws_bytes = ws.numel() * ws.element_size() if ws is not None else 0
+    ws_bytes = _ws_bytes(ws, ws_bytes)
+    _check_layer(d, X=X, A=A, B=B, Y=Y, P=P, Z=Z, H=H)
     _check(lib().cola_fwd_outer(ctypes.byref(d), ACTS[outer] if isinstance(outer, str) else int(outer), _ptr(X),
                                 _ptr(A), _ptr(B), _ptr(Y), _ptr(P), _ptr(Z), _ptr(H), _ptr(ws), ws_bytes,
                                 _stream(stream)))
@@ -215,8 +367,8 @@ def fwd_outer(d: ColaDesc, outer, X, A, B, Y, P, Z, H, ws=None, ws_bytes=None, s
 
 def bwd_outer(d: ColaDesc, outer, dY, P, X, Z, H, A, B, dX, dA, dB, ws=None, ws_bytes=None, stream=None):
     """Both-sigma backward: dP = dY * sigma_out'(P), then the layer backward on dP."""
-    if ws_bytes is None:
-        ws_bytes = ws.numel() * ws.element_size() if ws is not None else 0
+    ws_bytes = _ws_bytes(ws, ws_bytes)
+    _check_layer(d, dY=dY, P=P, X=X, Z=Z, H=H, A=A, B=B, dX=dX, dA=dA, dB=dB)
     _check(lib().cola_bwd_outer(ctypes.byref(d), ACTS[outer] if isinstance(outer, str) else int(outer), _ptr(dY),
                                 _ptr(P), _ptr(X), _ptr(Z), _ptr(H), _ptr(A), _ptr(B), _ptr(dX), _ptr(dA), _ptr(dB),
                                 _ptr(ws), ws_bytes, _stream(stream)))
@@ -224,30 +376,30 @@ def bwd_outer(d: ColaDesc, outer, dY, P, X, Z, H, A, B, dX, dA, dB, ws=None, ws_
 
 def infer(d: ColaDesc, X, A, B, Y, ws=None, ws_bytes=None, stream=None):
     """Inference forward: Y = sigma(X A^T) B^T, nothing kept for a backward pass."""
-    if ws_bytes is None:
-        ws_bytes = ws.numel() * ws.element_size() if ws is not None else 0
+    ws_bytes = _ws_bytes(ws, ws_bytes)
+    _check_layer(d, X=X, A=A, B=B, Y=Y)
     _check(lib().cola_infer(ctypes.byref(d), _ptr(X), _ptr(A), _ptr(B), _ptr(Y), _ptr(ws), ws_bytes,
                             _stream(stream)))
 
 
 def bwd(d: ColaDesc, dY, X, Z, H, A, B, dX, dA, dB, ws=None, ws_bytes=None, stream=None):
     """dZ = (dY B) * sigma'(Z), dX = dZ A, dA = dZ^T X, dB = dY^T H (H None in CoLA-M)."""
-    if ws_bytes is None:
-        ws_bytes = ws.numel() * ws.element_size() if ws is not None else 0
+    ws_bytes = _ws_bytes(ws, ws_bytes)
+    _check_layer(d, dY=dY, X=X, Z=Z, H=H, A=A, B=B, dX=dX, dA=dA, dB=dB)
     _check(lib().cola_bwd(ctypes.byref(d), _ptr(dY), _ptr(X), _ptr(Z), _ptr(H), _ptr(A), _ptr(B),
                           _ptr(dX), _ptr(dA), _ptr(dB), _ptr(ws), ws_bytes, _stream(stream)))
 
 
 def dense_fwd(d: DenseDesc, X, W, Y, ws=None, ws_bytes=None, stream=None):
-    if ws_bytes is None:
-        ws_bytes = ws.numel() * ws.element_size() if ws is not None else 0
+    ws_bytes = _ws_bytes(ws, ws_bytes)
+    _check_dense(d, X=X, W=W, Y=Y)
     _check(lib().dense_fwd(ctypes.byref(d), _ptr(X), _ptr(W), _ptr(Y), _ptr(ws), ws_bytes,
                            _stream(stream)))
 
 
 def dense_bwd(d: DenseDesc, dY, X, W, dX, dW, ws=None, ws_bytes=None, stream=None):
-    if ws_bytes is None:
-        ws_bytes = ws.numel() * ws.element_size() if ws is not None else 0
+    ws_bytes = _ws_bytes(ws, ws_bytes)
+    _check_dense(d, dY=dY, X=X, W=W, dX=dX, dW=dW)
     _check(lib().dense_bwd(ctypes.byref(d), _ptr(dY), _ptr(X), _ptr(W), _ptr(dX), _ptr(dW),
                            _ptr(ws), ws_bytes, _stream(stream)))
 
@@ -273,3 +425,12 @@ def timing_read(kernel_class: int):
 
 def kernel_name(kernel_class: int) -> str:
     return lib().cola_kernel_name(kernel_class).decode()
+
+
+def set_option(option: int, value: int):
+    """Process-wide tuning option (OPT_STREAM_ONLY, OPT_WGRAD_PAIR) to 0 or 1."""
+    _check(lib().cola_set_option(int(option), int(value)))
+
+
+def get_option(option: int) -> int:
+    return int(lib().cola_get_option(int(option)))

@@ -16,7 +16,6 @@
 #include <mutex>
 #include <new>
 #include <stdio.h>
-#include <stdlib.h>
 #include <string.h>
 #include <vector>
 
@@ -202,15 +201,9 @@ Split plan_split(bool bf16, int64_t M, int64_t N, int64_t K, int tag) {
 }
 
 // The two weight gradients of a layer in one launch (bf16, both in the PP
-// family): their tiles share the slots and one split of K = T.
-// COLA_WGRAD_PAIR=0 launches them one by one (tuning, comparisons).
-bool wgrad_pairing_on() {
-    static const bool off = [] {
-        const char* e = getenv("COLA_WGRAD_PAIR");
-        return e != nullptr && e[0] == '0';
-    }();
-    return !off;
-}
+// family): their tiles share the slots and one split of K = T.  The option
+// COLA_OPT_WGRAD_PAIR = 0 launches them one by one (tuning, comparisons).
+bool wgrad_pairing_on() { return get_option(OPT_WGRAD_PAIR) == 1; }
 bool pair_wgrads(bool bf16, int64_t r, int64_t d_in, int64_t d_out) {
     return wgrad_pairing_on() && bf16 && gemm_family(r, d_in, TAG_BWD_DA) == FAM_PP &&
            gemm_family(d_out, r, TAG_BWD_DB) == FAM_PP;
@@ -524,6 +517,14 @@ OuterPlan plan_outer_bwd(const Dims& x, bool recompute) {
 extern "C" {
 
 int cola_abi_version(void) { return COLA_ABI_VERSION; }
+
+int cola_set_option(int option, int value) {
+    static_assert(COLA_OPT_STREAM_ONLY == OPT_STREAM_ONLY && COLA_OPT_WGRAD_PAIR == OPT_WGRAD_PAIR,
+                  "option numbering");
+    return set_option(option, value) == 0 ? COLA_OK : COLA_ERR_INVALID_ARG;
+}
+
+int cola_get_option(int option) { return get_option(option); }
 
 const char* cola_strerror(int status) {
     switch (status) {

@@ -303,16 +303,7 @@ struct PPTile {
     int split, nk;
 };
 
-// Output tile i (0, 1, ...) of this workgroup; false past the last one.  With
-// a grid and a tile count that are multiples of 8, XCD x (blockIdx % 8) owns
-// the contiguous tile range [x T/8, (x+1) T/8), swept by its workgroups
-// together, so tiles that share operand rows share an L2.  When that range
-// is whole rows of tiles (one split), it is swept in column bands of
-// kBand tiles (n fastest within a band, then the next row): the Q rows of a
-// band (kBand x 256 rows, 2 MB for K = 512) stay in the XCD's 4 MB L2 while
-// the band's rows stream, instead of every row of tiles pulling all of Q.
 constexpr int64_t kBand = 8;
-
 
 // Output tile i (0, 1, ...) of this workgroup; false past the last one.  With
 // a grid and a tile count that are multiples of 8, XCD x (blockIdx % 8) owns

@@ -47,15 +47,9 @@ struct GemmArgs {
 // Enqueue one GEMM.  Return hipSuccess or the launch error.
 hipError_t launch_gemm_bf16(const GemmArgs& a, hipStream_t s);
 // The kernel families behind launch_gemm_bf16:
-//   REG    -- BM x 128 tiles, register-staged loads, two workgroups per CU
 //   STREAM -- BM x 128 tiles, direct-to-LDS loads, three K stages, two per CU
-//   WIDE   -- 256 x 256 tiles, direct-to-LDS loads, one persistent workgroup per CU
-hipError_t launch_gemm_reg(const GemmArgs& a, hipStream_t s);
-hipError_t launch_gemm_stream(const GemmArgs& a, hipStream_t s);
-hipError_t launch_gemm_wide(const GemmArgs& a, hipStream_t s);
-//   BIG    -- 256 x 256 tiles, one wave per SIMD, software-pipelined K loop
 //   PP     -- 256 x 256 tiles, two wave groups per workgroup in ping-pong
-hipError_t launch_gemm_big(const GemmArgs& a, hipStream_t s);
+hipError_t launch_gemm_stream(const GemmArgs& a, hipStream_t s);
 hipError_t launch_gemm_pp(const GemmArgs& a, hipStream_t s);
 // Two weight-gradient products (both operands m-contiguous, fp32 output) in
 // one PP grid: a0's tiles and splits, then a1's.  Operands as for PP.
@@ -64,11 +58,20 @@ hipError_t launch_gemm_pp_pair(const GemmArgs& a0, const GemmArgs& a1, hipStream
 // takes (else one launch each, as launch_gemm_bf16).
 hipError_t launch_gemm_bf16_pair(const GemmArgs& a0, const GemmArgs& a1, hipStream_t s);
 
-enum Family : int { FAM_REG = 0, FAM_STREAM = 1, FAM_WIDE = 2, FAM_BIG = 3, FAM_PP = 4 };
-// Family used for a GEMM (also used by the split planner).  The environment
-// variable COLA_GEMM_FAMILY (reg | stream | wide | big | pp) overrides the
-// default, for tuning and comparisons.
+enum Family : int { FAM_STREAM = 1, FAM_PP = 4 };
+// Family used for a GEMM (also used by the split planner): PP where both
+// output dimensions exceed 128, else STREAM; the option OPT_STREAM_ONLY
+// sends every product to STREAM.
 int gemm_family(int64_t M, int64_t N, int tag);
+
+// Process-wide tuning options (the public cola_set_option): the values of
+// cola_option in include/cola.h.  set_option returns 0, or -1 for an unknown
+// option or a value other than 0 / 1.
+enum Option : int { OPT_STREAM_ONLY = 0, OPT_WGRAD_PAIR = 1 };
+int set_option(int option, int value);
+int get_option(int option);
+
+// fp32 storage: the VALU GEMM of gemm_f32.hip (true fp32 FMAs).
 hipError_t launch_gemm_f32(const GemmArgs& a, hipStream_t s);
 
 // out[i] = sum_{s < splits} part[s * stride + i], s in increasing order (fp32).
@@ -95,13 +98,12 @@ constexpr int BF16_BK = 64;
 // K tile of the fp32 kernel.
 constexpr int F32_BK = 16;
 
-// Tile geometry of the launchers (mirrored here for planning): the WIDE, BIG
-// and PP families use 256 x 256 (only when M > 128 and N > 128), the others BM x 128
-// with BM = 256 (128 when M <= 128); fp32 uses 64 x 64.
+// Tile geometry of the launchers (mirrored here for planning): the PP family
+// uses 256 x 256 (only when M > 128 and N > 128), STREAM BM x 128 with
+// BM = 256 (128 when M <= 128); fp32 uses 64 x 64.
 inline bool bf16_wide_ok(int64_t M, int64_t N) { return M > 128 && N > 128; }
 inline int64_t gemm_tiles(bool bf16, int64_t M, int64_t N, int tag) {
-    const int fam = bf16 ? gemm_family(M, N, tag) : -1;
-    const bool wide = fam == FAM_WIDE || fam == FAM_BIG || fam == FAM_PP;
+    const bool wide = bf16 && gemm_family(M, N, tag) == FAM_PP;
     const int64_t tm = bf16 ? (M > 128 ? 256 : 128) : 64;
     const int64_t tn = bf16 ? (wide ? 256 : 128) : 64;
     return ((M + tm - 1) / tm) * ((N + tn - 1) / tn);
@@ -109,8 +111,7 @@ inline int64_t gemm_tiles(bool bf16, int64_t M, int64_t N, int tag) {
 // Workgroups the chip holds at once (256 CUs).
 inline int64_t gemm_slots(bool bf16, int64_t M, int64_t N, int tag) {
     if (!bf16) return 1024;
-    const int fam = gemm_family(M, N, tag);
-    return fam == FAM_WIDE || fam == FAM_BIG || fam == FAM_PP ? 256 : 512;
+    return gemm_family(M, N, tag) == FAM_PP ? 256 : 512;
 }
 
 }  // namespace cola

@@ -28,7 +28,8 @@ def test_header_declares_expected_calls():
               "dense_fwd", "dense_bwd", "dense_workspace_bytes", "cola_timing_enable",
               "cola_timing_read", "cola_timing_reset", "cola_kernel_name",
               "cola_group_fwd", "cola_group_bwd", "cola_group_workspace_bytes", "cola_infer",
-              "cola_group_infer", "cola_fwd_outer", "cola_bwd_outer"):
+              "cola_group_infer", "cola_fwd_outer", "cola_bwd_outer", "cola_set_option",
+              "cola_get_option"):
         assert n in names
 
 
@@ -46,7 +47,7 @@ def test_library_exports_every_declared_symbol():
 
 def test_abi_version_and_strerror():
     L = cola.lib()
-    assert L.cola_abi_version() == 1
+    assert L.cola_abi_version() == 2
     for s in range(6):
         assert L.cola_strerror(s)
     assert L.cola_strerror(99) == b"unknown status"
@@ -336,3 +337,104 @@ def test_outer_checks():
     e = cola.desc(0, 32, 48, 8)
     assert cola.workspace_bytes(e, 3) == 0
     assert fwd_outer_status(e, X=None, A=None, B=None, Y=None, P=None, Z=None) == cola.OK
+
+
+# --------------------------------------------------------------------------
+# the binding refuses tensors that do not match the descriptor before the
+# library sees a pointer (CPU: every check but the device one runs first, so
+# a well-formed CPU tensor is refused only for being on the CPU)
+# --------------------------------------------------------------------------
+
+def _layer_tensors(T=64, d_in=32, d_out=24, r=8, dt=None):
+    import torch
+    dt = dt or torch.bfloat16
+    return dict(X=torch.zeros(T, d_in, dtype=dt), A=torch.zeros(r, d_in, dtype=dt),
+                B=torch.zeros(d_out, r, dtype=dt), Y=torch.zeros(T, d_out, dtype=dt),
+                Z=torch.zeros(T, r, dtype=dt), H=torch.zeros(T, r, dtype=dt),
+                dY=torch.zeros(T, d_out, dtype=dt), dX=torch.zeros(T, d_in, dtype=dt),
+                dA=torch.zeros(r, d_in, dtype=torch.float32), dB=torch.zeros(d_out, r, dtype=torch.float32))
+
+
+def _refused(match, fn, *args, **kw):
+    with pytest.raises(ValueError, match=match):
+        fn(*args, **kw)
+
+
+def test_binding_refuses_mismatched_tensors():
+    import torch
+    d = cola.desc(64, 32, 24, 8, "bf16", "silu", False)
+    t = _layer_tensors()
+    bwd_args = lambda **o: [o.get(k, t[k]) for k in ("dY", "X", "Z", "H", "A", "B", "dX", "dA", "dB")]
+    # dA allocated in bf16: the kernels write fp32
+    _refused("dA: dtype", cola.bwd, d, *bwd_args(dA=torch.zeros(8, 32, dtype=torch.bfloat16)))
+    # fp32 activations under a bf16 descriptor
+    _refused("X: dtype", cola.fwd, d, torch.zeros(64, 32), t["A"], t["B"], t["Y"], t["Z"], t["H"])
+    # too few rows, too narrow, 1-D
+    _refused("Y: shape", cola.fwd, d, t["X"], t["A"], t["B"], torch.zeros(63, 24, dtype=torch.bfloat16),
+             t["Z"], t["H"])
+    _refused("B: shape", cola.fwd, d, t["X"], t["A"], torch.zeros(24, 7, dtype=torch.bfloat16), t["Y"],
+             t["Z"], t["H"])
+    _refused("Z: expected a 2-D", cola.fwd, d, t["X"], t["A"], t["B"], t["Y"],
+             torch.zeros(64 * 8, dtype=torch.bfloat16), t["H"])
+    # a non-contiguous view (a transposed weight) and a strided column slice
+    _refused("A: strides", cola.fwd, d, t["X"], torch.zeros(32, 8, dtype=torch.bfloat16).t(), t["B"], t["Y"],
+             t["Z"], t["H"])
+    _refused("X: strides", cola.fwd, d, torch.zeros(64, 40, dtype=torch.bfloat16)[:, :32], t["A"], t["B"],
+             t["Y"], t["Z"], t["H"])
+    # a padded pitch that the tensor's storage does not cover
+    dp = cola.desc(64, 32, 24, 8, "bf16", "silu", False, ldx=40)
+    _refused("X: storage", cola.fwd, dp, torch.zeros(64 * 40 - 8, dtype=torch.bfloat16)[: 63 * 40 + 32]
+             .as_strided((64, 32), (40, 1)), t["A"], t["B"], t["Y"], t["Z"], t["H"])
+    # the same padded view, with storage for all 64 x 40 elements, passes every check but the device
+    x = torch.zeros(64, 40, dtype=torch.bfloat16)[:, :32]
+    _refused("X: tensor is on cpu", cola.fwd, dp, x, t["A"], t["B"], t["Y"], t["Z"], t["H"])
+    # workspace: more bytes claimed than the tensor holds
+    _refused("ws: ws_bytes", cola.fwd, d, t["X"], t["A"], t["B"], t["Y"], t["Z"], t["H"],
+             ws=torch.zeros(16, dtype=torch.uint8), ws_bytes=17)
+    # fp32 descriptor: dB must still be fp32, activations fp32
+    d32 = cola.desc(64, 32, 24, 8, "f32", "silu", False)
+    t32 = _layer_tensors(dt=torch.float32)
+    _refused("dY: tensor is on cpu", cola.bwd, d32, *[t32[k] for k in ("dY", "X", "Z", "H", "A", "B", "dX", "dA",
+                                                                        "dB")])
+
+
+def test_binding_refuses_mismatched_group_and_dense_tensors():
+    import torch
+    bf = torch.bfloat16
+    g = cola.group_desc(64, 32, [8, 16], [24, 40])
+    X = torch.zeros(64, 32, dtype=bf)
+    A_all = torch.zeros(24, 32, dtype=bf)
+    B = [torch.zeros(24, 8, dtype=bf), torch.zeros(40, 16, dtype=bf)]
+    Y = [torch.zeros(64, 24, dtype=bf), torch.zeros(64, 40, dtype=bf)]
+    Z = torch.zeros(64, 24, dtype=bf)
+    _refused("B\\[1\\]: shape", cola.group_fwd, g, X, A_all, [B[0], torch.zeros(40, 8, dtype=bf)], Y, Z, Z)
+    _refused("Y: 1 entries", cola.group_fwd, g, X, A_all, B, Y[:1], Z, Z)
+    _refused("A_all: shape", cola.group_fwd, g, X, torch.zeros(16, 32, dtype=bf), B, Y, Z, Z)
+    _refused("dB\\[0\\]: dtype", cola.group_bwd, g, Y, X, Z, Z, A_all, B, X, torch.zeros(24, 32),
+             [torch.zeros(24, 8, dtype=bf), torch.zeros(40, 16)])
+    dd = cola.dense_desc(64, 32, 24)
+    W = torch.zeros(24, 32, dtype=bf)
+    _refused("dW: dtype", cola.dense_bwd, dd, Y[0], X, W, X, torch.zeros(24, 32, dtype=bf))
+    _refused("W: shape", cola.dense_fwd, dd, X, torch.zeros(24, 31, dtype=bf), Y[0])
+    _refused("X: tensor is on cpu", cola.dense_fwd, dd, X, W, Y[0])
+
+
+def test_tuning_options():
+    L = cola.lib()
+    assert cola.get_option(cola.OPT_STREAM_ONLY) == 0
+    assert cola.get_option(cola.OPT_WGRAD_PAIR) == 1
+    assert L.cola_get_option(7) == -1
+    assert L.cola_set_option(7, 0) == cola.ERR_INVALID_ARG
+    assert L.cola_set_option(cola.OPT_WGRAD_PAIR, 2) == cola.ERR_INVALID_ARG
+    assert cola.get_option(cola.OPT_WGRAD_PAIR) == 1
+    # the workspace plan follows the setting: one split for both weight
+    # gradients when paired, one each when not
+    d = cola.desc(32768, 2048, 2048, 512)
+    paired = cola.workspace_bytes(d, 1)
+    cola.set_option(cola.OPT_WGRAD_PAIR, 0)
+    try:
+        assert cola.get_option(cola.OPT_WGRAD_PAIR) == 0
+        assert cola.workspace_bytes(d, 1) != paired
+    finally:
+        cola.set_option(cola.OPT_WGRAD_PAIR, 1)
+    assert cola.workspace_bytes(d, 1) == paired

@@ -114,3 +114,31 @@ def test_more_than_one_gpu_refused():
     assert r.returncode == 2
     assert "one GPU" in r.stderr
     assert r.stdout == ""
+
+
+# --------------------------------------------------------------------------
+# the benchmark's flop formulas are the oracle's counted work (2 flops per
+# multiply-add of every GEMM the oracle runs, Sec. 3.4)
+# --------------------------------------------------------------------------
+
+@pytest.mark.parametrize("shape", [(1, 1, 1, 1), (5, 12, 7, 3), (33, 40, 72, 8), (64, 24, 24, 24)])
+def test_bench_flops_equal_oracle_mac_count(shape):
+    import numpy as np
+    import oracle
+    T, d_in, d_out, r = shape
+    g = np.random.Generator(np.random.PCG64(5))
+    X = g.standard_normal((T, d_in))
+    A = g.standard_normal((r, d_in))
+    B = g.standard_normal((d_out, r))
+    W = g.standard_normal((d_out, d_in))
+    dY = g.standard_normal((T, d_out))
+    oracle.reset_macs()
+    Z, _, _ = oracle.cola_fwd(X, A, B)
+    fwd = 2 * oracle.macs()
+    oracle.cola_bwd(X, Z, A, B, dY)
+    assert bench.algo_flops_cola(T, d_in, d_out, r) == 2 * oracle.macs()
+    assert bench.algo_flops_cola_fwd(T, d_in, d_out, r) == fwd
+    oracle.reset_macs()
+    oracle.dense_fwd(X, W)
+    oracle.dense_bwd(X, W, dY)
+    assert bench.algo_flops_dense(T, d_in, d_out) == 2 * oracle.macs()

@@ -1,10 +1,13 @@
 """GPU parity at the full workload sizes (LLaMA-60M/350M/1B/7B-shaped blocks),
-in the launch configuration the benchmark times (row pitches padded to 16
-bytes, bf16, SiLU): the oracle evaluates sampled outputs one by one -- whole
-rows of Z, H, Y, dX for sampled tokens, and whole rows of dA / columns of dB
-for sampled rank indices -- and the GPU must match them within the bf16
-tolerance.  Unsampled outputs are checked for finiteness.  The 7B-shaped
-block runs in CoLA-M mode as well as CoLA."""
+in the launch configuration the benchmark times (row pitches padded to whole
+128-byte lines, bf16, SiLU): the oracle evaluates sampled outputs one by one
+-- whole rows of Z, H, Y, dX for one token in every 256-row tile (so every
+output tile of the row-major products is visited), and whole rows of dA /
+columns of dB for one rank index in every 256-wide block -- and the GPU must
+match them within the bf16 tolerance.  Unsampled outputs are checked for
+finiteness.  Every workload runs in CoLA and in CoLA-M mode.  The dense
+baseline runs at the 1B-shaped gate and down shapes the same way (rows of Y
+and dX, rows of dW)."""
 import numpy as np
 import pytest
 import torch
@@ -13,31 +16,33 @@ import oracle
 from paper_2502_10940_amd import cola
 from paper_2502_10940_amd import inputs as I
 
-from layer_runner import LayerRun, relerr
+from layer_runner import NAN_BITS, LayerRun, empty, relerr, to_device
 
 pytestmark = pytest.mark.gpu
 
 TOL = 1e-2
 
 
+def per_tile(n, seed, tile=256):
+    """One index in every `tile`-long block of [0, n) (seeded position within
+    the block), plus both ends and the two indices around the middle."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    idx = {0, 1, n // 2, n // 2 + 1, n - 2, n - 1}
+    for b in range(0, n, tile):
+        idx.add(int(rng.integers(b, min(n, b + tile))))
+    return np.array(sorted(i for i in idx if 0 <= i < n), dtype=np.int64)
+
+
 def sample_rows(T):
-    rows = {0, 1, 127, 128, 255, 256, T // 2, T // 2 + 1, T - 2, T - 1}
-    rng = np.random.Generator(np.random.PCG64(T))
-    rows |= set(int(x) for x in rng.integers(0, T, 6))
-    return np.array(sorted(r for r in rows if 0 <= r < T), dtype=np.int64)
+    return per_tile(T, T)
 
 
 def sample_rank(r):
-    return np.array(sorted({0, r // 2 + 1, r - 1}), dtype=np.int64)
+    return per_tile(r, r + 1)
 
 
-# workload, projection index (0 = q: d->d, 4 = gate: d->ffn, 6 = down: ffn->d), modes
-CASES = []
-for cfg in (2, 3, 4, 5):
-    for proj in (0, 4, 6):
-        modes = (False, True) if cfg in (4, 5) else (False,)
-        for m in modes:
-            CASES.append((cfg, proj, m))
+# workload, projection index (0 = q: d->d, 4 = gate: d->ffn, 6 = down: ffn->d), mode
+CASES = [(cfg, proj, m) for cfg in (2, 3, 4, 5) for proj in (0, 4, 6) for m in (False, True)]
 
 
 @pytest.fixture(scope="module", autouse=True)
@@ -87,3 +92,44 @@ def test_fullsize_sampled(cfg, proj, recompute):
     ref_dA, ref_dB = oracle.cola_wgrad_cols(X, A, B, dY, ranks, "silu")
     assert relerr(got_dA, ref_dA) <= TOL
     assert relerr(got_dB, ref_dB) <= TOL
+
+
+DENSE_CASES = [(4, 4), (4, 6)]
+
+
+@pytest.mark.parametrize("cfg,proj", DENSE_CASES, ids=[f"w{c}-{I.PROJECTIONS[p]}" for c, p in DENSE_CASES])
+def test_fullsize_dense_sampled(cfg, proj):
+    w = I.WORKLOADS[cfg]
+    name, idx, d_in, d_out = I.projections(cfg)[proj]
+    T = w["T"]
+    print(f"\n[fullsize dense] workload {cfg} {name} T={T} {d_in}->{d_out}", flush=True)
+    ins = I.layer_inputs(cfg, idx, d_in, d_out, w["r"], T, "bf16", with_dense=True)
+    ldx, ldy = I.padded_ld(d_in, "bf16"), I.padded_ld(d_out, "bf16")
+    d = cola.dense_desc(T, d_in, d_out, "bf16", ldx, ldy)
+    Xd = to_device(ins["X"].store, "bf16", ldx)
+    Wd = to_device(ins["W"].store, "bf16")
+    dYd = to_device(ins["dY"].store, "bf16", ldy)
+    Y = empty(T, ldy, "bf16", NAN_BITS["bf16"])
+    dX = empty(T, ldx, "bf16", NAN_BITS["bf16"])
+    dW = torch.full((d_out, d_in), float("nan"), dtype=torch.float32, device=Xd.device)
+    ws = torch.empty(max(1, cola.dense_workspace_bytes(d, 0), cola.dense_workspace_bytes(d, 1)),
+                     dtype=torch.uint8, device=Xd.device)
+    cola.dense_fwd(d, Xd, Wd, Y, ws)
+    cola.dense_bwd(d, dYd, Xd, Wd, dX, dW, ws)
+    torch.cuda.synchronize()
+    for t, width in ((Y, d_out), (dX, d_in), (dW, d_in)):
+        assert torch.isfinite(t[:, :width].float()).all()
+    for t, width in ((Y, d_out), (dX, d_in)):
+        assert torch.isnan(t[:, width:].float()).all()
+
+    rows = sample_rows(T)
+    outs = per_tile(d_out, d_out + 2)
+    rows_t = torch.from_numpy(rows).to(Xd.device)
+    X, W, dY = ins["X"].f64, ins["W"].f64, ins["dY"].f64
+    ref_Y, ref_dX = oracle.dense_rows(X, W, dY, rows)
+    got_Y = Y.index_select(0, rows_t)[:, :d_out].double().cpu().numpy()
+    got_dX = dX.index_select(0, rows_t)[:, :d_in].double().cpu().numpy()
+    got_dW = dW.index_select(0, torch.from_numpy(outs).to(Xd.device)).double().cpu().numpy()
+    assert relerr(got_Y, ref_Y) <= TOL
+    assert relerr(got_dX, ref_dX) <= TOL
+    assert relerr(got_dW, oracle.dense_wgrad_rows(X, dY, outs)) <= TOL

@@ -210,46 +210,22 @@ def test_single_infer(case):
         assert torch.equal(Yi, Y)
 
 
-GROUP_CHILD = r"""
-import sys, numpy as np
-sys.path[:0] = [sys.argv[1], sys.argv[2]]
-import test_gpu_group as G
-for case in map(int, sys.argv[4].split(",")):
-    name, T, d_in, ranks, widths, dtype, act = G.CASES[case]
-    X, As, Bs, dYs = G.group_inputs(case, T, d_in, ranks, widths, dtype)
-    res = G.GroupRun(X, As, Bs, dYs, T, d_in, ranks, widths, dtype, act, False).run().results()
-    flat = {"dX": res["dX"]}
-    for k in ("Z", "H", "Y", "dA", "dB"):
-        for p, v in enumerate(res[k]):
-            flat[f"{k}{p}"] = v
-    np.savez(f"{sys.argv[3]}_{case}.npz", **flat)
-    print("child done", name, flush=True)
-"""
-
-
-def test_group_weight_gradients_unpaired_switch(tmp_path):
-    """COLA_WGRAD_PAIR=0 (read once per process) launches every weight-gradient
-    product of a group on its own instead of two by two: both paths match the
-    oracle, the fp32 gradients agree to summation order and the rest bitwise."""
-    import os
-    import subprocess
-    import sys
+def test_group_weight_gradients_unpaired_switch():
+    """COLA_OPT_WGRAD_PAIR = 0 launches every weight-gradient product of a group
+    on its own instead of two by two: both paths match the oracle, the fp32
+    gradients agree to summation order and the rest bitwise."""
     cases = [0, 2]      # q, k, v (three products of dB and dA_all); gate, up (wide, 136-rank)
-    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
-    dst = str(tmp_path / "unpaired")
-    env = dict(os.environ, COLA_WGRAD_PAIR="0")
-    res = subprocess.run([sys.executable, "-u", "-c", GROUP_CHILD, root, os.path.join(root, "tests"), dst,
-                          ",".join(map(str, cases))], env=env, capture_output=True, text=True, timeout=240)
-    assert res.returncode == 0, res.stdout[-2000:] + res.stderr[-2000:]
     for case in cases:
         name, T, d_in, ranks, widths, dtype, act = CASES[case]
         X, As, Bs, dYs = group_inputs(case, T, d_in, ranks, widths, dtype)
         ref = oracle_group(X, As, Bs, dYs, act)
         paired = GroupRun(X, As, Bs, dYs, T, d_in, ranks, widths, dtype, act, False).run().results()
-        got = np.load(f"{dst}_{case}.npz")
-        unpaired = {"dX": got["dX"]}
-        for k in ("Z", "H", "Y", "dA", "dB"):
-            unpaired[k] = [got[f"{k}{p}"] for p in range(len(ranks))]
+        old = cola.get_option(cola.OPT_WGRAD_PAIR)
+        cola.set_option(cola.OPT_WGRAD_PAIR, 0)
+        try:
+            unpaired = GroupRun(X, As, Bs, dYs, T, d_in, ranks, widths, dtype, act, False).run().results()
+        finally:
+            cola.set_option(cola.OPT_WGRAD_PAIR, old)
         check(paired, ref, dtype, f"{name}/paired")
         check(unpaired, ref, dtype, f"{name}/unpaired")
         for k in ("dA", "dB"):

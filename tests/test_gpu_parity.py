@@ -194,37 +194,30 @@ def test_identity_cola_equals_dense_with_merged_weight():
     assert relerr(to_f64(run.Y), to_f64(Yd)) <= 1e-5
 
 
-CHILD = r"""
-import sys, numpy as np
-sys.path[:0] = [sys.argv[1], sys.argv[2]]
-from paper_2502_10940_amd import inputs as I
-from layer_runner import LayerRun
-T, d_in, d_out, r = 1000, 768, 1376, 192
-ins = I.layer_inputs(160, 0, d_in, d_out, r, T, "bf16")
-out = LayerRun(ins, T, d_in, d_out, r, "bf16", "silu", False).run().outputs()
-np.savez(sys.argv[3], **out)
-print("child done", flush=True)
-"""
+class _option:
+    """Set a library tuning option for the duration of a with-block."""
+
+    def __init__(self, option, value):
+        self.option, self.value = option, value
+
+    def __enter__(self):
+        self.old = cola.get_option(self.option)
+        cola.set_option(self.option, self.value)
+
+    def __exit__(self, *exc):
+        cola.set_option(self.option, self.old)
 
 
-def test_weight_gradients_unpaired_switch(tmp_path):
-    """COLA_WGRAD_PAIR=0 (read once per process) launches dA and dB one by one
-    instead of in one launch: both paths match the oracle and each other."""
-    import os
-    import subprocess
-    import sys
+def test_weight_gradients_unpaired_switch():
+    """COLA_OPT_WGRAD_PAIR = 0 launches dA and dB one by one instead of in one
+    launch: both paths match the oracle and each other."""
     T, d_in, d_out, r = 1000, 768, 1376, 192
     ins = I.layer_inputs(160, 0, d_in, d_out, r, T, "bf16")
     ref = oracle_all(ins, "silu")
     paired = LayerRun(ins, T, d_in, d_out, r, "bf16", "silu", False).run().outputs()
     check(paired, ref, "bf16", "paired")
-    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
-    dst = str(tmp_path / "unpaired.npz")
-    env = dict(os.environ, COLA_WGRAD_PAIR="0")
-    res = subprocess.run([sys.executable, "-u", "-c", CHILD, root, os.path.join(root, "tests"), dst],
-                         env=env, capture_output=True, text=True, timeout=240)
-    assert res.returncode == 0, res.stdout[-2000:] + res.stderr[-2000:]
-    unpaired = dict(np.load(dst))
+    with _option(cola.OPT_WGRAD_PAIR, 0):
+        unpaired = LayerRun(ins, T, d_in, d_out, r, "bf16", "silu", False).run().outputs()
     check(unpaired, ref, "bf16", "unpaired")
     for k in ("dA", "dB"):
         assert relerr(unpaired[k], paired[k]) <= 1e-5, k
@@ -232,42 +225,42 @@ def test_weight_gradients_unpaired_switch(tmp_path):
         assert np.array_equal(unpaired[k], paired[k]), k
 
 
-FAMILY_CHILD = r"""
-import sys, numpy as np
-sys.path[:0] = [sys.argv[1], sys.argv[2]]
-import test_gpu_parity as P
-from layer_runner import LayerRun
-for case in map(int, sys.argv[4].split(",")):
-    name, T, d_in, d_out, r, dtype, act = P.CASES[case]
-    ins = P.gen(case, T, d_in, d_out, r, dtype)
-    for rc in (False, True):
-        out = LayerRun(ins, T, d_in, d_out, r, dtype, act, rc).run().outputs()
-        np.savez(f"{sys.argv[3]}_{case}_{int(rc)}.npz", **out)
-    print("child done", name, flush=True)
-"""
-
-
-@pytest.mark.parametrize("family", ["big", "wide", "reg", "stream"])
-def test_forced_gemm_family(family, tmp_path):
-    """COLA_GEMM_FAMILY (read once per process) forces every bf16 product onto
-    one kernel family (the 256 x 256 ones only where both output dimensions
-    exceed 128): each family against the oracle on ragged tiles, unaligned
+def test_streaming_family_forced():
+    """COLA_OPT_STREAM_ONLY = 1 sends every bf16 product to the streaming
+    family (BM x 128 tiles): against the oracle on ragged tiles, unaligned
     output rows and an odd rank above 128, CoLA and CoLA-M."""
-    import os
-    import subprocess
-    import sys
     names = ("tiles_ragged_bf16", "odd_width_rank136_bf16", "odd_rank137_bf16")
     cases = [i for i, c in enumerate(CASES) if c[0] in names]
     assert len(cases) == len(names)
-    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
-    dst = str(tmp_path / family)
-    env = dict(os.environ, COLA_GEMM_FAMILY=family)
-    res = subprocess.run([sys.executable, "-u", "-c", FAMILY_CHILD, root, os.path.join(root, "tests"), dst,
-                          ",".join(map(str, cases))], env=env, capture_output=True, text=True, timeout=240)
-    assert res.returncode == 0, res.stdout[-2000:] + res.stderr[-2000:]
-    for case in cases:
-        name, T, d_in, d_out, r, dtype, act = CASES[case]
-        ref = oracle_all(gen(case, T, d_in, d_out, r, dtype), act)
-        for rc in (0, 1):
-            got = dict(np.load(f"{dst}_{case}_{rc}.npz"))
-            check(got, ref, dtype, f"{family}/{name}/recompute={rc}")
+    with _option(cola.OPT_STREAM_ONLY, 1):
+        for case in cases:
+            name, T, d_in, d_out, r, dtype, act = CASES[case]
+            ins = gen(case, T, d_in, d_out, r, dtype)
+            ref = oracle_all(ins, act)
+            for rc in (False, True):
+                got = LayerRun(ins, T, d_in, d_out, r, dtype, act, rc).run().outputs()
+                check(got, ref, dtype, f"stream/{name}/recompute={rc}")
+
+
+@pytest.mark.parametrize("recompute", [False, True])
+def test_library_flop_counters_equal_oracle_macs(recompute):
+    """The library's per-launch flop counters (2 M N K per GEMM) summed over one
+    forward + backward equal twice the oracle's counted multiply-adds for the
+    same shape (Sec. 3.4), in both modes, with the weight gradients split over
+    tokens."""
+    T, d_in, d_out, r = 2048, 520, 264, 136
+    ins = gen(60, T, d_in, d_out, r, "bf16")
+    run = LayerRun(ins, T, d_in, d_out, r, "bf16", "silu", recompute)
+    cola.timing_reset()
+    cola.timing_enable(True)
+    try:
+        run.run()
+    finally:
+        cola.timing_enable(False)
+    total = sum(cola.timing_read(k)[2] for k in range(len(cola.KERNEL_CLASSES)))
+    cola.timing_reset()
+    X, A, B, dY = ins["X"].f64, ins["A"].f64, ins["B"].f64, ins["dY"].f64
+    oracle.reset_macs()
+    Z, _, _ = oracle.cola_fwd(X, A, B)
+    oracle.cola_bwd(X, Z, A, B, dY)
+    assert total == 2 * oracle.macs()

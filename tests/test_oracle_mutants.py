@@ -35,6 +35,9 @@ MUTANTS = {
     "outer_forward_skips_sigma": ("Y[i] = oracle_sigma(outer, P[i]);", "Y[i] = P[i];"),
     "outer_uses_inner_act": ("dP[i] = dY[i] * oracle_sigma_prime(outer, P[i]);",
                              "dP[i] = dY[i] * oracle_sigma_prime(act, P[i]);"),
+    "dense_dW_transposed": ("gemm_tn(d_out, d_in, T, dY, X, dW);", "gemm_tn(d_in, d_out, T, X, dY, dW);"),
+    "dense_dX_reads_W_transposed": ("gemm_nn(T, d_in, d_out, dY, W, dX);", "gemm_nt(T, d_in, d_out, dY, W, dX);"),
+    "dense_fwd_reads_W_transposed": ("gemm_nt(T, d_out, d_in, X, W, Y);", "gemm_nn(T, d_out, d_in, X, W, Y);"),
     "mac_counter_fwd_only_one_gemm": ("static void gemm_nt(int64_t M, int64_t N, int64_t K,\n                    const double* P, const double* Q, double* C) {\n    g_mac_count += M * N * K;",
                                       "static void gemm_nt(int64_t M, int64_t N, int64_t K,\n                    const double* P, const double* Q, double* C) {\n    g_mac_count += M * N;"),
 }
@@ -60,6 +63,8 @@ def battery():
         ("outer_identity", pins.test_outer_identity_is_the_plain_layer, ("silu",)),
         ("outer_fd", pins.test_outer_gradients_by_central_differences, ((3, 5, 4, 2), "identity", "silu")),
         ("outer_torch", pins.test_outer_against_torch_fp64_autograd, ("silu", "gelu")),
+        ("dense_fd", pins.test_dense_gradients_by_central_differences, ((4, 2, 7),)),
+        ("dense_cross", pins.test_dense_backward_cross_pinned_to_cola, ((9, 7, 5, 3),)),
     ]
     failed = []
     for name, fn, args in checks:

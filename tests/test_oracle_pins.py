@@ -146,6 +146,70 @@ def test_dense_oracle_against_numpy_and_merged_cola():
 
 
 # --------------------------------------------------------------------------
+# dense backward (Sec. 3.4, the 2x rule): pinned by finite differences, by
+# torch autograd, and across to the finite-difference-pinned CoLA gradients
+# --------------------------------------------------------------------------
+
+@pytest.mark.parametrize("shape", [(1, 1, 1), (3, 5, 4), (4, 2, 7), (6, 3, 3)])
+def test_dense_gradients_by_central_differences(shape):
+    # L = <dY, X W^T> is bilinear, so central differences are exact up to
+    # rounding: dL/dX = dY W, dL/dW = dY^T X
+    T, d_in, d_out = shape
+    g = rng(71 + T)
+    X = g.standard_normal((T, d_in))
+    W = g.standard_normal((d_out, d_in))
+    dY = g.standard_normal((T, d_out))
+
+    def loss(X_, W_):
+        return float(np.sum(dY * oracle.dense_fwd(X_, W_)))
+
+    dX, dW = oracle.dense_bwd(X, W, dY)
+    h = 1e-4
+    for name, arr, grad in (("X", X, dX), ("W", W, dW)):
+        fd = np.zeros_like(arr)
+        for idx in np.ndindex(arr.shape):
+            p = arr.copy(); p[idx] += h
+            m = arr.copy(); m[idx] -= h
+            lp = loss(p, W) if name == "X" else loss(X, p)
+            lm = loss(m, W) if name == "X" else loss(X, m)
+            fd[idx] = (lp - lm) / (2 * h)
+        assert grad.shape == arr.shape
+        assert relerr(grad, fd) < 1e-9, name
+
+
+@pytest.mark.parametrize("shape", [(9, 7, 5, 3), (16, 12, 20, 4), (5, 6, 6, 6)])
+def test_dense_backward_cross_pinned_to_cola(shape):
+    # identity sigma with W = B A: the dense layer and the CoLA layer are the
+    # same function of X, so dX agrees; and by the chain rule through W = B A
+    # the CoLA weight gradients are dA = B^T dW and dB = dW A^T
+    T, d_in, d_out, r = shape
+    X, A, B, dY = rand_layer(81 + T, T, d_in, d_out, r)
+    W = B @ A
+    dXd, dW = oracle.dense_bwd(X, W, dY)
+    Z, _, _ = oracle.cola_fwd(X, A, B, act="identity")
+    _, dXc, dA, dB = oracle.cola_bwd(X, Z, A, B, dY, act="identity")
+    assert relerr(dXd, dXc) < 1e-13
+    assert relerr(B.T @ dW, dA) < 1e-13
+    assert relerr(dW @ A.T, dB) < 1e-13
+
+
+def test_dense_against_torch_fp64_autograd():
+    T, d_in, d_out = 21, 13, 17
+    g = rng(91)
+    X = g.standard_normal((T, d_in))
+    W = g.standard_normal((d_out, d_in))
+    dY = g.standard_normal((T, d_out))
+    tX = torch.tensor(X, requires_grad=True)
+    tW = torch.tensor(W, requires_grad=True)
+    tY = torch.nn.functional.linear(tX, tW)
+    tY.backward(torch.tensor(dY))
+    Y = oracle.dense_fwd(X, W)
+    dX, dW = oracle.dense_bwd(X, W, dY)
+    for ours, ref in ((Y, tY), (dX, tX.grad), (dW, tW.grad)):
+        assert relerr(ours, ref.detach().numpy()) < 1e-14
+
+
+# --------------------------------------------------------------------------
 # SiLU gradients: brute-force central differences of L = <dY, Y(X, A, B)>
 # --------------------------------------------------------------------------
 
@@ -319,6 +383,27 @@ def test_sampled_rows_and_columns_match_full():
         oracle.cola_rows(X, A, B, dY, [T])
     with pytest.raises(ValueError):
         oracle.cola_wgrad_cols(X, A, B, dY, [r])
+
+
+def test_sampled_dense_rows_match_full():
+    # the full dense oracle is pinned by finite differences and the CoLA cross-pin above
+    T, d_in, d_out = 37, 19, 23
+    g = rng(63)
+    X = g.standard_normal((T, d_in))
+    W = g.standard_normal((d_out, d_in))
+    dY = g.standard_normal((T, d_out))
+    Y = oracle.dense_fwd(X, W)
+    dX, dW = oracle.dense_bwd(X, W, dY)
+    rows = [0, 36, 11, 11]
+    Yr, dXr = oracle.dense_rows(X, W, dY, rows)
+    assert relerr(Yr, Y[rows]) < 1e-14
+    assert relerr(dXr, dX[rows]) < 1e-14
+    outs = [22, 0, 7]
+    assert relerr(oracle.dense_wgrad_rows(X, dY, outs), dW[outs]) < 1e-14
+    with pytest.raises(ValueError):
+        oracle.dense_rows(X, W, dY, [T])
+    with pytest.raises(ValueError):
+        oracle.dense_wgrad_rows(X, dY, [d_out])
 
 
 # --------------------------------------------------------------------------
