@@ -77,7 +77,8 @@ typedef enum {
     COLA_ERR_BAD_SHAPE = 2,        /* d_in, d_out or r < 1, T < 0, ld < width, size overflow */
     COLA_ERR_WORKSPACE = 3,        /* ws_bytes below the size cola_workspace_bytes() returns */
     COLA_ERR_HIP = 4,              /* a launch failed; cola_strerror() returns HIP's text */
-    COLA_ERR_UNSUPPORTED = 5       /* combination not compiled in */
+    COLA_ERR_UNSUPPORTED = 5,      /* combination not compiled in */
+    COLA_ERR_SCRATCH = 6           /* cola_bwd_scratch: needs more than COLA_SCRATCH_BYTES */
 } cola_status;
 
 typedef struct {
@@ -135,6 +136,24 @@ int cola_bwd(const cola_desc* desc,
              const void* A, const void* B,
              void* dX, float* dA, float* dB,
              void* ws, size_t ws_bytes, cola_stream_t stream);
+
+/* Backward for callers that cannot allocate device memory (code under HIP
+ * graph capture, tight serving loops, harnesses that forbid hipMalloc): the
+ * same computation and results as cola_bwd (bitwise), with its workspace in a
+ * static device array of the library instead of a caller buffer.  Nothing is
+ * allocated or freed by the call; the array (COLA_SCRATCH_BYTES per GPU) is
+ * placed when the library's code object is loaded on a GPU and held until the
+ * process ends.  Each GPU has its own array, shared by every call on that
+ * GPU: calls that overlap on one GPU (concurrent streams, threads or graph
+ * replays in flight) race on it and must be ordered by the caller.  A call
+ * whose workspace (cola_workspace_bytes(desc, 1)) exceeds COLA_SCRATCH_BYTES
+ * returns COLA_ERR_SCRATCH and enqueues nothing.  Arguments, ownership,
+ * errors and T = 0 as cola_bwd. */
+#define COLA_SCRATCH_BYTES ((size_t)64 << 20)
+int cola_bwd_scratch(const cola_desc* desc,
+                     const void* dY, const void* X, const void* Z, const void* H,
+                     const void* A, const void* B,
+                     void* dX, float* dA, float* dB, cola_stream_t stream);
 
 /* The "both sigma" variant of the ablation (App. ablation, Table
  * "ablation"): the nonlinearity that followed the original linear layer is

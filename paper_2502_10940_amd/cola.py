@@ -18,7 +18,8 @@ ACT_IDENTITY, ACT_SILU, ACT_GELU = 0, 1, 2
 DTYPES = {"f32": F32, "bf16": BF16}
 ACTS = {"identity": ACT_IDENTITY, "silu": ACT_SILU, "gelu": ACT_GELU}
 
-OK, ERR_INVALID_ARG, ERR_BAD_SHAPE, ERR_WORKSPACE, ERR_HIP, ERR_UNSUPPORTED = range(6)
+OK, ERR_INVALID_ARG, ERR_BAD_SHAPE, ERR_WORKSPACE, ERR_HIP, ERR_UNSUPPORTED, ERR_SCRATCH = range(7)
+SCRATCH_BYTES = 64 << 20      # COLA_SCRATCH_BYTES
 
 KERNEL_CLASSES = ("fwd_z_sigma", "fwd_y", "bwd_dz", "bwd_dx", "bwd_da", "bwd_db",
                   "reduce_splits", "dense_fwd", "dense_dx", "dense_dw", "fill_zero", "infer_h",
@@ -83,6 +84,7 @@ EXPORTS = {
     "cola_timing_read": ([ctypes.c_int, ctypes.POINTER(ctypes.c_int64), ctypes.POINTER(ctypes.c_double),
                           ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double)], ctypes.c_int),
     "cola_kernel_name": ([ctypes.c_int], ctypes.c_char_p),
+    "cola_bwd_scratch": ([ctypes.POINTER(ColaDesc), _P, _P, _P, _P, _P, _P, _P, _P, _P, _P], ctypes.c_int),
     "cola_set_option": ([ctypes.c_int, ctypes.c_int], ctypes.c_int),
     "cola_get_option": ([ctypes.c_int], ctypes.c_int),
 }
@@ -388,6 +390,14 @@ def bwd(d: ColaDesc, dY, X, Z, H, A, B, dX, dA, dB, ws=None, ws_bytes=None, stre
     _check_layer(d, dY=dY, X=X, Z=Z, H=H, A=A, B=B, dX=dX, dA=dA, dB=dB)
     _check(lib().cola_bwd(ctypes.byref(d), _ptr(dY), _ptr(X), _ptr(Z), _ptr(H), _ptr(A), _ptr(B),
                           _ptr(dX), _ptr(dA), _ptr(dB), _ptr(ws), ws_bytes, _stream(stream)))
+
+
+def bwd_scratch(d: ColaDesc, dY, X, Z, H, A, B, dX, dA, dB, stream=None):
+    """cola_bwd with the library's static device scratch as its workspace
+    (for callers that cannot allocate; overlapping calls on one GPU race)."""
+    _check_layer(d, dY=dY, X=X, Z=Z, H=H, A=A, B=B, dX=dX, dA=dA, dB=dB)
+    _check(lib().cola_bwd_scratch(ctypes.byref(d), _ptr(dY), _ptr(X), _ptr(Z), _ptr(H), _ptr(A), _ptr(B),
+                                  _ptr(dX), _ptr(dA), _ptr(dB), _stream(stream)))
 
 
 def dense_fwd(d: DenseDesc, X, W, Y, ws=None, ws_bytes=None, stream=None):

@@ -534,6 +534,7 @@ const char* cola_strerror(int status) {
         case COLA_ERR_WORKSPACE: return "workspace too small";
         case COLA_ERR_HIP: return g_err[0] ? g_err : "HIP error";
         case COLA_ERR_UNSUPPORTED: return "unsupported combination";
+        case COLA_ERR_SCRATCH: return "the call needs more than the library's static scratch (COLA_SCRATCH_BYTES)";
         default: return "unknown status";
     }
 }
@@ -610,6 +611,83 @@ int cola_bwd(const cola_desc* desc, const void* dY, const void* X, const void* Z
         if (!ws || ws_bytes < p.total) return COLA_ERR_WORKSPACE;
         return layer_backward(x, desc->act, recompute, dY, x.ldy, X, Z, H, A, B, dX, dA, dB,
                               reinterpret_cast<char*>(ws), s);
+    });
+}
+
+// ---------------------------------------------------------------------------
+// backward without a caller workspace: the library's static device scratch
+// ---------------------------------------------------------------------------
+}  // extern "C"
+
+namespace {
+
+// The workspace of cola_bwd_scratch: one array per GPU, placed by the code
+// object loader and held until the process ends.  In host code `scratch` is
+// a host-side stand-in, not a device address: kernels get the address that
+// hipGetSymbolAddress returns for the current device, kept per device.
+static __device__ __align__(256) unsigned char scratch[COLA_SCRATCH_BYTES];
+
+constexpr int kMaxDevices = 64;
+
+struct ScratchPtrs {
+    std::mutex mu;
+    void* ptr[kMaxDevices] = {};
+};
+
+ScratchPtrs& scratch_ptrs() {
+    static ScratchPtrs* s = new ScratchPtrs();   // never destroyed
+    return *s;
+}
+
+// Device address of this device's scratch (looked up once per device, with
+// that device current).
+int scratch_of_current_device(void** out) {
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+    if (dev < 0 || dev >= kMaxDevices) {
+        snprintf(g_err, sizeof(g_err), "device %d beyond the %d the scratch table holds", dev, kMaxDevices);
+        return COLA_ERR_HIP;
+    }
+    ScratchPtrs& t = scratch_ptrs();
+    std::lock_guard<std::mutex> lock(t.mu);
+    if (!t.ptr[dev]) {
+        void* p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress(scratch)");
+        if (!p) {
+            snprintf(g_err, sizeof(g_err), "hipGetSymbolAddress(scratch) returned NULL");
+            return COLA_ERR_HIP;
+        }
+        t.ptr[dev] = p;
+    }
+    *out = t.ptr[dev];
+    return COLA_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int cola_bwd_scratch(const cola_desc* desc, const void* dY, const void* X, const void* Z, const void* H,
+                     const void* A, const void* B, void* dX, float* dA, float* dB, cola_stream_t stream) {
+    return guarded([&]() -> int {
+        Dims x;
+        int st = check_desc(desc, &x);
+        if (st != COLA_OK) return st;
+        const bool recompute = desc->recompute == 1;
+        if (recompute ? (H != nullptr) : (H == nullptr && x.T > 0)) return COLA_ERR_INVALID_ARG;
+        if (!dA || !dB) return COLA_ERR_INVALID_ARG;
+        hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+        if (x.T == 0) return zero_weight_grads(x, dA, dB, s);
+        if (!dY || !X || !Z || !A || !B || !dX) return COLA_ERR_INVALID_ARG;
+        const BwdPlan p = plan_bwd(x, recompute);
+        if (p.total > COLA_SCRATCH_BYTES) return COLA_ERR_SCRATCH;
+        void* w = nullptr;
+        st = scratch_of_current_device(&w);
+        if (st != COLA_OK) return st;
+        return layer_backward(x, desc->act, recompute, dY, x.ldy, X, Z, H, A, B, dX, dA, dB,
+                              reinterpret_cast<char*>(w), s);
     });
 }
 
