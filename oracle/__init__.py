@@ -54,6 +54,7 @@ def _load(path=None):
     lib.oracle_cola_wgrad_cols.argtypes = [i64, i64, i64, i64, c_int, d, d, d, d,
                                            i64, ctypes.POINTER(ctypes.c_int64), d, d]
     lib.oracle_cola_wgrad_cols.restype = c_int
+    lib.oracle_cola_up_from_z.argtypes = [i64, i64, i64, c_int, d, d, d, d]
     lib.oracle_dense_rows.argtypes = [i64, i64, i64, d, d, d, i64, ctypes.POINTER(ctypes.c_int64), d, d]
     lib.oracle_dense_wgrad_rows.argtypes = [i64, i64, i64, d, d, i64, ctypes.POINTER(ctypes.c_int64), d]
     _lib = lib
@@ -257,3 +258,15 @@ def dense_wgrad_rows(X, dY, outs):
     _load().oracle_dense_wgrad_rows(T, d_in, d_out, _p(X), _p(dY), outs.size,
                                     outs.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)), _p(dW))
     return dW
+
+
+def cola_up_from_z(Z, B, act="silu"):
+    """CoLA-M's recompute from the saved pre-activation: H = sigma(Z), Y = H B^T.
+    Returns (H, Y)."""
+    Z = _f64(Z); B = _f64(B)
+    T, r = Z.shape
+    d_out = B.shape[0]
+    _f64(B, (d_out, r))
+    H = np.empty((T, r)); Y = np.empty((T, d_out))
+    _load().oracle_cola_up_from_z(T, d_out, r, _act(act), _p(Z), _p(B), _p(H), _p(Y))
+    return H, Y

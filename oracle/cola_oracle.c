@@ -219,6 +219,15 @@ void oracle_cola_bwd_outer(int64_t T, int64_t d_in, int64_t d_out, int64_t r, in
     if (dP_out) memcpy(dP_out, dP, (size_t)(T * d_out) * sizeof(double));
 }
 
+/* CoLA-M's recompute of a layer output from its saved pre-activation (Sec.
+ * 4.2, App. C: only the r-wide activation is kept, the up projection B h is
+ * recomputed in backward): H = sigma(Z), Y = H B^T. */
+void oracle_cola_up_from_z(int64_t T, int64_t d_out, int64_t r, int act,
+                           const double* Z, const double* B, double* H, double* Y) {
+    for (int64_t i = 0; i < T * r; ++i) H[i] = oracle_sigma(act, Z[i]);
+    gemm_nt(T, d_out, r, H, B, Y);                /* Y[t][o] = sum_j H[t][j] B[o][j] */
+}
+
 /* ------------------------------------------------------------------------ */
 /* dense baseline, Eq. full-rank-linear and the 2x rule                      */
 /* ------------------------------------------------------------------------ */

@@ -184,3 +184,43 @@ def with_pitch(a: np.ndarray, ld: int, fill) -> np.ndarray:
     out = np.full((rows, ld), fill, dtype=a.dtype)
     out[:, :width] = a
     return out
+
+
+# ---------------------------------------------------------------------------
+# decoder block inputs (the block-level path): the residual-stream input, the
+# upstream gradient of the block output, the two RMSNorm gains and the
+# weights of the seven projections
+# ---------------------------------------------------------------------------
+
+# LLaMA head counts of the workloads (head dim 64 up to the 1B shape, 128 at 7B)
+HEADS = {2: 8, 3: 16, 4: 32, 5: 32}
+SEQ_LEN = 256
+BLOCK_TENSOR_IDS = {"x0": 0, "dx2": 1, "g1": 2, "g2": 3, "A_qkv": 4, "B_q": 5, "B_k": 6, "B_v": 7, "A_o": 8,
+                    "B_o": 9, "A_gu": 10, "B_g": 11, "B_u": 12, "A_d": 13, "B_d": 14}
+
+
+def block_shapes(d: int, ffn: int, r: int) -> dict:
+    """Shapes of the block's parameters: A of the same-input groups stacked
+    (q, k, v: [3r][d]; gate, up: [2r][d])."""
+    return {"g1": (d,), "g2": (d,), "A_qkv": (3 * r, d), "B_q": (d, r), "B_k": (d, r), "B_v": (d, r),
+            "A_o": (r, d), "B_o": (d, r), "A_gu": (2 * r, d), "B_g": (ffn, r), "B_u": (ffn, r),
+            "A_d": (r, ffn), "B_d": (d, r)}
+
+
+def block_inputs(seed: int, n_seq: int, seq_len: int, d: int, ffn: int, r: int, dtype: str = "bf16") -> dict:
+    """x0, dx2 ~ N(0, 1) [T][d]; gains g = 1 + N(0, 0.1^2); A ~ N(0, 1/d_in),
+    B ~ N(0, 1/r) per projection (the layer recipe).  Tensor seed =
+    100000 + 1000 * seed + tensor id."""
+    T = n_seq * seq_len
+    base = 100000 + 1000 * seed
+    out = {"x0": make(base + 0, (T, d), 1.0, dtype), "dx2": make(base + 1, (T, d), 1.0, dtype)}
+    for name, shape in block_shapes(d, ffn, r).items():
+        sid = base + BLOCK_TENSOR_IDS[name]
+        if name in ("g1", "g2"):
+            g = gaussian(sid, (1, shape[0]), 0.1).reshape(shape) + np.float32(1.0)
+            out[name] = Tensor(f32_to_bf16_bits(g) if dtype == "bf16" else g, dtype)
+        elif name.startswith("A"):
+            out[name] = make(sid, shape, 1.0 / math.sqrt(shape[1]), dtype)
+        else:
+            out[name] = make(sid, shape, 1.0 / math.sqrt(r), dtype)
+    return out
