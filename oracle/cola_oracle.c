@@ -225,6 +225,7 @@ void oracle_cola_bwd_outer(int64_t T, int64_t d_in, int64_t d_out, int64_t r, in
 void oracle_cola_up_from_z(int64_t T, int64_t d_out, int64_t r, int act,
                            const double* Z, const double* B, double* H, double* Y) {
     for (int64_t i = 0; i < T * r; ++i) H[i] = oracle_sigma(act, Z[i]);
+    /* the up projection */
     gemm_nt(T, d_out, r, H, B, Y);                /* Y[t][o] = sum_j H[t][j] B[o][j] */
 }
 
