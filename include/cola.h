@@ -267,6 +267,91 @@ int dense_fwd(const dense_desc* desc, const void* X, const void* W, void* Y,
 int dense_bwd(const dense_desc* desc, const void* dY, const void* X, const void* W,
               void* dX, float* dW, void* ws, size_t ws_bytes, cola_stream_t stream);
 
+/* ------------------------------------------------------------------------
+ * Decoder block: a LLaMA-style pre-norm block whose seven linear projections
+ * are CoLA layers (Sec. 3.2, Fig. "block"), in CoLA or block-level CoLA-M
+ * (Sec. 4.2, App. C).  The self-attention's scaled dot product, the residual
+ * connections and the gated product of the MLP are the usual ones; with only
+ * the low-rank sigma (the paper's 1B/7B setting, App. ablation) the MLP is
+ * down(gate(b) (.) up(b)) without the original SiLU:
+ *   a   = rmsnorm(x0) (.) g1
+ *   q, k, v = CoLA_q(a), CoLA_k(a), CoLA_v(a)                    (one group)
+ *   att = per sequence and head, softmax(rope(q) rope(k)^T / sqrt(hd),
+ *         causal) v       (hd = d / heads; RoPE pairs element i of a head
+ *         with i + hd/2, angle pos * rope_base^(-2i/hd), pos = the token's
+ *         index in its sequence)
+ *   x1  = x0 + CoLA_o(att)
+ *   b   = rmsnorm(x1) (.) g2,   rmsnorm(x) = x / sqrt(mean(x^2) + eps)
+ *   gt, u = CoLA_gate(b), CoLA_up(b)                             (one group)
+ *   x2  = x1 + CoLA_down(gt (.) u)
+ * CoLA keeps every activation the backward reads in `saved` (and the
+ * log2-sum-exp of the attention scores).  CoLA-M keeps x1 and the seven
+ * r-wide pre-activations Z only (with the caller's x0: 2nd + 7nr values,
+ * App. C); its backward recomputes the norms, the up projections
+ * B sigma(Z) of q, k, v, gate and up, the gated product and the attention,
+ * then runs the same backward.  Both modes give bitwise the same outputs.
+ *
+ * Tensors: x0, x2, dx2, dx0 are [T][d] bf16 contiguous, T = n_seq * seq_len,
+ * sequence s in rows s*seq_len ..; weights bf16 contiguous, gradients fp32
+ * contiguous (overwritten), in the shapes of cola_block_weights.  The layout
+ * of `saved` is the library's (cola_block_saved_slot gives each tensor's
+ * offset and pitch).  bf16 only; head_dim 64 or 128; d and r multiples of 8;
+ * x0, x2, dx2, dx0, g1, g2, saved and ws 16-byte aligned (else
+ * COLA_ERR_INVALID_ARG); n_seq and heads at most 65535.
+ * Ownership, streams and errors as for cola_fwd; T = 0 enqueues nothing in
+ * the forward and zero-fills the gradients in the backward.
+ * ------------------------------------------------------------------------ */
+typedef struct {
+    int64_t n_seq, seq_len;   /* sequences and tokens per sequence (>= 1) */
+    int64_t d, ffn, heads;    /* model width, MLP width, attention heads */
+    int64_t r;                /* rank of all seven projections */
+    int32_t act;              /* cola_act of the CoLA layers */
+    int32_t recompute;        /* 0 = CoLA, 1 = CoLA-M */
+    float rope_base;          /* rotary base, e.g. 10000 */
+    float eps;                /* RMSNorm epsilon, e.g. 1e-6 */
+} cola_block_desc;
+
+typedef struct {
+    const void *g1, *g2;              /* [d] RMSNorm gains */
+    const void *A_qkv;                /* [3r][d]: A_q, A_k, A_v stacked */
+    const void *B_q, *B_k, *B_v;      /* [d][r] each */
+    const void *A_o, *B_o;            /* [r][d], [d][r] */
+    const void *A_gu;                 /* [2r][d]: A_gate, A_up stacked */
+    const void *B_g, *B_u;            /* [ffn][r] each */
+    const void *A_d, *B_d;            /* [r][ffn], [d][r] */
+} cola_block_weights;
+
+typedef struct {                      /* fp32, shapes as cola_block_weights */
+    float *g1, *g2, *A_qkv, *B_q, *B_k, *B_v, *A_o, *B_o, *A_gu, *B_g, *B_u, *A_d, *B_d;
+} cola_block_grads;
+
+/* Tensors in `saved` (cola_block_saved_slot): x1, the pre-activations Z of
+ * q,k,v [T][3r], o [T][r], gate,up [T][2r], down [T][r] (both modes); CoLA
+ * also a, H_qkv, q, k, v, att, the attention's log2-sum-exp (fp32
+ * [heads][T], scores scaled by log2(e)/sqrt(hd)), H_o, b, H_gu, gt, u, m =
+ * gt (.) u, H_down. */
+typedef enum {
+    COLA_BLK_X1 = 0, COLA_BLK_Z_QKV, COLA_BLK_Z_O, COLA_BLK_Z_GU, COLA_BLK_Z_DOWN,
+    COLA_BLK_A, COLA_BLK_H_QKV, COLA_BLK_Q, COLA_BLK_K, COLA_BLK_V, COLA_BLK_ATT, COLA_BLK_LSE,
+    COLA_BLK_H_O, COLA_BLK_B, COLA_BLK_H_GU, COLA_BLK_GATE, COLA_BLK_UP, COLA_BLK_M, COLA_BLK_H_DOWN,
+    COLA_BLK_SLOTS
+} cola_block_slot;
+
+/* Bytes of `saved` for the descriptor's mode; 0 on an invalid descriptor. */
+size_t cola_block_saved_bytes(const cola_block_desc* desc);
+/* Byte offset and row pitch (elements) of a slot in `saved`; returns
+ * COLA_ERR_INVALID_ARG for a slot the mode does not keep. */
+int cola_block_saved_slot(const cola_block_desc* desc, int slot, size_t* offset, int64_t* ld);
+/* Workspace bytes for phase 0 (forward) or 1 (backward); 0 if invalid. */
+size_t cola_block_workspace_bytes(const cola_block_desc* desc, int phase);
+
+int cola_block_fwd(const cola_block_desc* desc, const cola_block_weights* w, const void* x0, void* x2,
+                   void* saved, size_t saved_bytes, void* ws, size_t ws_bytes, cola_stream_t stream);
+/* x0: the forward's input (the caller keeps it); dx0 is overwritten. */
+int cola_block_bwd(const cola_block_desc* desc, const cola_block_weights* w, const void* x0,
+                   const void* saved, size_t saved_bytes, const void* dx2, void* dx0,
+                   const cola_block_grads* grads, void* ws, size_t ws_bytes, cola_stream_t stream);
+
 /* Tuning options, process-wide (every GPU and thread of the process), read
  * at each call; for tuning, comparisons and tests, not needed for correct
  * results.  Every setting gives results within the stated tolerances;
@@ -305,7 +390,12 @@ typedef enum {
     COLA_KC_BWD_DADB = 13, /* dA and dB in one launch (bf16, both outputs
                               wider than 128): the two token-split weight
                               gradients share the launch and the split    */
-    COLA_KC_COUNT = 14
+    COLA_KC_ATTN_FWD = 14, /* block: causal attention forward             */
+    COLA_KC_ATTN_BWD = 15, /* block: attention backward (dq, then dk dv)  */
+    COLA_KC_NORM = 16,     /* block: RMSNorm forward (+ residual sum)     */
+    COLA_KC_NORM_BWD = 17, /* block: RMSNorm backward (+ residual grad)   */
+    COLA_KC_POINTWISE = 18,/* block: gated product, residual add, sigma   */
+    COLA_KC_COUNT = 19
 } cola_kernel_class;
 
 /* Per-class totals since the last reset: launches, elapsed milliseconds,

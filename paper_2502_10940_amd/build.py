@@ -19,7 +19,8 @@ LIB = os.path.join(PKG, "libcola.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 
-SOURCES = ["gemm_dispatch.hip", "gemm_stream.hip", "gemm_pp.hip", "gemm_f32.hip", "cola_abi.hip"]
+SOURCES = ["gemm_dispatch.hip", "gemm_stream.hip", "gemm_pp.hip", "gemm_f32.hip", "cola_abi.hip",
+           "attention.hip", "block_ops.hip", "block_abi.hip"]
 # Per-source extra flags.  The 256 x 256 kernel's epilogues run over 256
 # accumulators per lane: past the default limit the unroller stops and the
 # accumulators go to scratch memory.

@@ -23,7 +23,7 @@ SCRATCH_BYTES = 64 << 20      # COLA_SCRATCH_BYTES
 
 KERNEL_CLASSES = ("fwd_z_sigma", "fwd_y", "bwd_dz", "bwd_dx", "bwd_da", "bwd_db",
                   "reduce_splits", "dense_fwd", "dense_dx", "dense_dw", "fill_zero", "infer_h",
-                  "outer_grad", "bwd_da_db")
+                  "outer_grad", "bwd_da_db", "attn_fwd", "attn_bwd", "norm", "norm_bwd", "pointwise")
 
 
 class ColaError(RuntimeError):
@@ -53,6 +53,28 @@ class GroupDesc(ctypes.Structure):
                 ("r", ctypes.c_int64 * GROUP_MAX), ("d_out", ctypes.c_int64 * GROUP_MAX),
                 ("ldy", ctypes.c_int64 * GROUP_MAX), ("ldx", ctypes.c_int64), ("ldz", ctypes.c_int64)]
 
+
+class BlockDesc(ctypes.Structure):
+    _fields_ = [("n_seq", ctypes.c_int64), ("seq_len", ctypes.c_int64), ("d", ctypes.c_int64),
+                ("ffn", ctypes.c_int64), ("heads", ctypes.c_int64), ("r", ctypes.c_int64),
+                ("act", ctypes.c_int32), ("recompute", ctypes.c_int32), ("rope_base", ctypes.c_float),
+                ("eps", ctypes.c_float)]
+
+
+BLOCK_PARAMS = ("g1", "g2", "A_qkv", "B_q", "B_k", "B_v", "A_o", "B_o", "A_gu", "B_g", "B_u", "A_d", "B_d")
+
+
+class BlockWeights(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in BLOCK_PARAMS]
+
+
+class BlockGrads(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in BLOCK_PARAMS]
+
+
+# cola_block_slot: tensors of the block's saved buffer
+BLOCK_SLOTS = ("x1", "Z_qkv", "Z_o", "Z_gu", "Z_down", "a", "H_qkv", "q", "k", "v", "att", "lse", "H_o", "b",
+               "H_gu", "gate", "up", "m", "H_down")
 
 _lib = None
 
@@ -85,6 +107,14 @@ EXPORTS = {
                           ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double)], ctypes.c_int),
     "cola_kernel_name": ([ctypes.c_int], ctypes.c_char_p),
     "cola_bwd_scratch": ([ctypes.POINTER(ColaDesc), _P, _P, _P, _P, _P, _P, _P, _P, _P, _P], ctypes.c_int),
+    "cola_block_saved_bytes": ([ctypes.POINTER(BlockDesc)], _SZ),
+    "cola_block_saved_slot": ([ctypes.POINTER(BlockDesc), ctypes.c_int, ctypes.POINTER(ctypes.c_size_t),
+                               ctypes.POINTER(ctypes.c_int64)], ctypes.c_int),
+    "cola_block_workspace_bytes": ([ctypes.POINTER(BlockDesc), ctypes.c_int], _SZ),
+    "cola_block_fwd": ([ctypes.POINTER(BlockDesc), ctypes.POINTER(BlockWeights), _P, _P, _P, _SZ, _P, _SZ, _P],
+                       ctypes.c_int),
+    "cola_block_bwd": ([ctypes.POINTER(BlockDesc), ctypes.POINTER(BlockWeights), _P, _P, _SZ, _P, _P,
+                        ctypes.POINTER(BlockGrads), _P, _SZ, _P], ctypes.c_int),
     "cola_set_option": ([ctypes.c_int, ctypes.c_int], ctypes.c_int),
     "cola_get_option": ([ctypes.c_int], ctypes.c_int),
 }
@@ -444,3 +474,90 @@ def set_option(option: int, value: int):
 
 def get_option(option: int) -> int:
     return int(lib().cola_get_option(int(option)))
+
+
+
+# ---------------------------------------------------------------------------
+# decoder block (cola_block_*)
+# ---------------------------------------------------------------------------
+
+def block_desc(n_seq, seq_len, d, ffn, heads, r, act="silu", recompute=False, rope_base=10000.0, eps=1e-6):
+    return BlockDesc(n_seq, seq_len, d, ffn, heads, r, ACTS[act] if isinstance(act, str) else int(act),
+                     int(bool(recompute)), rope_base, eps)
+
+
+def block_shapes(d: BlockDesc) -> dict:
+    r, dm, f = d.r, d.d, d.ffn
+    return {"g1": (dm,), "g2": (dm,), "A_qkv": (3 * r, dm), "B_q": (dm, r), "B_k": (dm, r), "B_v": (dm, r),
+            "A_o": (r, dm), "B_o": (dm, r), "A_gu": (2 * r, dm), "B_g": (f, r), "B_u": (f, r), "A_d": (r, f),
+            "B_d": (dm, r)}
+
+
+def block_saved_bytes(d: BlockDesc) -> int:
+    return int(lib().cola_block_saved_bytes(ctypes.byref(d)))
+
+
+def block_workspace_bytes(d: BlockDesc, phase: int) -> int:
+    return int(lib().cola_block_workspace_bytes(ctypes.byref(d), phase))
+
+
+def block_saved_slot(d: BlockDesc, slot) -> tuple:
+    """(byte offset, row pitch in elements) of a tensor in the saved buffer."""
+    idx = BLOCK_SLOTS.index(slot) if isinstance(slot, str) else int(slot)
+    off = ctypes.c_size_t()
+    ld = ctypes.c_int64()
+    _check(lib().cola_block_saved_slot(ctypes.byref(d), idx, ctypes.byref(off), ctypes.byref(ld)))
+    return int(off.value), int(ld.value)
+
+
+def _check_block(d: BlockDesc, params: dict, dtype, **acts):
+    import torch
+    if d.n_seq < 0 or d.seq_len < 1 or d.d < 1 or d.ffn < 1 or d.r < 1:
+        return                      # the library refuses the descriptor itself
+    for name, shape in block_shapes(d).items():
+        t = params.get(name)
+        if t is None:
+            raise ValueError(f"{name}: missing")
+        if isinstance(t, int):
+            continue
+        if t.dtype != dtype or tuple(t.shape) != shape or not t.is_contiguous():
+            raise ValueError(f"{name}: expected a contiguous {dtype} tensor of shape {shape}, got "
+                             f"{t.dtype} {tuple(t.shape)}")
+    T = d.n_seq * d.seq_len
+    for name, t in acts.items():
+        _need(name, t, T, d.d, d.d, torch.bfloat16)
+    if T > 0:
+        _on_gpu(list(acts.items()) + [(k, params[k]) for k in BLOCK_PARAMS])
+
+
+def _bytes_of(t, n):
+    if n is None:
+        n = t.numel() * t.element_size() if t is not None and not isinstance(t, int) else 0
+    _need_ws(t, n)
+    return n
+
+
+def block_fwd(d: BlockDesc, w: dict, x0, x2, saved, ws, saved_bytes=None, ws_bytes=None, stream=None):
+    """x2 = the block applied to x0 (w: bf16 tensors by BLOCK_PARAMS); `saved`
+    receives what the backward needs."""
+    import torch
+    _check_block(d, w, torch.bfloat16, x0=x0, x2=x2)
+    saved_bytes = _bytes_of(saved, saved_bytes)
+    ws_bytes = _bytes_of(ws, ws_bytes)
+    W = BlockWeights(*[_ptr(w[n]) for n in BLOCK_PARAMS])
+    _check(lib().cola_block_fwd(ctypes.byref(d), ctypes.byref(W), _ptr(x0), _ptr(x2), _ptr(saved), saved_bytes,
+                                _ptr(ws), ws_bytes, _stream(stream)))
+
+
+def block_bwd(d: BlockDesc, w: dict, x0, saved, dx2, dx0, grads: dict, ws, saved_bytes=None, ws_bytes=None,
+              stream=None):
+    """dx0 and the fp32 parameter gradients (grads: tensors by BLOCK_PARAMS)."""
+    import torch
+    _check_block(d, w, torch.bfloat16, x0=x0, dx2=dx2, dx0=dx0)
+    _check_block(d, grads, torch.float32)
+    saved_bytes = _bytes_of(saved, saved_bytes)
+    ws_bytes = _bytes_of(ws, ws_bytes)
+    W = BlockWeights(*[_ptr(w[n]) for n in BLOCK_PARAMS])
+    G = BlockGrads(*[_ptr(grads[n]) for n in BLOCK_PARAMS])
+    _check(lib().cola_block_bwd(ctypes.byref(d), ctypes.byref(W), _ptr(x0), _ptr(saved), saved_bytes, _ptr(dx2),
+                                _ptr(dx0), ctypes.byref(G), _ptr(ws), ws_bytes, _stream(stream)))

@@ -514,12 +514,30 @@ OuterPlan plan_outer_bwd(const Dims& x, bool recompute) {
 
 }  // namespace
 
+// ---- hooks for the other translation units (the block path) ----
+namespace cola {
+
+hipError_t timed_call(int kc, double flops, double bytes, hipStream_t s, hipError_t (*fn)(void*), void* ctx) {
+    return timed(kc, flops, bytes, s, [&] { return fn(ctx); });
+}
+
+int set_hip_error(hipError_t e, const char* where) { return hip_fail(e, where); }
+
+hipError_t launch_up_projection(int64_t T, int64_t d_out, int64_t r, const void* H, int64_t ldh, const void* B,
+                                void* Y, int64_t ldy, hipStream_t s) {
+    GemmArgs k2 = make_args(TAG_FWD_Y, T, d_out, r, H, ldh, KMAJ, B, r, KMAJ, Y, ldy, EPI_STORE, 0);
+    const double bytes = 2.0 * ((double)T * r + (double)d_out * r + (double)T * d_out);
+    return timed(COLA_KC_FWD_Y, gemm_flops(T, d_out, r), bytes, s, [&] { return gemm(k2, true, s); });
+}
+
+}  // namespace cola
+
 extern "C" {
 
 int cola_abi_version(void) { return COLA_ABI_VERSION; }
 
 int cola_set_option(int option, int value) {
-    static_assert(COLA_OPT_STREAM_ONLY == OPT_STREAM_ONLY && COLA_OPT_WGRAD_PAIR == OPT_WGRAD_PAIR,
+    static_assert((int)COLA_OPT_STREAM_ONLY == (int)OPT_STREAM_ONLY && (int)COLA_OPT_WGRAD_PAIR == (int)OPT_WGRAD_PAIR,
                   "option numbering");
     return set_option(option, value) == 0 ? COLA_OK : COLA_ERR_INVALID_ARG;
 }
@@ -543,7 +561,7 @@ const char* cola_kernel_name(int kc) {
     static const char* names[COLA_KC_COUNT] = {
         "fwd_z_sigma", "fwd_y", "bwd_dz", "bwd_dx", "bwd_da", "bwd_db",
         "reduce_splits", "dense_fwd", "dense_dx", "dense_dw", "fill_zero", "infer_h", "outer_grad",
-        "bwd_da_db"};
+        "bwd_da_db", "attn_fwd", "attn_bwd", "norm", "norm_bwd", "pointwise"};
     if (kc < 0 || kc >= COLA_KC_COUNT) return "invalid";
     return names[kc];
 }

@@ -438,3 +438,83 @@ def test_tuning_options():
     finally:
         cola.set_option(cola.OPT_WGRAD_PAIR, 1)
     assert cola.workspace_bytes(d, 1) == paired
+
+
+# --------------------------------------------------------------------------
+# decoder block entry points: descriptor validation and the saved set (host
+# only; every call here is refused before anything is enqueued)
+# --------------------------------------------------------------------------
+
+def test_block_descriptor_validation():
+    L = cola.lib()
+    ok = cola.block_desc(2, 256, 512, 1376, 8, 128)
+    assert cola.block_saved_bytes(ok) > 0
+    assert cola.block_workspace_bytes(ok, 0) > 0 and cola.block_workspace_bytes(ok, 1) > 0
+    assert cola.block_workspace_bytes(ok, 2) == 0
+    bad = [cola.block_desc(2, 256, 512, 1376, 16, 128),      # head dim 32: not compiled in
+           cola.block_desc(2, 256, 500, 1376, 5, 128),       # d not a multiple of 8
+           cola.block_desc(2, 256, 512, 1376, 8, 100),       # r not a multiple of 8
+           cola.block_desc(2, 0, 512, 1376, 8, 128),         # empty sequences
+           cola.block_desc(-1, 256, 512, 1376, 8, 128),
+           cola.block_desc(2, 256, 512, 1376, 7, 128),       # heads do not divide d
+           cola.block_desc(2, 256, 512, 1376, 8, 128, act=5),
+           cola.block_desc(2, 256, 512, 1376, 8, 128, rope_base=0.0),
+           cola.block_desc(70000, 1, 512, 1376, 8, 128)]     # beyond the attention grid
+    for d in bad:
+        assert cola.block_saved_bytes(d) == 0
+        assert cola.block_workspace_bytes(d, 1) == 0
+    W = cola.BlockWeights(*([FAKE] * len(cola.BLOCK_PARAMS)))
+    G = cola.BlockGrads(*([FAKE] * len(cola.BLOCK_PARAMS)))
+    st = L.cola_block_fwd(ctypes.byref(bad[0]), ctypes.byref(W), FAKE, FAKE, FAKE, 1 << 40, FAKE, 1 << 40, None)
+    assert st == cola.ERR_UNSUPPORTED
+    st = L.cola_block_fwd(ctypes.byref(bad[1]), ctypes.byref(W), FAKE, FAKE, FAKE, 1 << 40, FAKE, 1 << 40, None)
+    assert st == cola.ERR_BAD_SHAPE
+    # a NULL weight, a misaligned input, a short saved buffer, a short workspace
+    W0 = cola.BlockWeights(*([FAKE] * (len(cola.BLOCK_PARAMS) - 1) + [None]))
+    assert L.cola_block_fwd(ctypes.byref(ok), ctypes.byref(W0), FAKE, FAKE, FAKE, 1 << 40, FAKE, 1 << 40,
+                            None) == cola.ERR_INVALID_ARG
+    assert L.cola_block_fwd(ctypes.byref(ok), ctypes.byref(W), FAKE + 2, FAKE, FAKE, 1 << 40, FAKE, 1 << 40,
+                            None) == cola.ERR_INVALID_ARG
+    need_s = cola.block_saved_bytes(ok)
+    need_w = cola.block_workspace_bytes(ok, 0)
+    assert L.cola_block_fwd(ctypes.byref(ok), ctypes.byref(W), FAKE, FAKE, FAKE, need_s - 1, FAKE, need_w,
+                            None) == cola.ERR_WORKSPACE
+    assert L.cola_block_fwd(ctypes.byref(ok), ctypes.byref(W), FAKE, FAKE, FAKE, need_s, FAKE, need_w - 1,
+                            None) == cola.ERR_WORKSPACE
+    assert L.cola_block_bwd(ctypes.byref(ok), ctypes.byref(W), FAKE, FAKE, need_s, FAKE, FAKE, None, FAKE,
+                            1 << 40, None) == cola.ERR_INVALID_ARG
+    need_b = cola.block_workspace_bytes(ok, 1)
+    assert L.cola_block_bwd(ctypes.byref(ok), ctypes.byref(W), FAKE, FAKE, need_s, FAKE, FAKE, ctypes.byref(G),
+                            FAKE, need_b - 1, None) == cola.ERR_WORKSPACE
+
+
+@pytest.mark.parametrize("shape", [(2, 256, 512, 1376, 8, 128), (128, 256, 2048, 5461, 32, 512),
+                                   (64, 256, 4096, 11008, 32, 1024)])
+def test_block_cola_m_saved_set_is_2nd_plus_7nr(shape):
+    # App. C: CoLA-M keeps 2nd + 7nr values per block: the block input (the
+    # caller's x0), the mid-block residual x1 and the seven r-wide
+    # pre-activations; bf16, so 2 bytes each (r a multiple of 64 and an even T:
+    # no row or alignment padding)
+    n_seq, L, d, ffn, heads, r = shape
+    n = n_seq * L
+    dm = cola.block_desc(n_seq, L, d, ffn, heads, r, recompute=True)
+    saved_m = cola.block_saved_bytes(dm)
+    assert saved_m + 2 * n * d == 2 * (2 * n * d + 7 * n * r)
+    # CoLA keeps the 14 nr of the low-rank activations (Z and H of the seven)
+    # and, besides x1, the n x d norms, q, k, v, att and the n x ffn gate, up, product
+    dc = cola.block_desc(n_seq, L, d, ffn, heads, r, recompute=False)
+    ffn_pitch = (ffn + 63) // 64 * 64
+    lse = (n * heads * 4 + 255) // 256 * 256
+    assert cola.block_saved_bytes(dc) == 2 * (7 * n * d + 14 * n * r + 3 * n * ffn_pitch) + lse
+    # the slots tile the buffer without overlap; CoLA-M has no CoLA-only slot
+    spans = []
+    for i, name in enumerate(cola.BLOCK_SLOTS):
+        off, ld = cola.block_saved_slot(dc, name)
+        rows = heads if name == "lse" else n
+        spans.append((off, off + rows * ld * (4 if name == "lse" else 2)))
+        if i >= 5:
+            with pytest.raises(cola.ColaError):
+                cola.block_saved_slot(dm, name)
+    spans.sort()
+    assert all(a[1] <= b[0] for a, b in zip(spans, spans[1:]))
+    assert spans[-1][1] <= cola.block_saved_bytes(dc)
