@@ -54,6 +54,12 @@ def parse():
                     help="skip the block with same-input projections grouped (q,k,v and gate,up)")
     ap.add_argument("--only", choices=["cola", "cola_m", "dense"], default=None,
                     help="run only one mode (profiling)")
+    ap.add_argument("--no-block", action="store_true", help="skip the decoder-block record")
+    ap.add_argument("--no-workloads", action="store_true", help="skip the records of the other workloads")
+    ap.add_argument("--sub-steps", type=int, default=50, help="timed steps of the block and workload records")
+    ap.add_argument("--sub-warmup", type=int, default=10)
+    ap.add_argument("--library-baseline", action="store_true",
+                    help="time hipBLASLt (torch.matmul) on the workload's GEMM shapes and exit")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run only a plain 1 GiB device copy (3 times), for scaling HBM counters")
     ap.add_argument("--traffic-from", nargs=4, metavar=("FETCH_CSV", "WRITE_CSV", "COPY_FETCH_CSV",
@@ -334,16 +340,21 @@ def kernel_table(cola):
     return out
 
 
+# the sources the layer's GEMM kernels and their launch plans are built from
+GEMM_SOURCES = ("cola_abi.hip", "device_math.hpp", "epilogue.hpp", "gemm_dispatch.hip", "gemm_f32.hip",
+                "gemm_pp.hip", "gemm_stream.hip", "internal.hpp", "lds_tile.hpp")
+
+
 def kernel_source_hash():
-    """sha256 (first 16 hex digits) over every HIP source of the library, so a
-    stored counter reading is dropped as soon as any kernel changes."""
+    """sha256 (first 16 hex digits) over the sources of the layer's GEMM kernels
+    and their launch plans, so a stored counter reading is dropped as soon as
+    any of them changes."""
     import hashlib
     d = os.path.join(ROOT, "paper_2502_10940_amd", "csrc")
     h = hashlib.sha256()
-    for name in sorted(os.listdir(d)):
-        if name.endswith((".hip", ".hpp")):
-            h.update(name.encode())
-            h.update(open(os.path.join(d, name), "rb").read())
+    for name in GEMM_SOURCES:
+        h.update(name.encode())
+        h.update(open(os.path.join(d, name), "rb").read())
     return h.hexdigest()[:16]
 
 
@@ -389,6 +400,297 @@ def cpu_baseline(projs, cfg_T, tokens):
             "seconds": t_total, "tokens_per_s": tokens / t_total}
 
 
+class Harness:
+    """The projections of one workload on the device, their grouping, the
+    streams they are spread over and one workspace per stream; the step
+    functions of every measured mode."""
+
+    def __init__(self, cfg, dense, cola_m, fused, nstreams):
+        import torch
+        from paper_2502_10940_amd import inputs as I
+        w = I.WORKLOADS[cfg]
+        self.cfg, self.w = cfg, w
+        self.dtype = w["dtype"]
+        self.T, self.r = w["T"], w["r"]
+        self.projs = [Projection(cfg, name, idx, d_in, d_out, self.r, self.T, self.dtype, dense, cola_m)
+                      for name, idx, d_in, d_out in I.projections(cfg)]
+        self.units = []     # the grouped block: groups for same-input projections, single layers otherwise
+        if fused and cfg != 1:
+            by = {p.name: p for p in self.projs}
+            self.units = [Group([by["q"], by["k"], by["v"]], self.dtype), by["o"],
+                          Group([by["gate"], by["up"]], self.dtype), by["down"]]
+        ws_need = max([p.ws_need for p in self.projs] + [u.ws_need for u in self.units if isinstance(u, Group)])
+        # independent projections spread over several HIP streams (default
+        # priority), each with its own workspace, balanced by work: a
+        # projection runs its forward and backward on one stream, and one
+        # kernel's ramp-up overlaps another stream's drain.  The step still
+        # starts and ends on the current stream.
+        self.nstreams = max(1, nstreams)
+        self.streams = [None] + [torch.cuda.Stream() for _ in range(self.nstreams - 1)]
+        self.wss = [torch.empty(ws_need, dtype=torch.uint8, device="cuda:0") for _ in range(self.nstreams)]
+        self.flops_cola = sum(algo_flops_cola(self.T, p.d_in, p.d_out, self.r) for p in self.projs)
+        self.flops_dense = sum(algo_flops_dense(self.T, p.d_in, p.d_out) for p in self.projs)
+        self.flops_infer = sum(algo_flops_cola_fwd(self.T, p.d_in, p.d_out, self.r) for p in self.projs)
+
+    def spread(self, items, fwd, bwd=None, dense=False):
+        """fwd over items in order, then bwd in reverse order; each item on
+        the stream `assign_streams` gives it, with that stream's workspace."""
+        import torch
+        main = torch.cuda.current_stream()
+        for st in self.streams[1:]:
+            st.wait_stream(main)
+        where = assign_streams([proj_work(x, dense) for x in items], self.nstreams)
+        order = list(enumerate(items))
+        phases = [(fwd, order)] + ([(bwd, order[::-1])] if bwd is not None else [])
+        for phase, seq in phases:
+            for i, p in seq:
+                k = where[i]
+                if k == 0:
+                    phase(p, self.wss[0])
+                else:
+                    with torch.cuda.stream(self.streams[k]):
+                        phase(p, self.wss[k])
+        for st in self.streams[1:]:
+            main.wait_stream(st)
+
+    def step(self, mode):
+        if mode == "cola":
+            return lambda: self.spread(self.projs, lambda p, w: p.fwd(w), lambda p, w: p.bwd(w))
+        if mode == "cola_1s":           # one stream: the pass whose launches carry events
+            def run():
+                for p in self.projs:
+                    p.fwd(self.wss[0])
+                for p in reversed(self.projs):
+                    p.bwd(self.wss[0])
+            return run
+        if mode == "cola_m":
+            return lambda: self.spread(self.projs, lambda p, w: p.fwd(w, True), lambda p, w: p.bwd(w, True))
+        if mode == "fused":
+            return lambda: self.spread(self.units, lambda u, w: u.fwd(w), lambda u, w: u.bwd(w))
+        if mode == "dense":
+            return lambda: self.spread(self.projs, lambda p, w: p.dense_step(w), dense=True)
+        if mode == "infer":
+            return lambda: self.spread(self.units, lambda u, w: u.infer(w))
+        if mode == "dense_infer":
+            return lambda: self.spread(self.projs, lambda p, w: p.dense_fwd(w), dense=True)
+        raise ValueError(mode)
+
+
+class SclkSampler:
+    """The GPU's current shader clock (MHz), sampled from the driver's sysfs
+    DPM table while a measurement runs; None where the table is not readable."""
+
+    def __init__(self):
+        import glob
+        self.files = sorted(glob.glob("/sys/class/drm/card*/device/pp_dpm_sclk"))
+        self.vals = []
+        self._stop = None
+
+    def read(self):
+        import re
+        best = None
+        for f in self.files:
+            try:
+                with open(f) as fh:
+                    for line in fh:
+                        if line.rstrip().endswith("*"):
+                            m = re.search(r"(\d+)\s*mhz", line, re.I)
+                            if m:
+                                best = max(best or 0, int(m.group(1)))
+            except OSError:
+                continue
+        return best
+
+    def __enter__(self):
+        import threading
+        self._stop = threading.Event()
+
+        def loop():
+            while not self._stop.is_set():
+                v = self.read()
+                if v is not None:
+                    self.vals.append(v)
+                self._stop.wait(0.01)
+
+        self._t = threading.Thread(target=loop, daemon=True)
+        self._t.start()
+        return self
+
+    def __exit__(self, *exc):
+        self._stop.set()
+        self._t.join()
+
+    def median(self):
+        if not self.vals:
+            return None
+        v = sorted(self.vals)
+        return v[len(v) // 2]
+
+
+def roofline_of(kernels, peak):
+    """The dominant kernel class (largest total time) against its roofline:
+    MFMA-bound when its algorithmic intensity is above the ridge point, else
+    HBM-bound."""
+    dom = max(kernels, key=lambda k: kernels[k]["total_ms"])
+    kd = kernels[dom]
+    ai = kd["flops_per_launch"] / kd["bytes_per_launch"] if kd["bytes_per_launch"] > 0 else float("inf")
+    ridge = peak * 1e12 / (HBM_PEAK_GBS * 1e9)
+    if ai >= ridge:
+        achieved = kd["flops_per_launch"] / (kd["avg_us"] * 1e6)        # TFLOP/s
+        out = {"kernel": dom, "bound": "mfma", "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
+               "frac": round(achieved / peak, 4)}
+    else:
+        achieved = kd["bytes_per_launch"] / (kd["avg_us"] * 1e3)        # GB/s
+        out = {"kernel": dom, "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
+               "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4)}
+    out.update({"avg_us": round(kd["avg_us"], 2), "flops_per_launch": kd["flops_per_launch"],
+                "bytes_per_launch": kd["bytes_per_launch"], "intensity": round(ai, 1), "ridge": round(ridge, 1)})
+    return dom, out
+
+
+def events_pass(cola, step, steps):
+    """`steps` steps with a HIP event pair around every launch (recorded on its
+    launch stream): per-kernel-class durations."""
+    cola.timing_reset()
+    cola.timing_enable(True)
+    try:
+        for _ in range(steps):
+            step()
+    finally:
+        cola.timing_enable(False)
+    table = kernel_table(cola)
+    cola.timing_reset()
+    return table
+
+
+# modes measured per workload (as the configuration list names them; the
+# headline workload measures every mode)
+WORKLOAD_MODES = {1: ("cola", "cola_m"), 2: ("cola", "cola_m"), 3: ("cola", "cola_m", "dense"),
+                  5: ("cola_m", "cola", "dense")}
+
+
+def workload_record(cfg, args):
+    """Compact record of one workload: median step time over `--sub-steps`
+    steps after `--sub-warmup`, per mode, with TFLOP/s, tokens/s, the speedup
+    over dense, the dominant kernel against its roofline, and the clock."""
+    import torch
+    from paper_2502_10940_amd import cola
+    from paper_2502_10940_amd import inputs as I
+    modes = WORKLOAD_MODES[cfg]
+    t0 = time.time()
+    h = Harness(cfg, dense="dense" in modes, cola_m="cola_m" in modes, fused=False, nstreams=args.streams)
+    setup = time.time() - t0
+    peak = BF16_PEAK_TFLOPS if h.dtype == "bf16" else FP32_PEAK_TFLOPS
+    rec = {"workload": h.w["name"], "dtype": h.dtype, "tokens": h.T, "steps": args.sub_steps,
+           "warmup": args.sub_warmup, "timing": "median per-step HIP events", "modes": {}}
+    with SclkSampler() as sc:
+        for mode in modes:
+            ms = timed_steps_median(h.step(mode), args.sub_steps, args.sub_warmup)
+            fl = h.flops_dense if mode == "dense" else h.flops_cola
+            rec["modes"][mode] = {"ms_per_step": round(ms, 4), "tflops": round(fl / (ms * 1e9), 2),
+                                  "pct_of_peak": round(100.0 * fl / (ms * 1e9) / peak, 2),
+                                  "tokens_per_s": round(h.T / (ms / 1e3), 1)}
+    rec["sclk_mhz"] = sc.median()
+    if "dense" in rec["modes"]:
+        for mode in modes:
+            if mode != "dense":
+                rec["modes"][mode]["speedup_vs_dense"] = round(rec["modes"]["dense"]["ms_per_step"] /
+                                                               rec["modes"][mode]["ms_per_step"], 3)
+    main_mode = modes[0]
+    kern = events_pass(cola, h.step("cola_1s") if main_mode == "cola" else h.step(main_mode), 3)
+    if kern:
+        dom, rec["roofline"] = roofline_of(kern, peak)
+    rec["setup_s"] = round(setup, 1)
+    del h
+    torch.cuda.empty_cache()
+    return rec
+
+
+def block_record(cfg, args):
+    """The decoder block (cola_block_fwd + cola_block_bwd: norms, attention,
+    gated product and the seven CoLA projections) at the workload's shape, in
+    CoLA and in CoLA-M: median step time, tokens/s, the saved bytes of each
+    mode and the recompute overhead."""
+    import torch
+    from paper_2502_10940_amd import cola
+    from paper_2502_10940_amd import inputs as I
+    w = I.WORKLOADS[cfg]
+    L = I.SEQ_LEN
+    n_seq, d, ffn, r, heads = w["T"] // L, w["d"], w["ffn"], w["r"], I.HEADS[cfg]
+    T = n_seq * L
+    ins = I.block_inputs(cfg, n_seq, L, d, ffn, r)
+    dev = lambda a: torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).to("cuda:0").view(torch.bfloat16)
+    wts = {k: dev(ins[k].store) for k in cola.BLOCK_PARAMS}
+    x0, dx2 = dev(ins["x0"].store), dev(ins["dx2"].store)
+    x2 = torch.empty_like(x0)
+    dx0 = torch.empty_like(x0)
+    grads = {k: torch.empty(v.shape, dtype=torch.float32, device="cuda:0") for k, v in wts.items()}
+    descs = {m: cola.block_desc(n_seq, L, d, ffn, heads, r, "silu", m == "cola_m") for m in ("cola", "cola_m")}
+    saved_b = {m: cola.block_saved_bytes(descs[m]) for m in descs}
+    ws_b = max(cola.block_workspace_bytes(descs[m], p) for m in descs for p in (0, 1))
+    saved = torch.empty(max(saved_b.values()), dtype=torch.uint8, device="cuda:0")
+    ws = torch.empty(ws_b, dtype=torch.uint8, device="cuda:0")
+
+    def step(m):
+        def run():
+            cola.block_fwd(descs[m], wts, x0, x2, saved, ws, saved_b[m], ws_b)
+            cola.block_bwd(descs[m], wts, x0, saved, dx2, dx0, grads, ws, saved_b[m], ws_b)
+        return run
+
+    shapes = [(d, d)] * 4 + [(d, ffn)] * 2 + [(ffn, d)]
+    lin = sum(algo_flops_cola(T, a, b, r) for a, b in shapes)
+    pairs = L * (L + 1) / 2
+    attn = 12.0 * pairs * d * n_seq                     # causal: 4 (fwd) + 8 (bwd) flops per pair and element
+    rec = {"workload": f"decoder block at the {w['name']}, heads={heads}, seq_len={L}",
+           "tokens": T, "steps": args.sub_steps, "warmup": args.sub_warmup,
+           "flops_per_step": {"projections": lin, "attention_causal": attn},
+           "saved_bytes": dict(saved_b), "input_bytes": 2 * T * d, "modes": {}}
+    with SclkSampler() as sc:
+        for m in ("cola", "cola_m"):
+            ms = timed_steps_median(step(m), args.sub_steps, args.sub_warmup)
+            rec["modes"][m] = {"ms_per_step": round(ms, 4), "tokens_per_s": round(T / (ms / 1e3), 1),
+                               "tflops": round((lin + attn) / (ms * 1e9), 2)}
+    rec["sclk_mhz"] = sc.median()
+    # CoLA-M's activation memory against CoLA's, the caller's x0 counted in both
+    rec["cola_m_memory_ratio"] = round((saved_b["cola_m"] + 2 * T * d) / (saved_b["cola"] + 2 * T * d), 4)
+    rec["cola_m_overhead"] = round(rec["modes"]["cola_m"]["ms_per_step"] / rec["modes"]["cola"]["ms_per_step"] - 1,
+                                   4)
+    kern = events_pass(cola, step("cola_m"), 2)
+    rec["cola_m_kernels_ms_per_step"] = {k: round(v["total_ms"] / 2, 4) for k, v in kern.items()}
+    del saved, ws
+    torch.cuda.empty_cache()
+    return rec
+
+
+def library_baseline(args):
+    """hipBLASLt through torch.matmul (bf16 in, fp32 accumulate) on the GEMM
+    shapes of the headline workload's CoLA steps and dense layers, for
+    comparison with the library's own kernels: median of 20 launches each."""
+    import torch
+    from paper_2502_10940_amd import inputs as I
+    w = I.WORKLOADS[args.workload]
+    T, r = w["T"], w["r"]
+    shapes = {}
+    for name, idx, d_in, d_out in I.projections(args.workload):
+        # (M, N, K): the six CoLA GEMMs and the three dense ones
+        for step, mnk in (("K1 Z=X A^T", (T, r, d_in)), ("K2 Y=H B^T", (T, d_out, r)),
+                          ("K3 dH=dY B", (T, r, d_out)), ("K4 dX=dZ A", (T, d_in, r)),
+                          ("K5 dA=dZ^T X", (r, d_in, T)), ("K6 dB=dY^T H", (d_out, r, T)),
+                          ("D1 Y=X W^T", (T, d_out, d_in)), ("D2 dX=dY W", (T, d_in, d_out)),
+                          ("D3 dW=dY^T X", (d_out, d_in, T))):
+            shapes.setdefault((step, mnk), 0)
+            shapes[(step, mnk)] += 1
+    out = {"library": "hipBLASLt (torch.matmul, bf16)", "workload": w["name"], "shapes": []}
+    for (step, (M, N, K)), count in sorted(shapes.items()):
+        a = torch.randn(M, K, device="cuda:0", dtype=torch.bfloat16)
+        b = torch.randn(K, N, device="cuda:0", dtype=torch.bfloat16)
+        ms = timed_steps_median(lambda: torch.matmul(a, b), 20, 5)
+        out["shapes"].append({"step": step, "M": M, "N": N, "K": K, "projections": count, "ms": round(ms, 4),
+                              "tflops": round(2.0 * M * N * K / (ms * 1e9), 1)})
+        del a, b
+    print(json.dumps(out), flush=True)
+
+
 def main():
     args = parse()
     if args.traffic_from:
@@ -406,105 +708,52 @@ def main():
         copy_calibration()
         return
     cola.lib()
+    if args.library_baseline:
+        library_baseline(args)
+        return
     w = I.WORKLOADS[args.workload]
     dtype = w["dtype"]
     T, r = w["T"], w["r"]
     do_dense = not args.no_dense and args.only in (None, "dense")
     do_m = not args.no_cola_m and args.only in (None, "cola_m")
     do_cola = args.only in (None, "cola")
-    t0 = time.time()
-    projs = [Projection(args.workload, name, idx, d_in, d_out, r, T, dtype, do_dense, do_m)
-             for name, idx, d_in, d_out in I.projections(args.workload)]
     do_fused = not args.no_fused and args.only is None and args.workload != 1
-    units = []          # the fused block: groups for same-input projections, single layers otherwise
-    if do_fused:
-        by = {p.name: p for p in projs}
-        units = [Group([by["q"], by["k"], by["v"]], dtype), by["o"], Group([by["gate"], by["up"]], dtype),
-                 by["down"]]
-    ws_need = max([p.ws_need for p in projs] + [u.ws_need for u in units if isinstance(u, Group)])
-    ws = torch.empty(ws_need, dtype=torch.uint8, device="cuda:0")
-    # independent projections spread over several HIP streams (default
-    # priority), each with its own workspace, balanced by work: a projection
-    # runs its forward and backward on one stream, and one kernel's ramp-up
-    # overlaps another stream's drain.  The step still starts and ends on the
-    # current stream.
-    nstreams = max(1, args.streams)
-    streams = [None] + [torch.cuda.Stream() for _ in range(nstreams - 1)]
-    wss = [ws] + [torch.empty(ws_need, dtype=torch.uint8, device="cuda:0") for _ in range(nstreams - 1)]
+    t0 = time.time()
+    h = Harness(args.workload, do_dense, do_m, do_fused, args.streams)
     setup_s = time.time() - t0
-
-    def spread(items, fwd, bwd=None, dense=False):
-        """fwd over items in order, then bwd in reverse order; each item on
-        the stream `assign_streams` gives it, with that stream's workspace."""
-        main = torch.cuda.current_stream()
-        for st in streams[1:]:
-            st.wait_stream(main)
-        where = assign_streams([proj_work(x, dense) for x in items], nstreams)
-        order = list(enumerate(items))
-        phases = [(fwd, order)] + ([(bwd, order[::-1])] if bwd is not None else [])
-        for phase, seq in phases:
-            for i, p in seq:
-                k = where[i]
-                if k == 0:
-                    phase(p, wss[0])
-                else:
-                    with torch.cuda.stream(streams[k]):
-                        phase(p, wss[k])
-        for st in streams[1:]:
-            main.wait_stream(st)
-
-    def step_cola_1s():
-        for p in projs:
-            p.fwd(ws)
-        for p in reversed(projs):
-            p.bwd(ws)
-
-    def step_cola():
-        spread(projs, lambda p, w: p.fwd(w), lambda p, w: p.bwd(w))
-
-    def step_cola_m():
-        spread(projs, lambda p, w: p.fwd(w, True), lambda p, w: p.bwd(w, True))
-
-    def step_fused():
-        spread(units, lambda u, w: u.fwd(w), lambda u, w: u.bwd(w))
-
-    def step_dense():
-        spread(projs, lambda p, w: p.dense_step(w), dense=True)
-
-    def step_infer():
-        spread(units, lambda u, w: u.infer(w))
-
-    def step_dense_infer():
-        spread(projs, lambda p, w: p.dense_fwd(w), dense=True)
-
-    flops_cola = sum(algo_flops_cola(T, p.d_in, p.d_out, r) for p in projs)
-    flops_dense = sum(algo_flops_dense(T, p.d_in, p.d_out) for p in projs)
+    projs = h.projs
+    flops_cola, flops_dense = h.flops_cola, h.flops_dense
     peak = BF16_PEAK_TFLOPS if dtype == "bf16" else FP32_PEAK_TFLOPS
 
     res = {}
     kernels = {}
-    if do_cola:
-        # the headline: exactly K steps as a caller runs them, no per-kernel events
-        cola.timing_enable(False)
-        res["cola"] = timed_steps(step_cola, args.steps, args.warmup)
-        # then K more steps with a HIP event pair around every launch (recorded on
-        # the launch stream): per-kernel durations for the roofline and the table
-        cola.timing_reset()
-        cola.timing_enable(True)
-        res["cola_events"] = timed_steps(step_cola_1s, args.steps, 0)
-        cola.timing_enable(False)
-        kernels = kernel_table(cola)
-    # the headline mode: total time of exactly K steps / K; the others: median step
-    if do_m:
-        res["cola_m"] = (timed_steps if not do_cola else timed_steps_median)(step_cola_m, args.steps, args.warmup)
-    if do_dense:
-        res["dense"] = (timed_steps if not (do_cola or do_m) else timed_steps_median)(step_dense, args.steps,
-                                                                                     args.warmup)
-    if do_fused:
-        res["fused"] = timed_steps_median(step_fused, args.steps, args.warmup)
-        res["infer"] = timed_steps_median(step_infer, args.steps, args.warmup)
+    sampler = SclkSampler()
+    with sampler:
+        if do_cola:
+            # the headline: exactly K steps as a caller runs them, no per-kernel events
+            cola.timing_enable(False)
+            res["cola"] = timed_steps(h.step("cola"), args.steps, args.warmup)
+            # the median of per-step times over max(K, 50) steps after 10 warm-up
+            res["cola_median"] = timed_steps_median(h.step("cola"), max(args.steps, 50), 10)
+            # then K more steps with a HIP event pair around every launch (recorded on the
+            # launch stream): per-kernel durations for the roofline and the table
+            cola.timing_reset()
+            cola.timing_enable(True)
+            res["cola_events"] = timed_steps(h.step("cola_1s"), args.steps, 0)
+            cola.timing_enable(False)
+            kernels = kernel_table(cola)
+        # the headline mode: total time of exactly K steps / K; the others: median step
+        if do_m:
+            res["cola_m"] = (timed_steps if not do_cola else timed_steps_median)(h.step("cola_m"), args.steps,
+                                                                                 args.warmup)
         if do_dense:
-            res["dense_infer"] = timed_steps_median(step_dense_infer, args.steps, args.warmup)
+            res["dense"] = (timed_steps if not (do_cola or do_m) else timed_steps_median)(h.step("dense"),
+                                                                                         args.steps, args.warmup)
+        if do_fused:
+            res["fused"] = timed_steps_median(h.step("fused"), args.steps, args.warmup)
+            res["infer"] = timed_steps_median(h.step("infer"), args.steps, args.warmup)
+            if do_dense:
+                res["dense_infer"] = timed_steps_median(h.step("dense_infer"), args.steps, args.warmup)
 
     main_mode = "cola" if do_cola else ("cola_m" if do_m else "dense")
     ms = res[main_mode]
@@ -528,10 +777,20 @@ def main():
         "config": {"workload": w["name"], "tokens": T, "d": w["d"], "ffn": w["ffn"], "rank": r,
                    "projections": [p.name for p in projs], "act": "silu", "mode": main_mode,
                    "step": "fwd of all projections, then bwd in reverse order",
-                   "streams": nstreams},
+                   "streams": h.nstreams},
         "pct_of_bf16_mfma_peak": round(100.0 * value / peak, 2),
         "tokens_per_s": round(T / (ms / 1e3), 1),
+        "sclk_mhz": sampler.median(),
     }
+    if args.workload == 4 and main_mode == "cola":
+        # the target: 60 % of the bf16 dense MFMA peak on this block
+        target_ms = flops_cola / (0.6 * peak * 1e9)
+        out["target"] = {"pct_of_peak": 60.0, "ms_per_step": round(target_ms, 4),
+                         "gap": round(ms / target_ms, 3)}
+    if "cola_median" in res:
+        out["median_ms_per_step"] = {"steps": max(args.steps, 50), "warmup": 10,
+                                     "ms": round(res["cola_median"], 4),
+                                     "tflops": round(flops_cola / (res["cola_median"] * 1e9), 2)}
     if "cola_events" in res:
         out["cola_with_kernel_events"] = {"ms_per_step": round(res["cola_events"], 4),
                                           "tflops": round(flops_cola / (res["cola_events"] * 1e9), 2),
@@ -558,38 +817,27 @@ def main():
             out["fused_block"]["speedup_vs_dense"] = round(res["dense"] / res["fused"], 3)
     if "infer" in res:
         # forward only, nothing kept for a backward pass; grouped as fused_block
-        fl = sum(algo_flops_cola_fwd(T, p.d_in, p.d_out, r) for p in projs)
         out["inference"] = {"ms_per_step": round(res["infer"], 4),
-                            "tflops": round(fl / (res["infer"] * 1e9), 2),
+                            "tflops": round(h.flops_infer / (res["infer"] * 1e9), 2),
                             "tokens_per_s": round(T / (res["infer"] / 1e3), 1)}
         if "dense_infer" in res:
             out["inference"]["dense_tokens_per_s"] = round(T / (res["dense_infer"] / 1e3), 1)
             out["inference"]["speedup_vs_dense"] = round(res["dense_infer"] / res["infer"], 3)
     if kernels:
-        dom = max(kernels, key=lambda k: kernels[k]["total_ms"])
-        kd = kernels[dom]
-        traffic = load_traffic(dom)
-        # the kernel's algorithmic intensity against the ridge point decides the bound
-        ai = kd["flops_per_launch"] / kd["bytes_per_launch"] if kd["bytes_per_launch"] > 0 else float("inf")
-        ridge = peak * 1e12 / (HBM_PEAK_GBS * 1e9)
-        if ai >= ridge:
-            achieved = kd["flops_per_launch"] / (kd["avg_us"] * 1e6)   # TFLOP/s
-            out["roofline"] = {"kernel": dom, "bound": "mfma", "achieved": round(achieved, 2),
-                               "peak": peak, "unit": "TFLOP/s", "frac": round(achieved / peak, 4)}
-        else:
-            achieved = kd["bytes_per_launch"] / (kd["avg_us"] * 1e3)   # GB/s
-            out["roofline"] = {"kernel": dom, "bound": "hbm", "achieved": round(achieved, 1),
-                               "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4)}
-        out["roofline"].update({"traffic": traffic, "avg_us": round(kd["avg_us"], 2),
-                                "flops_per_launch": kd["flops_per_launch"],
-                                "bytes_per_launch": kd["bytes_per_launch"], "intensity": round(ai, 1),
-                                "ridge": round(ridge, 1)})
+        dom, out["roofline"] = roofline_of(kernels, peak)
+        out["roofline"]["traffic"] = load_traffic(dom)
         out["kernels"] = {k: {kk: (round(vv, 3) if isinstance(vv, float) else vv)
                               for kk, vv in v.items()} for k, v in kernels.items()}
     if not args.no_cpu_baseline and main_mode != "dense":
         out["cpu_baseline"] = cpu_baseline(projs, T, min(args.cpu_tokens, T))
         out["cpu_baseline"]["value"] = round(out["cpu_baseline"]["value"], 6)
     out["setup_s"] = round(setup_s, 1)
+    del h, projs
+    torch.cuda.empty_cache()
+    if not args.no_block and args.only is None and args.workload != 1:
+        out["block"] = block_record(args.workload, args)
+    if not args.no_workloads and args.only is None:
+        out["workloads"] = {str(c): workload_record(c, args) for c in (1, 2, 3, 5) if c != args.workload}
     print(json.dumps(out), flush=True)
 
 

@@ -32,6 +32,7 @@
 #include <math.h>
 
 #include "internal.hpp"
+#include "block.hpp"
 #include "device_math.hpp"
 
 namespace cola {

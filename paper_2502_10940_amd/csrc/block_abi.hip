@@ -23,6 +23,7 @@
 
 #include "../../include/cola.h"
 #include "internal.hpp"
+#include "block.hpp"
 
 using namespace cola;
 

@@ -5,6 +5,7 @@
 // H that CoLA-M recomputes, App. C).  All HBM-bound: one pass over the
 // operands, 16-byte accesses on aligned interior chunks.
 #include "internal.hpp"
+#include "block.hpp"
 #include "device_math.hpp"
 
 namespace cola {

@@ -21,6 +21,7 @@
 
 #include "../../include/cola.h"
 #include "internal.hpp"
+#include "block.hpp"
 
 using namespace cola;
 
