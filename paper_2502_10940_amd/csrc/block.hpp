@@ -17,7 +17,13 @@ struct AttnShape {
     int n_seq, seq_len, heads, head_dim;
     int64_t ld;
     float rope_base;
+    const float* rope;    // the (cos, sin) table of launch_attn_rope_table
 };
+// The rotation table [seq_len][head_dim / 2] of (cos, sin) pairs that the
+// attention kernels read: attn_rope_table_floats floats, filled by
+// launch_attn_rope_table before them on the same stream.
+int64_t attn_rope_table_floats(int seq_len, int head_dim);
+hipError_t launch_attn_rope_table(const AttnShape& sh, float* rope, hipStream_t s);
 // att = softmax(rope(q) rope(k)^T / sqrt(hd), causal) v; lse = log2-sum-exp
 // of the scores scaled by log2(e) / sqrt(hd).
 hipError_t launch_attn_fwd(const AttnShape& sh, const void* q, const void* k, const void* v, void* att, float* lse,

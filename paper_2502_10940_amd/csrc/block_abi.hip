@@ -143,6 +143,7 @@ size_t smax(size_t a, size_t b) { return a > b ? a : b; }
 // ---- workspace layouts ----
 struct Ws {
     size_t sub, sub_bytes;                 // the sub-calls' workspace
+    size_t rope;                           // the attention's rotation table
     size_t tmp;                            // forward: o and y before their residual sums  [T][d]
     // transients of CoLA-M (forward: everything CoLA would keep; backward: the recomputes)
     size_t a, q, k, v, att, lse, b, hqkv, hgu, gt, up, m;
@@ -168,6 +169,7 @@ Ws plan_ws(const Blk& b, int phase) {
         w.sub_bytes = smax(smax(cola_group_workspace_bytes(&g1, 0), cola_group_workspace_bytes(&g2, 0)),
                            smax(cola_workspace_bytes(&c1, 0), cola_workspace_bytes(&c2, 0)));
         w.sub = take(w.sub_bytes);
+        w.rope = take((size_t)attn_rope_table_floats((int)b.L, (int)b.hd) * 4);
         w.tmp = take(nd);
         if (b.m) {
             w.a = take(nd); w.q = take(nd); w.k = take(nd); w.v = take(nd); w.att = take(nd); w.lse = take(nl);
@@ -180,6 +182,7 @@ Ws plan_ws(const Blk& b, int phase) {
         w.sub_bytes = smax(smax(cola_group_workspace_bytes(&g1, 1), cola_group_workspace_bytes(&g2, 1)),
                            smax(cola_workspace_bytes(&c1, 1), cola_workspace_bytes(&c2, 1)));
         w.sub = take(w.sub_bytes);
+        w.rope = take((size_t)attn_rope_table_floats((int)b.L, (int)b.hd) * 4);
         w.dx1 = take(nd); w.datt = take(nd); w.dq = take(nd); w.dk = take(nd); w.dv = take(nd);
         w.db = take(nd); w.da = take(nd); w.dm = take(nf); w.dgt = take(nf); w.du = take(nf);
         w.D = take(nl);
@@ -199,6 +202,7 @@ Ws plan_ws(const Blk& b, int phase) {
 struct Ctx {
     const Blk& b;
     hipStream_t s;
+    const float* rope;      // the rotation table in the workspace
 };
 
 int chk(hipError_t e, const char* where) { return e == hipSuccess ? COLA_OK : set_hip_error(e, where); }
@@ -235,18 +239,24 @@ int ew(const Ctx& c, int op, int64_t width, const void* a, int64_t lda, const vo
                "pointwise");
 }
 
-AttnShape attn_shape(const Blk& b) {
+AttnShape attn_shape(const Blk& b, const float* rope) {
     AttnShape a{};
     a.n_seq = (int)b.n_seq; a.seq_len = (int)b.L; a.heads = (int)b.heads; a.head_dim = (int)b.hd;
-    a.ld = b.d; a.rope_base = b.base;
+    a.ld = b.d; a.rope_base = b.base; a.rope = rope;
     return a;
+}
+
+int rope_table(const Ctx& c, float* rope) {
+    const AttnShape sh = attn_shape(c.b, rope);
+    return chk(timed_fn(COLA_KC_POINTWISE, 0.0, 8.0 * (double)c.b.L * c.b.hd / 2.0, c.s,
+                        [&] { return launch_attn_rope_table(sh, rope, c.s); }), "rope_table");
 }
 
 int attn_fwd(const Ctx& c, const void* q, const void* k, const void* v, void* att, float* lse) {
     const Blk& b = c.b;
     const double flops = 4.0 * causal_pairs(b) * (double)b.hd * (double)b.heads * (double)b.n_seq;
     const double bytes = 2.0 * (double)b.T * b.d * 4.0 + 4.0 * (double)b.T * b.heads;
-    const AttnShape sh = attn_shape(b);
+    const AttnShape sh = attn_shape(b, c.rope);
     return chk(timed_fn(COLA_KC_ATTN_FWD, flops, bytes, c.s, [&] { return launch_attn_fwd(sh, q, k, v, att, lse, c.s); }),
                "attn_fwd");
 }
@@ -256,7 +266,7 @@ int attn_bwd(const Ctx& c, const void* q, const void* k, const void* v, const vo
     const Blk& b = c.b;
     const double flops = 8.0 * causal_pairs(b) * (double)b.hd * (double)b.heads * (double)b.n_seq;
     const double bytes = 2.0 * (double)b.T * b.d * 8.0 + 8.0 * (double)b.T * b.heads;
-    const AttnShape sh = attn_shape(b);
+    const AttnShape sh = attn_shape(b, c.rope);
     return chk(timed_fn(COLA_KC_ATTN_BWD, flops, bytes, c.s,
                         [&] { return launch_attn_bwd(sh, q, k, v, att, lse, dO, dq, dk, dv, D, c.s); }),
                "attn_bwd");
@@ -329,9 +339,10 @@ int cola_block_fwd(const cola_block_desc* desc, const cola_block_weights* w, con
         if (saved_bytes < S.total) return COLA_ERR_WORKSPACE;
         if (W.total > 0 && (!ws || ws_bytes < W.total)) return COLA_ERR_WORKSPACE;
         hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-        const Ctx c{b, s};
         char* sv = static_cast<char*>(saved);
         char* wk = static_cast<char*>(ws);
+        const Ctx c{b, s, reinterpret_cast<const float*>(wk + W.rope)};
+        if ((st = rope_table(c, reinterpret_cast<float*>(wk + W.rope))) != COLA_OK) return st;
         auto SV = [&](int slot) -> char* { return sv + S.off[slot]; };
         // where each activation lives: `saved` (CoLA) or the workspace (CoLA-M)
         char* a = b.m ? wk + W.a : SV(COLA_BLK_A);
@@ -412,9 +423,10 @@ int cola_block_bwd(const cola_block_desc* desc, const cola_block_weights* w, con
         const Ws W = plan_ws(b, 1);
         if (saved_bytes < S.total) return COLA_ERR_WORKSPACE;
         if (!ws || ws_bytes < W.total) return COLA_ERR_WORKSPACE;
-        const Ctx c{b, s};
         const char* sv = static_cast<const char*>(saved);
         char* wk = static_cast<char*>(ws);
+        const Ctx c{b, s, reinterpret_cast<const float*>(wk + W.rope)};
+        if ((st = rope_table(c, reinterpret_cast<float*>(wk + W.rope))) != COLA_OK) return st;
         auto SV = [&](int slot) -> const char* { return sv + S.off[slot]; };
         const char* x1 = SV(COLA_BLK_X1);
         const char* Zqkv = SV(COLA_BLK_Z_QKV);

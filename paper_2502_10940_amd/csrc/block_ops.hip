@@ -184,9 +184,25 @@ __global__ __launch_bounds__(NT) void rmsnorm_bwd_kernel(const uint16_t* x, cons
     }
 }
 
+// First stage of the gain-gradient sum: out1[g][c] = sum of partial rows
+// g * GROUP .. g * GROUP + GROUP - 1 of column c, in row order (one thread
+// per column, coalesced rows); the second stage sums the groups in order.
+constexpr int GROUP = 64;
+__global__ __launch_bounds__(NT) void colsum_kernel(const float* __restrict__ part, int64_t S, int64_t d,
+                                                    float* __restrict__ out1) {
+    const int64_t col = (int64_t)blockIdx.x * NT + threadIdx.x;
+    if (col >= d) return;
+    const int64_t s0 = (int64_t)blockIdx.y * GROUP;
+    const int64_t s1 = min(S, s0 + GROUP);
+    float acc = 0.0f;
+    for (int64_t r = s0; r < s1; ++r) acc += part[r * d + col];
+    out1[(int64_t)blockIdx.y * d + col] = acc;
+}
+
 int64_t rows_per_workgroup(int64_t T) {
-    // at most 1024 partial rows; whole waves of rows per workgroup
-    int64_t r = (T + 1023) / 1024;
+    // at most 4096 partial rows (enough workgroups to keep every CU's loads
+    // in flight); whole waves of rows per workgroup
+    int64_t r = (T + 4095) / 4096;
     r = (r + NWAVE - 1) / NWAVE * NWAVE;
     return r < NWAVE ? NWAVE : r;
 }
@@ -275,7 +291,14 @@ hipError_t rms_bwd_nc(const void* x, const void* g, const void* dy, const void* 
                        static_cast<uint16_t*>(out), partials, T, (int)d, ld, eps, rpw);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    return launch_reduce_splits(partials, (int)nwg, d, dg, d, s);
+    // dg = sum over the nwg partial rows: groups of GROUP rows, then the groups
+    const int64_t ng = (nwg + GROUP - 1) / GROUP;
+    float* groups = partials + nwg * d;
+    hipLaunchKernelGGL(colsum_kernel, dim3((unsigned)((d + NT - 1) / NT), (unsigned)ng), dim3(NT), 0, s, partials,
+                       nwg, d, groups);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    return launch_reduce_splits(groups, (int)ng, d, dg, d, s);
 }
 
 }  // namespace
@@ -295,7 +318,8 @@ hipError_t launch_rmsnorm_fwd(const void* x, const void* res, void* xsum, const 
 int64_t rmsnorm_bwd_partials(int64_t T, int64_t d) {
     if (T <= 0) return 0;
     const int64_t rpw = rows_per_workgroup(T);
-    return (T + rpw - 1) / rpw * d;
+    const int64_t nwg = (T + rpw - 1) / rpw;
+    return (nwg + (nwg + GROUP - 1) / GROUP) * d;       // the workgroups' rows, then the group sums
 }
 
 hipError_t launch_rmsnorm_bwd(const void* x, const void* g, const void* dy, const void* res_grad, void* out,
