@@ -175,37 +175,56 @@ struct RowTile {
     }
 };
 
-// Stage STG rows (sequence positions p0 .. p0 + STG - 1, zeros from L on) of
-// one head into a row-major LDS tile, rotated by position when ROT.  Each
-// thread moves pairs of chunks (c, c + HD / 16): elements i and i + HD/2.
-template <int HD, bool ROT>
-__device__ __forceinline__ void stage(char* rt, const uint16_t* base, int64_t ld, int64_t seq_row0, int p0, int L,
-                                      int col0, const float* rope) {
-    constexpr int HC = HD / 16;              // chunk pairs per row
-    constexpr int PAIRS = STG * HC;
+// STG rows (sequence positions p0 .. p0 + STG - 1, zeros from L on) of one
+// head on their way into a row-major LDS tile: load() brings this thread's
+// share into registers (issued a stage ahead, so the loads fly during the
+// current stage's MFMAs), put() rotates them by position when ROT and writes
+// them to LDS.  Each thread moves pairs of chunks (c, c + HD / 16):
+// elements i and i + HD/2.
+template <int HD>
+struct Stage {
+    static constexpr int HC = HD / 16;                 // chunk pairs per row
+    static constexpr int NI = STG * HC / (NW * 64);    // pairs per thread
+    u32x4 a[NI], b[NI];
+    int p0;
+
+    __device__ __forceinline__ void load(const uint16_t* base, int64_t ld, int64_t seq_row0, int p, int L,
+                                         int col0) {
+        p0 = p;
 #pragma unroll
-    for (int it = 0; it < PAIRS / (NW * 64); ++it) {
-        const int i = threadIdx.x + NW * 64 * it;
-        const int row = i / HC;
-        const int c = i % HC;
-        const int pos = p0 + row;
-        const bool ok = pos < L;
-        u32x4 a = load8(base, ld, seq_row0 + pos, ok, col0 + 8 * c);
-        u32x4 b = load8(base, ld, seq_row0 + pos, ok, col0 + 8 * (c + HC));
-        if constexpr (ROT) {
-            if (ok) {
-                float lo[8], hi[8];
-                unpack8(a, lo);
-                unpack8(b, hi);
-                rope8<HD>(lo, hi, 8 * c, pos, rope);
-                a = pack8(lo);
-                b = pack8(hi);
-            }
+        for (int it = 0; it < NI; ++it) {
+            const int i = threadIdx.x + NW * 64 * it;
+            const int row = i / HC, c = i % HC;
+            const int pos = p0 + row;
+            const bool ok = pos < L;
+            a[it] = load8(base, ld, seq_row0 + pos, ok, col0 + 8 * c);
+            b[it] = load8(base, ld, seq_row0 + pos, ok, col0 + 8 * (c + HC));
         }
-        *reinterpret_cast<u32x4*>(rt + RowTile<HD>::off(row, c)) = a;
-        *reinterpret_cast<u32x4*>(rt + RowTile<HD>::off(row, c + HC)) = b;
     }
-}
+
+    template <bool ROT>
+    __device__ __forceinline__ void put(char* rt, int L, const float* rope) {
+#pragma unroll
+        for (int it = 0; it < NI; ++it) {
+            const int i = threadIdx.x + NW * 64 * it;
+            const int row = i / HC, c = i % HC;
+            const int pos = p0 + row;
+            u32x4 x = a[it], y = b[it];
+            if constexpr (ROT) {
+                if (pos < L) {
+                    float lo[8], hi[8];
+                    unpack8(x, lo);
+                    unpack8(y, hi);
+                    rope8<HD>(lo, hi, 8 * c, pos, rope);
+                    x = pack8(lo);
+                    y = pack8(hi);
+                }
+            }
+            *reinterpret_cast<u32x4*>(rt + RowTile<HD>::off(row, c)) = x;
+            *reinterpret_cast<u32x4*>(rt + RowTile<HD>::off(row, c + HC)) = y;
+        }
+    }
+};
 
 // Row (key or query) of register v of a 32 x 32 accumulator, within its tile.
 __device__ __forceinline__ int acc_row(int v, int hh) { return 8 * (v >> 2) + 4 * hh + (v & 3); }
@@ -293,11 +312,18 @@ __global__ __launch_bounds__(NW * 64) void attn_fwd_kernel(AttnArgs a) {
     float m = -INFINITY, l = 0.0f;
 
     const int kend = min(L, chunk * CHUNK + CHUNK);       // keys any query of the workgroup sees
+    Stage<HD> sk, sv;
+    sk.load(a.k, a.ld, row0, 0, L, col0);
+    sv.load(a.v, a.ld, row0, 0, L, col0);
     for (int k0 = 0; k0 < kend; k0 += STG) {
         __syncthreads();                                   // the previous tiles are consumed
-        stage<HD, true>(kt, a.k, a.ld, row0, k0, L, col0, a.rope);
-        stage<HD, false>(vt, a.v, a.ld, row0, k0, L, col0, a.rope);
+        sk.template put<true>(kt, L, a.rope);
+        sv.template put<false>(vt, L, a.rope);
         __syncthreads();
+        if (k0 + STG < kend) {                             // the next stage's rows fly during this one
+            sk.load(a.k, a.ld, row0, k0 + STG, L, col0);
+            sv.load(a.v, a.ld, row0, k0 + STG, L, col0);
+        }
 #pragma unroll
         for (int sub = 0; sub < 2; ++sub) {
             const int kb = k0 + 32 * sub;
@@ -385,10 +411,16 @@ __global__ __launch_bounds__(NW * 64) void attn_bwd_dq_kernel(AttnArgs a) {
 #pragma unroll
     for (int t = 0; t < NT; ++t) dq[t] = f32x16{};
     const int kend = min(L, chunk * CHUNK + CHUNK);
+    // (no prefetch of the next stage here: its registers would cost occupancy)
     for (int k0 = 0; k0 < kend; k0 += STG) {
         __syncthreads();
-        stage<HD, true>(kt, a.k, a.ld, row0, k0, L, col0, a.rope);
-        stage<HD, false>(vt, a.v, a.ld, row0, k0, L, col0, a.rope);
+        {
+            Stage<HD> sk, sv;
+            sk.load(a.k, a.ld, row0, k0, L, col0);
+            sv.load(a.v, a.ld, row0, k0, L, col0);
+            sk.template put<true>(kt, L, a.rope);
+            sv.template put<false>(vt, L, a.rope);
+        }
         __syncthreads();
 #pragma unroll
         for (int sub = 0; sub < 2; ++sub) {
@@ -452,10 +484,16 @@ __global__ __launch_bounds__(NW * 64) void attn_bwd_dkdv_kernel(AttnArgs a) {
         dv[t] = f32x16{};
     }
     // query blocks from the workgroup's first key (rounded down to a stage) to the sequence end
+    // (no prefetch of the next stage here: its registers would cost occupancy)
     for (int q0 = (chunk * CHUNK) / STG * STG; q0 < L; q0 += STG) {
         __syncthreads();
-        stage<HD, true>(qt, a.q, a.ld, row0, q0, L, col0, a.rope);
-        stage<HD, false>(dt, a.dO, a.ld, row0, q0, L, col0, a.rope);
+        {
+            Stage<HD> sq, sd;
+            sq.load(a.q, a.ld, row0, q0, L, col0);
+            sd.load(a.dO, a.ld, row0, q0, L, col0);
+            sq.template put<true>(qt, L, a.rope);
+            sd.template put<false>(dt, L, a.rope);
+        }
         if (threadIdx.x < STG) {
             const int qpos = q0 + threadIdx.x;
             const bool ok = qpos < L;
