@@ -52,7 +52,7 @@ def parse():
                     help="tokens per projection in the oracle's CPU sample")
     ap.add_argument("--no-fused", action="store_true",
                     help="skip the block with same-input projections grouped (q,k,v and gate,up)")
-    ap.add_argument("--only", choices=["cola", "cola_m", "dense"], default=None,
+    ap.add_argument("--only", choices=["cola", "cola_m", "dense", "block"], default=None,
                     help="run only one mode (profiling)")
     ap.add_argument("--no-block", action="store_true", help="skip the decoder-block record")
     ap.add_argument("--no-workloads", action="store_true", help="skip the records of the other workloads")
@@ -75,6 +75,9 @@ KERNEL_TAGS = {0: "fwd_z_sigma", 1: "fwd_y", 2: "bwd_dz", 3: "bwd_dx", 4: "bwd_d
 
 
 def copy_calibration():
+    """Dispatches of known HBM traffic for scaling the counters: a plain 1 GiB
+    device copy (reads and writes COPY_BYTES), then a read-only pass, a sum
+    over the same 1 GiB (reads COPY_BYTES, writes a few bytes), 3 times each."""
     import torch
     src = torch.empty(COPY_BYTES, dtype=torch.uint8, device="cuda:0").fill_(1)
     dst = torch.empty_like(src)
@@ -82,7 +85,11 @@ def copy_calibration():
     for _ in range(3):
         dst.copy_(src)
     torch.cuda.synchronize()
-    print(json.dumps({"copy_calibration_bytes": COPY_BYTES, "repeats": 3}), flush=True)
+    f = src.view(torch.float32)
+    for _ in range(3):
+        f.sum()
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_calibration_bytes": COPY_BYTES, "repeats": 3, "read_only_pass": "sum"}), flush=True)
 
 
 def _pmc_rows(path, counter):
@@ -113,6 +120,11 @@ def traffic_summary(fetch_csv, write_csv, copy_fetch_csv, copy_write_csv):
 
     ff = copy_factor(copy_fetch_csv, "FETCH_SIZE")
     fw = copy_factor(copy_write_csv, "WRITE_SIZE")
+    # cross-check of the fetch factor: the read-only pass (a reduction over the
+    # same 1 GiB) in the same counter run
+    ro = [v for name, _, v in _pmc_rows(copy_fetch_csv, "FETCH_SIZE") if "reduce" in name.lower()
+          and v * 1024 > 0.25 * COPY_BYTES]
+    ff_ro = COPY_BYTES / (sorted(ro)[len(ro) // 2] * 1024.0) if ro else None
     per = {}
     for path, counter, scale, key in ((fetch_csv, "FETCH_SIZE", ff, "fetch"),
                                       (write_csv, "WRITE_SIZE", fw, "write")):
@@ -125,7 +137,9 @@ def traffic_summary(fetch_csv, write_csv, copy_fetch_csv, copy_write_csv):
             per.setdefault(cls, {}).setdefault(key, []).append(v * 1024.0 * scale)
     h = kernel_source_hash()
     out = {"_note": "HBM bytes per launch from rocprofv3 FETCH_SIZE + WRITE_SIZE, scaled by a "
-                    "1 GiB copy (fetch factor %.4f, write factor %.4f)" % (ff, fw)}
+                    "1 GiB copy (fetch factor %.4f, write factor %.4f; a read-only 1 GiB pass gives fetch "
+                    "factor %s)" % (ff, fw, "%.4f" % ff_ro if ff_ro else "n/a"),
+           "_fetch_factor": ff, "_write_factor": fw, "_fetch_factor_read_only": ff_ro}
     for cls, d in per.items():
         f = d.get("fetch", [])
         w = d.get("write", [])
@@ -710,6 +724,10 @@ def main():
     cola.lib()
     if args.library_baseline:
         library_baseline(args)
+        return
+    if args.only == "block":
+        # the decoder-block record alone (profiling)
+        print(json.dumps({"block": block_record(args.workload, args)}), flush=True)
         return
     w = I.WORKLOADS[args.workload]
     dtype = w["dtype"]
