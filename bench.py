@@ -58,6 +58,8 @@ def parse():
     ap.add_argument("--no-workloads", action="store_true", help="skip the records of the other workloads")
     ap.add_argument("--sub-steps", type=int, default=50, help="timed steps of the block and workload records")
     ap.add_argument("--sub-warmup", type=int, default=10)
+    ap.add_argument("--per-projection", action="store_true",
+                    help="per-projection kernel-class durations of the workload (event-timed, one stream) and exit")
     ap.add_argument("--library-baseline", action="store_true",
                     help="time hipBLASLt (torch.matmul) on the workload's GEMM shapes and exit")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -705,6 +707,32 @@ def library_baseline(args):
     print(json.dumps(out), flush=True)
 
 
+def per_projection(args):
+    """Kernel-class durations per projection: after 3 warm-up steps, each
+    projection's forward and backward 5 times with an event pair around every
+    launch (one stream).  One JSON line per projection."""
+    import torch
+    from paper_2502_10940_amd import cola
+    h = Harness(args.workload, dense=False, cola_m=False, fused=False, nstreams=1)
+    ws = h.wss[0]
+    step = h.step("cola_1s")
+    for _ in range(3):
+        step()
+    torch.cuda.synchronize()
+    for p in h.projs:
+        cola.timing_reset()
+        cola.timing_enable(True)
+        for _ in range(5):
+            p.fwd(ws)
+            p.bwd(ws)
+        cola.timing_enable(False)
+        t = kernel_table(cola)
+        print(json.dumps({"projection": p.name, "d_in": p.d_in, "d_out": p.d_out, "r": p.r, "T": p.T,
+                          "avg_us": {k: round(v["avg_us"], 1) for k, v in t.items()},
+                          "tflops": {k: round(v["tflops"], 1) for k, v in t.items()}}), flush=True)
+    cola.timing_reset()
+
+
 def main():
     args = parse()
     if args.traffic_from:
@@ -724,6 +752,9 @@ def main():
     cola.lib()
     if args.library_baseline:
         library_baseline(args)
+        return
+    if args.per_projection:
+        per_projection(args)
         return
     if args.only == "block":
         # the decoder-block record alone (profiling)
