@@ -24,7 +24,10 @@ SOURCES = ["gemm_dispatch.hip", "gemm_stream.hip", "gemm_pp.hip", "gemm_f32.hip"
 # Per-source extra flags.  The 256 x 256 kernel's epilogues run over 256
 # accumulators per lane: past the default limit the unroller stops and the
 # accumulators go to scratch memory.
-EXTRA = {"gemm_pp.hip": ["-mllvm", "-pragma-unroll-threshold=500000"]}
+EXTRA = {"gemm_pp.hip": ["-mllvm", "-pragma-unroll-threshold=500000"],
+         # MFMA accumulators in ordinary VGPRs: the attention kernels scale and read
+         # theirs with VALU code between MFMAs (no copies to and from AGPRs)
+         "attention.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
 FLAGS = ["-std=c++17", "-O3", "-fPIC", f"--offload-arch={ARCH}", "-I", INCLUDE, "-I", CSRC,
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
          "-Wall", "-Wno-unused-function"]

@@ -29,6 +29,8 @@ CASES = [
     ("llama60m_two_sequences", 2, 256, 512, 1376, 8, 128, "silu"),
     ("gelu_hd64_L40", 2, 40, 128, 96, 2, 16, "gelu"),
     ("single_token_sequences", 5, 1, 128, 64, 1, 8, "silu"),
+    # longer than the whole-sequence attention kernels take: the staged ones
+    ("hd64_L300_staged_attention", 2, 300, 128, 96, 2, 16, "silu"),
 ]
 
 
