@@ -139,8 +139,53 @@ hipError_t launch_gemm_f32(const GemmArgs& a, hipStream_t s) {
 // ---------------------------------------------------------------------------
 namespace {
 
-// out[i] = sum_k part[k * stride + i] over k = 0 .. splits-1 in that order,
-// by block blk of nblk blocks (grid-stride over float4 groups, scalar tail).
+// The split reduction's fixed order, which depends only on the split count:
+// the partials in chunks of kChunk in split order, each chunk summed in
+// order, then the chunk sums in order (up to kChunk splits: the plain sum in
+// split order).  Two kernels follow it: one thread per output group summing
+// every chunk in turn, and, for split counts above kChunk, kChunkLanes
+// threads per output group summing chunks side by side and combining them in
+// LDS, which keeps several times as many loads in flight when the output is
+// small.
+constexpr int kChunk = 8;
+constexpr int kChunkLanes = 4;
+constexpr int kMaxChunks = 32;
+
+__device__ __forceinline__ float4 add4(float4 a, float4 b) {
+    return make_float4(a.x + b.x, a.y + b.y, a.z + b.z, a.w + b.w);
+}
+__device__ __forceinline__ float add4(float a, float b) { return a + b; }
+
+// Sum of partials k0 .. k1-1 (k1 > k0) of element i; V = float4 (stride in
+// float4 units) or float.
+// (All of a chunk's loads are issued before its sums.)
+template <class V>
+__device__ __forceinline__ V chunk_sum(const V* __restrict__ part, int64_t stride, int64_t i, int k0, int k1) {
+    V v[kChunk];
+#pragma unroll
+    for (int u = 0; u < kChunk; ++u)
+        if (k0 + u < k1) v[u] = part[(int64_t)(k0 + u) * stride + i];
+    V s = v[0];
+#pragma unroll
+    for (int u = 1; u < kChunk; ++u)
+        if (k0 + u < k1) s = add4(s, v[u]);
+    return s;
+}
+
+template <class V>
+__device__ __forceinline__ V ordered_sum(const V* __restrict__ part, int64_t stride, int64_t i, int splits) {
+    V s = chunk_sum(part, stride, i, 0, min(kChunk, splits));
+    for (int k0 = kChunk; k0 < splits; k0 += kChunk) s = add4(s, chunk_sum(part, stride, i, k0, min(k0 + kChunk, splits)));
+    return s;
+}
+
+bool reduce_vec_ok(const float* part, int64_t stride, const float* out) {
+    return (stride & 3) == 0 && (reinterpret_cast<uintptr_t>(part) & 15u) == 0 &&
+           (reinterpret_cast<uintptr_t>(out) & 15u) == 0;
+}
+
+// One thread per output group, block blk of nblk (grid-stride over float4
+// groups, scalar tail).
 __device__ __forceinline__ void reduce_splits_range(const float* __restrict__ part, int splits, int64_t stride,
                                                     float* __restrict__ out, int64_t n, int64_t blk,
                                                     int64_t nblk) {
@@ -150,22 +195,41 @@ __device__ __forceinline__ void reduce_splits_range(const float* __restrict__ pa
     const int64_t step = nblk * blockDim.x;
     int64_t i = blk * blockDim.x + threadIdx.x;
     if (vec) {
-        for (; i < n4; i += step) {
-            float4 s = reinterpret_cast<const float4*>(part)[i];
-            for (int k = 1; k < splits; ++k) {
-                const float4 v = reinterpret_cast<const float4*>(part + (int64_t)k * stride)[i];
-                s.x += v.x; s.y += v.y; s.z += v.z; s.w += v.w;
-            }
-            reinterpret_cast<float4*>(out)[i] = s;
-        }
+        const float4* p4 = reinterpret_cast<const float4*>(part);
+        for (; i < n4; i += step) reinterpret_cast<float4*>(out)[i] = ordered_sum(p4, stride >> 2, i, splits);
         // scalar tail
         i = n4 * 4 + blk * blockDim.x + threadIdx.x;
     }
-    for (; i < n; i += step) {
-        float s = part[i];
-        for (int k = 1; k < splits; ++k) s += part[(int64_t)k * stride + i];
-        out[i] = s;
+    for (; i < n; i += step) out[i] = ordered_sum(part, stride, i, splits);
+}
+
+// kChunkLanes threads per float4 output group (n a multiple of 4, 16-byte
+// aligned rows): 256 / kChunkLanes groups per block.
+__device__ __forceinline__ void reduce_chunks_range(const float* __restrict__ part, int splits, int64_t stride,
+                                                    float* __restrict__ out, int64_t n, int64_t blk) {
+    constexpr int OPB = 256 / kChunkLanes;
+    __shared__ float4 sums[kMaxChunks][OPB];
+    const int j = threadIdx.x / OPB, o = threadIdx.x % OPB;
+    const int64_t i = blk * OPB + o, n4 = n >> 2;
+    const int chunks = (splits + kChunk - 1) / kChunk;
+    const float4* p4 = reinterpret_cast<const float4*>(part);
+    if (i < n4)
+        for (int c = j; c < chunks; c += kChunkLanes)
+            sums[c][o] = chunk_sum(p4, stride >> 2, i, kChunk * c, min(kChunk * c + kChunk, splits));
+    __syncthreads();
+    if (j == 0 && i < n4) {
+        float4 s = sums[0][o];
+        for (int c = 1; c < chunks; ++c) s = add4(s, sums[c][o]);
+        reinterpret_cast<float4*>(out)[i] = s;
     }
+}
+
+__global__ __launch_bounds__(256) void reduce_chunks_kernel(const float* __restrict__ p0, int64_t st0,
+                                                            float* __restrict__ o0, int64_t n0, int64_t g0,
+                                                            const float* __restrict__ p1, int64_t st1,
+                                                            float* __restrict__ o1, int64_t n1, int splits) {
+    if ((int64_t)blockIdx.x < g0) reduce_chunks_range(p0, splits, st0, o0, n0, blockIdx.x);
+    else reduce_chunks_range(p1, splits, st1, o1, n1, (int64_t)blockIdx.x - g0);
 }
 
 __global__ __launch_bounds__(256) void reduce_splits_kernel(const float* __restrict__ part, int splits,
@@ -267,10 +331,24 @@ unsigned grid_for(int64_t work) {
 
 }  // namespace
 
+// Whether the chunk-parallel kernel takes a reduction (the same order, so
+// the same bits, as the one-thread-per-group kernel).
+static bool chunks_ok(const float* part, int64_t stride, const float* out, int64_t n, int splits) {
+    return splits > kChunk && splits <= kChunk * kMaxChunks && n % 4 == 0 && reduce_vec_ok(part, stride, out);
+}
+static int64_t chunk_blocks(int64_t n) { return (n / 4 + 256 / kChunkLanes - 1) / (256 / kChunkLanes); }
+
 hipError_t launch_reduce_splits2(const float* p0, int64_t st0, float* o0, int64_t n0, const float* p1, int64_t st1,
                                  float* o1, int64_t n1, int splits, hipStream_t s) {
     if (n0 <= 0) return launch_reduce_splits(p1, splits, st1, o1, n1, s);
     if (n1 <= 0) return launch_reduce_splits(p0, splits, st0, o0, n0, s);
+    if (chunks_ok(p0, st0, o0, n0, splits) && chunks_ok(p1, st1, o1, n1, splits)) {
+        const int64_t b0 = chunk_blocks(n0), b1 = chunk_blocks(n1);
+        if (b0 + b1 > 0x7fffffffLL) return hipErrorInvalidConfiguration;
+        hipLaunchKernelGGL(reduce_chunks_kernel, dim3((unsigned)(b0 + b1)), dim3(256), 0, s, p0, st0, o0, n0, b0, p1,
+                           st1, o1, n1, splits);
+        return hipGetLastError();
+    }
     const unsigned g0 = grid_for((n0 + 3) / 4), g1 = grid_for((n1 + 3) / 4);
     hipLaunchKernelGGL(reduce_splits2_kernel, dim3(g0 + g1), dim3(256), 0, s, p0, st0, o0, n0, (int64_t)g0, p1, st1,
                        o1, n1, splits);
@@ -280,6 +358,13 @@ hipError_t launch_reduce_splits2(const float* p0, int64_t st0, float* o0, int64_
 hipError_t launch_reduce_splits(const float* part, int splits, int64_t stride, float* out, int64_t n,
                                 hipStream_t s) {
     if (n <= 0) return hipSuccess;
+    if (chunks_ok(part, stride, out, n, splits)) {
+        const int64_t b = chunk_blocks(n);
+        if (b > 0x7fffffffLL) return hipErrorInvalidConfiguration;
+        hipLaunchKernelGGL(reduce_chunks_kernel, dim3((unsigned)b), dim3(256), 0, s, part, stride, out, n, b, part,
+                           stride, out, (int64_t)0, splits);
+        return hipGetLastError();
+    }
     hipLaunchKernelGGL(reduce_splits_kernel, dim3(grid_for((n + 3) / 4)), dim3(256), 0, s, part, splits,
                        stride, out, n);
     return hipGetLastError();
