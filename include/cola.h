@@ -361,11 +361,15 @@ int cola_block_bwd(const cola_block_desc* desc, const cola_block_weights* w, con
  *     ping-pong family.
  *   COLA_OPT_WGRAD_PAIR (default 1): 0 launches the two weight gradients of a
  *     layer (and of a group) one by one instead of in one launch.
+ *   COLA_OPT_FUSE_GATE (default 1): 0 keeps the decoder block's gated
+ *     product (m = gate * up) and its backward in separate elementwise
+ *     kernels instead of the epilogues of the up projection's Y = H B^T and
+ *     the down projection's dX = dZ A (same roundings, so the same bits).
  * Workspace sizes depend on the settings: size the workspace after setting
  * them (a call whose workspace is too small returns COLA_ERR_WORKSPACE).
  * cola_set_option returns COLA_ERR_INVALID_ARG for an unknown option or a
  * value other than 0 or 1; cola_get_option returns the value, or -1. */
-typedef enum { COLA_OPT_STREAM_ONLY = 0, COLA_OPT_WGRAD_PAIR = 1 } cola_option;
+typedef enum { COLA_OPT_STREAM_ONLY = 0, COLA_OPT_WGRAD_PAIR = 1, COLA_OPT_FUSE_GATE = 2 } cola_option;
 int cola_set_option(int option, int value);
 int cola_get_option(int option);
 

@@ -119,7 +119,7 @@ EXPORTS = {
     "cola_get_option": ([ctypes.c_int], ctypes.c_int),
 }
 
-OPT_STREAM_ONLY, OPT_WGRAD_PAIR = 0, 1
+OPT_STREAM_ONLY, OPT_WGRAD_PAIR, OPT_FUSE_GATE = 0, 1, 2
 
 
 def lib():
@@ -468,7 +468,7 @@ def kernel_name(kernel_class: int) -> str:
 
 
 def set_option(option: int, value: int):
-    """Process-wide tuning option (OPT_STREAM_ONLY, OPT_WGRAD_PAIR) to 0 or 1."""
+    """Process-wide tuning option (OPT_STREAM_ONLY, OPT_WGRAD_PAIR, OPT_FUSE_GATE) to 0 or 1."""
     _check(lib().cola_set_option(int(option), int(value)))
 
 

@@ -3,6 +3,7 @@
 // of the public ABI (that is include/cola.h).
 #pragma once
 
+#include "../../include/cola.h"
 #include "internal.hpp"
 
 namespace cola {
@@ -73,7 +74,24 @@ hipError_t timed_fn(int kc, double flops, double bytes, hipStream_t s, F f) {
     return timed_call(kc, flops, bytes, s, [](void* c) { return (*static_cast<F*>(c))(); }, &f);
 }
 int set_hip_error(hipError_t e, const char* where);
+// Y = H B^T (bf16, B [d_out][r] with pitch r).  With `fused` non-NULL the
+// gated product is tried in its epilogue: Y = u and m = g u (g, m with
+// Y's pitch); *fused tells whether it ran (else the caller forms m).
 hipError_t launch_up_projection(int64_t T, int64_t d_out, int64_t r, const void* H, int64_t ldh, const void* B,
-                                void* Y, int64_t ldy, hipStream_t s);
+                                void* Y, int64_t ldy, hipStream_t s, const void* g = nullptr, void* m = nullptr,
+                                bool* fused = nullptr);
+// cola_group_fwd whose last projection also stores m = g u (g the group's
+// first output; g, u, m with pitch ld), and cola_bwd whose dX = dm GEMM
+// stores dg = dm u and du = dm g instead (g, u, dg, du with pitch ld); each
+// sets *fused to whether the fused epilogue ran (the ping-pong family takes
+// the product and the fusion option is on), else the caller forms the
+// products with the elementwise kernels.
+int group_fwd_gated(const cola_group_desc* desc, const void* X, const void* A_all, const void* const* B,
+                    void* const* Y, void* Z_all, void* H_all, void* ws, size_t ws_bytes, cola_stream_t stream,
+                    const void* g, int64_t ld, void* m, bool* fused);
+int layer_bwd_gated(const cola_desc* desc, const void* dY, const void* X, const void* Z, const void* H,
+                    const void* A, const void* B, void* dX, float* dA, float* dB, void* ws, size_t ws_bytes,
+                    cola_stream_t stream, const void* g, const void* u, int64_t ld, void* dg, void* du,
+                    bool* fused);
 
 }  // namespace cola

@@ -5,13 +5,16 @@
 // pre-activations, recompute the up projections and the attention).
 //
 // The projections run through the layer entry points (q, k, v and gate, up as
-// same-input groups); the rest is attention.hip and block_ops.hip.  Launch
-// order, one stream:
+// same-input groups); the rest is attention.hip and block_ops.hip.  The gated
+// product and its backward run in GEMM epilogues where the ping-pong family
+// takes the product (else, and with COLA_OPT_FUSE_GATE = 0, in elementwise
+// kernels: same roundings, same bits).  Launch order, one stream:
 //   forward : a = norm(x0); Z,H,q,k,v (group); att, lse; Z,H,o; x1 = x0 + o and
-//             b = norm(x1) (one pass); Z,H,gt,u (group); m = gt u; Z,H,y (down);
-//             x2 = x1 + y
-//   backward: [CoLA-M: b = norm(x1); H_gu = sigma(Z_gu); gt, u = H B^T; m]
-//             down bwd -> dm; dgt, du = dm u, dm gt; gate/up bwd -> db;
+//             b = norm(x1) (one pass); Z,H,gt,u (group) with m = gt u (in
+//             up's GEMM epilogue); Z,H,y (down); x2 = x1 + y
+//   backward: [CoLA-M: b = norm(x1); H_gu = sigma(Z_gu); gt, u = H B^T, m]
+//             down bwd with dgt, du = dm u, dm gt (in its dX GEMM epilogue);
+//             gate/up bwd -> db;
 //             dx1 = dx2 + norm_bwd(db) (+ dg2);
 //             [CoLA-M: a = norm(x0); H_qkv = sigma(Z_qkv); q, k, v = H B^T; att, lse]
 //             o bwd -> datt; attention bwd -> dq, dk, dv; q/k/v bwd -> da;
@@ -377,14 +380,18 @@ int cola_block_fwd(const cola_block_desc* desc, const cola_block_weights* w, con
         }
         if ((st = norm_fwd(c, x0, tmp, SV(COLA_BLK_X1), w->g2, bn)) != COLA_OK) return st;
         {
+            // gate and up as a group; m = gate * up in up's Y = H B^T epilogue
+            // where the ping-pong family runs it, else elementwise
             const cola_group_desc g = gu_desc(b, rc);
             const void* B2[2] = {w->B_g, w->B_u};
             void* Y2[2] = {gt, u};
-            st = cola_group_fwd(&g, bn, w->A_gu, B2, Y2, SV(COLA_BLK_Z_GU), b.m ? nullptr : SV(COLA_BLK_H_GU), sub,
-                                W.sub_bytes, stream);
+            bool fused = false;
+            st = group_fwd_gated(&g, bn, w->A_gu, B2, Y2, SV(COLA_BLK_Z_GU), b.m ? nullptr : SV(COLA_BLK_H_GU), sub,
+                                 W.sub_bytes, stream, gt, b.ldf, m, &fused);
             if (st != COLA_OK) return st;
+            if (!fused && (st = ew(c, EW_MUL, b.ffn, gt, b.ldf, u, b.ldf, nullptr, 0, m, b.ldf, nullptr, 0)) != COLA_OK)
+                return st;
         }
-        if ((st = ew(c, EW_MUL, b.ffn, gt, b.ldf, u, b.ldf, nullptr, 0, m, b.ldf, nullptr, 0)) != COLA_OK) return st;
         {
             const cola_desc dn = down_desc(b, rc);
             st = cola_fwd(&dn, m, w->A_d, w->B_d, tmp, SV(COLA_BLK_Z_DOWN), b.m ? nullptr : SV(COLA_BLK_H_DOWN), sub,
@@ -458,18 +465,27 @@ int cola_block_bwd(const cola_block_desc* desc, const cola_block_weights* w, con
                 COLA_OK)
                 return st;
             if ((st = up(c, b.ffn, wk + W.hgu, b.ld2, w->B_g, wk + W.gt, b.ldf)) != COLA_OK) return st;
-            if ((st = up(c, b.ffn, wk + W.hgu + b.r * 2, b.ld2, w->B_u, wk + W.up, b.ldf)) != COLA_OK) return st;
-            if ((st = ew(c, EW_MUL, b.ffn, gt, b.ldf, u, b.ldf, nullptr, 0, wk + W.m, b.ldf, nullptr, 0)) != COLA_OK)
+            bool fused = false;
+            if ((st = chk(launch_up_projection(b.T, b.ffn, b.r, wk + W.hgu + b.r * 2, b.ld2, w->B_u, wk + W.up, b.ldf,
+                                               s, gt, wk + W.m, &fused),
+                          "up_projection")) != COLA_OK)
+                return st;
+            if (!fused &&
+                (st = ew(c, EW_MUL, b.ffn, gt, b.ldf, u, b.ldf, nullptr, 0, wk + W.m, b.ldf, nullptr, 0)) != COLA_OK)
                 return st;
         }
         {
+            // down's backward; dgt = dm u and du = dm gt in its dX = dm
+            // epilogue where the ping-pong family runs it, else elementwise
             const cola_desc dn = down_desc(b, rc);
-            st = cola_bwd(&dn, dx2, m, SV(COLA_BLK_Z_DOWN), b.m ? nullptr : SV(COLA_BLK_H_DOWN), w->A_d, w->B_d, dm,
-                          gr->A_d, gr->B_d, sub, W.sub_bytes, stream);
+            bool fused = false;
+            st = layer_bwd_gated(&dn, dx2, m, SV(COLA_BLK_Z_DOWN), b.m ? nullptr : SV(COLA_BLK_H_DOWN), w->A_d, w->B_d,
+                                 dm, gr->A_d, gr->B_d, sub, W.sub_bytes, stream, gt, u, b.ldf, dgt, du, &fused);
             if (st != COLA_OK) return st;
+            if (!fused &&
+                (st = ew(c, EW_DMUL, b.ffn, gt, b.ldf, u, b.ldf, dm, b.ldf, dgt, b.ldf, du, b.ldf)) != COLA_OK)
+                return st;
         }
-        // dgt = dm u, du = dm gt
-        if ((st = ew(c, EW_DMUL, b.ffn, gt, b.ldf, u, b.ldf, dm, b.ldf, dgt, b.ldf, du, b.ldf)) != COLA_OK) return st;
         {
             const cola_group_desc g = gu_desc(b, 0);
             const void* dY2[2] = {dgt, du};

@@ -396,6 +396,23 @@ int guarded(F&& f) {
     }
 }
 
+// The gated product of the decoder block's MLP fused into a GEMM epilogue
+// (ping-pong family only; the caller runs the elementwise kernels when
+// *fused comes back false): forward, the last projection of a group stores
+// u and m = g u, g being the group's first output; backward, the layer's
+// dX = dm GEMM stores dg = dm u and du = dm g instead.  g, u, m, dg and du
+// share the row pitch ld.
+struct Gate {
+    const void* g;
+    const void* u;
+    int64_t ld;
+    void* out;       // m (forward) or dg (backward)
+    void* out2;      // du (backward)
+    bool* fused;
+};
+
+bool gate_fusion_on() { return get_option(OPT_FUSE_GATE) == 1; }
+
 // Forward of one validated layer with its pointers and workspace checked.
 // outer >= 0: the both-sigma variant (K2 stores P and Y = sigma_out(P)).
 int layer_forward(const Dims& x, int act, bool recompute, const void* X, const void* A, const void* B, void* Y,
@@ -440,7 +457,7 @@ int layer_forward(const Dims& x, int act, bool recompute, const void* X, const v
 // workspace checked; dY has row pitch ldy.
 int layer_backward(const Dims& x, int act, bool recompute, const void* dY, int64_t ldy, const void* X,
                    const void* Z, const void* H, const void* A, const void* B, void* dX, float* dA, float* dB,
-                   char* w, hipStream_t s) {
+                   char* w, hipStream_t s, const Gate* gate = nullptr) {
     const BwdPlan p = plan_bwd(x, recompute);
     void* dZ = w + p.off_dz;
     const void* Hbuf = recompute ? (const void*)(w + p.off_h) : H;
@@ -465,10 +482,25 @@ int layer_backward(const Dims& x, int act, bool recompute, const void* dY, int64
     e = timed(COLA_KC_BWD_DZ, gemm_flops(x.T, x.r, x.d_out), b3, s, [&] { return gemm(k3, x.bf16, s); });
     if (e != hipSuccess) return hip_fail(e, "bwd_dz");
 
-    // K4: dX = dZ A
+    // K4: dX = dZ A (or, gated, dg = dm u and du = dm g with dm = dZ A)
     GemmArgs k4 = make_args(TAG_BWD_DX, x.T, x.d_in, x.r, dZ, p.ldw, KMAJ, Aw, lda, MNMAJ, dX, x.ldx, EPI_STORE,
                             act);
-    const double b4 = es * ((double)x.T * x.r + (double)x.r * x.d_in + (double)x.T * x.d_in);
+    double b4 = es * ((double)x.T * x.r + (double)x.r * x.d_in + (double)x.T * x.d_in);
+    if (gate) {
+        GemmArgs kg = make_args(TAG_BWD_DXG, x.T, x.d_in, x.r, dZ, p.ldw, KMAJ, Aw, lda, MNMAJ, gate->out, gate->ld,
+                                EPI_DGATE, act);
+        kg.zin = gate->g;
+        kg.ldzin = gate->ld;
+        kg.zin2 = gate->u;
+        kg.ldzin2 = gate->ld;
+        kg.aux = gate->out2;
+        kg.ldaux = gate->ld;
+        *gate->fused = x.bf16 && gate_fusion_on() && pp_takes(kg);
+        if (*gate->fused) {
+            k4 = kg;
+            b4 = es * ((double)x.T * x.r + (double)x.r * x.d_in + 4.0 * x.T * x.d_in);
+        }
+    }
     e = timed(COLA_KC_BWD_DX, gemm_flops(x.T, x.d_in, x.r), b4, s, [&] { return gemm(k4, x.bf16, s); });
     if (e != hipSuccess) return hip_fail(e, "bwd_dx");
 
@@ -499,6 +531,25 @@ int zero_weight_grads(const Dims& x, float* dA, float* dB, hipStream_t s) {
     return e == hipSuccess ? COLA_OK : hip_fail(e, "fill_zero");
 }
 
+int bwd_checked(const cola_desc* desc, const void* dY, const void* X, const void* Z, const void* H, const void* A,
+                const void* B, void* dX, float* dA, float* dB, void* ws, size_t ws_bytes, cola_stream_t stream,
+                const Gate* gate) {
+    Dims x;
+    int st = check_desc(desc, &x);
+    if (st != COLA_OK) return st;
+    const bool recompute = desc->recompute == 1;
+    if (recompute ? (H != nullptr) : (H == nullptr && x.T > 0)) return COLA_ERR_INVALID_ARG;
+    if (!dA || !dB) return COLA_ERR_INVALID_ARG;
+    if (gate) *gate->fused = false;
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    if (x.T == 0) return zero_weight_grads(x, dA, dB, s);
+    if (!dY || !X || !Z || !A || !B || !dX) return COLA_ERR_INVALID_ARG;
+    const BwdPlan p = plan_bwd(x, recompute);
+    if (!ws || ws_bytes < p.total) return COLA_ERR_WORKSPACE;
+    return layer_backward(x, desc->act, recompute, dY, x.ldy, X, Z, H, A, B, dX, dA, dB,
+                          reinterpret_cast<char*>(ws), s, gate);
+}
+
 // Workspace of the both-sigma backward: the layer's, then dP = dY sigma_out'(P).
 struct OuterPlan {
     int64_t ldg;
@@ -525,9 +576,21 @@ hipError_t timed_call(int kc, double flops, double bytes, hipStream_t s, hipErro
 int set_hip_error(hipError_t e, const char* where) { return hip_fail(e, where); }
 
 hipError_t launch_up_projection(int64_t T, int64_t d_out, int64_t r, const void* H, int64_t ldh, const void* B,
-                                void* Y, int64_t ldy, hipStream_t s) {
+                                void* Y, int64_t ldy, hipStream_t s, const void* g, void* m, bool* fused) {
     GemmArgs k2 = make_args(TAG_FWD_Y, T, d_out, r, H, ldh, KMAJ, B, r, KMAJ, Y, ldy, EPI_STORE, 0);
-    const double bytes = 2.0 * ((double)T * r + (double)d_out * r + (double)T * d_out);
+    double bytes = 2.0 * ((double)T * r + (double)d_out * r + (double)T * d_out);
+    if (fused) {
+        GemmArgs kg = make_args(TAG_FWD_YG, T, d_out, r, H, ldh, KMAJ, B, r, KMAJ, Y, ldy, EPI_GATE, 0);
+        kg.zin = g;
+        kg.ldzin = ldy;
+        kg.aux = m;
+        kg.ldaux = ldy;
+        *fused = gate_fusion_on() && pp_takes(kg);
+        if (*fused) {
+            k2 = kg;
+            bytes = 2.0 * ((double)T * r + (double)d_out * r + 3.0 * T * d_out);
+        }
+    }
     return timed(COLA_KC_FWD_Y, gemm_flops(T, d_out, r), bytes, s, [&] { return gemm(k2, true, s); });
 }
 
@@ -616,21 +679,7 @@ int cola_fwd_outer(const cola_desc* desc, int outer_act, const void* X, const vo
 int cola_bwd(const cola_desc* desc, const void* dY, const void* X, const void* Z, const void* H,
              const void* A, const void* B, void* dX, float* dA, float* dB, void* ws, size_t ws_bytes,
              cola_stream_t stream) {
-    return guarded([&]() -> int {
-        Dims x;
-        int st = check_desc(desc, &x);
-        if (st != COLA_OK) return st;
-        const bool recompute = desc->recompute == 1;
-        if (recompute ? (H != nullptr) : (H == nullptr && x.T > 0)) return COLA_ERR_INVALID_ARG;
-        if (!dA || !dB) return COLA_ERR_INVALID_ARG;
-        hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-        if (x.T == 0) return zero_weight_grads(x, dA, dB, s);
-        if (!dY || !X || !Z || !A || !B || !dX) return COLA_ERR_INVALID_ARG;
-        const BwdPlan p = plan_bwd(x, recompute);
-        if (!ws || ws_bytes < p.total) return COLA_ERR_WORKSPACE;
-        return layer_backward(x, desc->act, recompute, dY, x.ldy, X, Z, H, A, B, dX, dA, dB,
-                              reinterpret_cast<char*>(ws), s);
-    });
+    return guarded([&]() -> int { return bwd_checked(desc, dY, X, Z, H, A, B, dX, dA, dB, ws, ws_bytes, stream, nullptr); });
 }
 
 // ---------------------------------------------------------------------------
@@ -1020,7 +1069,8 @@ namespace {
 // the inference forward: K1 stores only H (into the workspace), nothing is
 // kept for a backward pass.
 int group_forward(const GDims& g, int act, const void* X, const void* A_all, const void* const* B,
-                  void* const* Y, void* Z_all, void* H_all, bool h_in_ws, char* w, hipStream_t s) {
+                  void* const* Y, void* Z_all, void* H_all, bool h_in_ws, char* w, hipStream_t s,
+                  const Gate* gate = nullptr) {
     const GFwdPlan p = plan_group_fwd(g, h_in_ws);
     char* Hbuf = h_in_ws ? w + p.off_h : reinterpret_cast<char*>(H_all);
     const int64_t ldh = h_in_ws ? p.ldw : g.ldz;
@@ -1055,7 +1105,21 @@ int group_forward(const GDims& g, int act, const void* X, const void* A_all, con
         if (e != hipSuccess) return hip_fail(e, "pack_rows");
         GemmArgs k2 = make_args(TAG_FWD_Y, g.T, g.d_out[q], g.r[q], Hbuf + g.off[q] * g.esize, ldh, KMAJ, Bw,
                                 ldb, KMAJ, Y[q], g.ldy[q], EPI_STORE, act);
-        const double b2 = es * ((double)g.T * g.r[q] + (double)g.d_out[q] * g.r[q] + (double)g.T * g.d_out[q]);
+        double b2 = es * ((double)g.T * g.r[q] + (double)g.d_out[q] * g.r[q] + (double)g.T * g.d_out[q]);
+        if (gate && q == g.n - 1) {
+            // the last projection also stores m = g u (g: the group's first output)
+            GemmArgs kg = make_args(TAG_FWD_YG, g.T, g.d_out[q], g.r[q], Hbuf + g.off[q] * g.esize, ldh, KMAJ, Bw,
+                                    ldb, KMAJ, Y[q], gate->ld, EPI_GATE, act);
+            kg.zin = gate->g;
+            kg.ldzin = gate->ld;
+            kg.aux = gate->out;
+            kg.ldaux = gate->ld;
+            *gate->fused = g.bf16 && gate_fusion_on() && g.ldy[q] == gate->ld && pp_takes(kg);
+            if (*gate->fused) {
+                k2 = kg;
+                b2 = es * ((double)g.T * g.r[q] + (double)g.d_out[q] * g.r[q] + 3.0 * g.T * g.d_out[q]);
+            }
+        }
         e = timed(COLA_KC_FWD_Y, gemm_flops(g.T, g.d_out[q], g.r[q]), b2, s, [&] { return gemm(k2, g.bf16, s); });
         if (e != hipSuccess) return hip_fail(e, "fwd_y");
     }
@@ -1069,6 +1133,25 @@ GDims single_group(const Dims& x) {
     g.r[0] = x.r; g.d_out[0] = x.d_out; g.ldy[0] = x.ldy; g.off[0] = 0;
     g.bf16 = x.bf16; g.esize = x.esize;
     return g;
+}
+
+int group_fwd_checked(const cola_group_desc* desc, const void* X, const void* A_all, const void* const* B,
+                      void* const* Y, void* Z_all, void* H_all, void* ws, size_t ws_bytes, cola_stream_t stream,
+                      const Gate* gate) {
+    GDims g;
+    int st = check_group(desc, &g);
+    if (st != COLA_OK) return st;
+    const bool recompute = desc->recompute == 1;
+    if (recompute ? (H_all != nullptr) : (H_all == nullptr && g.T > 0)) return COLA_ERR_INVALID_ARG;
+    if (gate) *gate->fused = false;
+    if (g.T == 0) return COLA_OK;
+    if (!X || !A_all || !B || !Y || !Z_all) return COLA_ERR_INVALID_ARG;
+    for (int q = 0; q < g.n; ++q)
+        if (!B[q] || !Y[q]) return COLA_ERR_INVALID_ARG;
+    const GFwdPlan p = plan_group_fwd(g, recompute);
+    if (p.total > 0 && (!ws || ws_bytes < p.total)) return COLA_ERR_WORKSPACE;
+    return group_forward(g, desc->act, X, A_all, B, Y, Z_all, H_all, recompute, reinterpret_cast<char*>(ws),
+                         reinterpret_cast<hipStream_t>(stream), gate);
 }
 
 int infer_checked(const GDims& g, int act, const void* X, const void* A_all, const void* const* B, void* const* Y,
@@ -1090,19 +1173,7 @@ extern "C" {
 int cola_group_fwd(const cola_group_desc* desc, const void* X, const void* A_all, const void* const* B,
                    void* const* Y, void* Z_all, void* H_all, void* ws, size_t ws_bytes, cola_stream_t stream) {
     return guarded([&]() -> int {
-        GDims g;
-        int st = check_group(desc, &g);
-        if (st != COLA_OK) return st;
-        const bool recompute = desc->recompute == 1;
-        if (recompute ? (H_all != nullptr) : (H_all == nullptr && g.T > 0)) return COLA_ERR_INVALID_ARG;
-        if (g.T == 0) return COLA_OK;
-        if (!X || !A_all || !B || !Y || !Z_all) return COLA_ERR_INVALID_ARG;
-        for (int q = 0; q < g.n; ++q)
-            if (!B[q] || !Y[q]) return COLA_ERR_INVALID_ARG;
-        const GFwdPlan p = plan_group_fwd(g, recompute);
-        if (p.total > 0 && (!ws || ws_bytes < p.total)) return COLA_ERR_WORKSPACE;
-        return group_forward(g, desc->act, X, A_all, B, Y, Z_all, H_all, recompute, reinterpret_cast<char*>(ws),
-                             reinterpret_cast<hipStream_t>(stream));
+        return group_fwd_checked(desc, X, A_all, B, Y, Z_all, H_all, ws, ws_bytes, stream, nullptr);
     });
 }
 
@@ -1228,3 +1299,31 @@ int cola_group_bwd(const cola_group_desc* desc, const void* const* dY, const voi
 }
 
 }  // extern "C"
+
+// ---- the block's gated-product hooks (block.hpp) ----
+namespace cola {
+
+int group_fwd_gated(const cola_group_desc* desc, const void* X, const void* A_all, const void* const* B,
+                    void* const* Y, void* Z_all, void* H_all, void* ws, size_t ws_bytes, cola_stream_t stream,
+                    const void* g, int64_t ld, void* m, bool* fused) {
+    if (!fused) return COLA_ERR_INVALID_ARG;
+    *fused = false;
+    const Gate gate{g, nullptr, ld, m, nullptr, fused};
+    return guarded([&]() -> int {
+        return group_fwd_checked(desc, X, A_all, B, Y, Z_all, H_all, ws, ws_bytes, stream, &gate);
+    });
+}
+
+int layer_bwd_gated(const cola_desc* desc, const void* dY, const void* X, const void* Z, const void* H,
+                    const void* A, const void* B, void* dX, float* dA, float* dB, void* ws, size_t ws_bytes,
+                    cola_stream_t stream, const void* g, const void* u, int64_t ld, void* dg, void* du,
+                    bool* fused) {
+    if (!fused) return COLA_ERR_INVALID_ARG;
+    *fused = false;
+    const Gate gate{g, u, ld, dg, du, fused};
+    return guarded([&]() -> int {
+        return bwd_checked(desc, dY, X, Z, H, A, B, dX, dA, dB, ws, ws_bytes, stream, &gate);
+    });
+}
+
+}  // namespace cola

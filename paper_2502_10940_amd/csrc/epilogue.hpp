@@ -467,10 +467,11 @@ __device__ __forceinline__ void epilogue_t_impl(const GemmArgs& a, const f32x16 
     uint16_t* C = reinterpret_cast<uint16_t*>(a.c);
     uint16_t* Hp = reinterpret_cast<uint16_t*>(a.aux);
     const uint16_t* Zp = reinterpret_cast<const uint16_t*>(a.zin);
-    // EPI_DZ: Z (in the layout after exchange 1) of tile row i + 1 is loaded
-    // before the stores of tile row i (loads and stores share one wait
-    // counter, so waiting for a load issued after a store also waits for that
-    // store)
+    // EPI_DZ (Z), EPI_GATE (g): the input (in the layout after exchange 1) of
+    // tile row i + 1 is loaded before the stores of tile row i (loads and
+    // stores share one wait counter, so waiting for a load issued after a
+    // store also waits for that store)
+    constexpr bool kIn = EPI == EPI_DZ || EPI == EPI_GATE;
     u32x4_t zb[2][TN][2];
     auto zload = [&](int i, u32x4_t (&z)[TN][2]) {
 #pragma unroll
@@ -479,10 +480,10 @@ __device__ __forceinline__ void epilogue_t_impl(const GemmArgs& a, const f32x16 
             for (int p = 0; p < 2; ++p)
                 z[j][p] = load_bf16x8<FAST>(Zp, a.ldzin, a.M, a.N, row0 + 32 * i + r1, col0 + 32 * j + 16 * p + h1);
     };
-    if constexpr (EPI == EPI_DZ) zload(0, zb[0]);
+    if constexpr (kIn) zload(0, zb[0]);
 #pragma unroll
     for (int i = 0; i < TM; ++i) {
-        if constexpr (EPI == EPI_DZ) {
+        if constexpr (kIn) {
             if (i + 1 < TM) zload(i + 1, zb[(i + 1) & 1]);
         }
         const int64_t gx = row0 + 32 * i + r2;     // row of piece X (Y: gx + 16)
@@ -553,7 +554,7 @@ __device__ __forceinline__ void epilogue_t_impl(const GemmArgs& a, const f32x16 
                         for (int q = 0; q < 4; ++q) {
                             const int r = 8 * p + 2 * q;        // registers r, r + 1
                             const uint32_t zz = pack_bf16x2(v[r], v[r + 1]);
-                            if constexpr (EPI == EPI_STORE) {
+                            if constexpr (EPI == EPI_STORE || EPI == EPI_GATE) {
                                 o[p][q] = zz;
                             } else {
                                 // sigma of the rounded values
@@ -575,6 +576,19 @@ __device__ __forceinline__ void epilogue_t_impl(const GemmArgs& a, const f32x16 
                             swap_halves(h[p][0], h[p][2]);
                             swap_halves(h[p][1], h[p][3]);
                         }
+                        if constexpr (EPI == EPI_GATE) {
+                            // m = g u of the rounded u (o after exchange 1
+                            // matches the layout of g)
+                            const u32x4_t g = zb[i & 1][j][p];
+#pragma unroll
+                            for (int q = 0; q < 4; ++q) {
+                                const float y0 = __uint_as_float(o[p][q] << 16);
+                                const float y1 = __uint_as_float(o[p][q] & 0xffff0000u);
+                                const float g0 = __uint_as_float(g[q] << 16);
+                                const float g1 = __uint_as_float(g[q] & 0xffff0000u);
+                                h[p][q] = pack_bf16x2(g0 * y0, g1 * y1);
+                            }
+                        }
                     }
                 }
                 // exchange 2, then one store per piece
@@ -582,7 +596,7 @@ __device__ __forceinline__ void epilogue_t_impl(const GemmArgs& a, const f32x16 
                 for (int q = 0; q < 4; ++q) swap_rows16(o[0][q], o[1][q]);
                 store_bf16x8<FAST>(C, a.ldc, a.M, a.N, gx, gn, o[0]);
                 store_bf16x8<FAST>(C, a.ldc, a.M, a.N, gx + 16, gn, o[1]);
-                if constexpr (EPI == EPI_Z_H || EPI == EPI_DZ) {
+                if constexpr (EPI == EPI_Z_H || EPI == EPI_DZ || EPI == EPI_GATE) {
                     if (Hp) {
 #pragma unroll
                         for (int q = 0; q < 4; ++q) swap_rows16(h[0][q], h[1][q]);
@@ -592,6 +606,66 @@ __device__ __forceinline__ void epilogue_t_impl(const GemmArgs& a, const f32x16 
                 }
             }
         }
+    }
+}
+
+// EPI_DGATE: with dm = round(acc), c = round(dm u) and aux = round(dm g).
+// Same exchanges and stores as the elementwise epilogues above; the inputs
+// g and u of one 32 x 32 tile are loaded a tile ahead (a whole tile row
+// ahead, as EPI_DZ does, would need twice the registers for two inputs).
+template <bool FAST, int TM, int TN>
+__device__ __forceinline__ void epilogue_t_dgate(const GemmArgs& a, const f32x16 (&acc)[TM][TN], int64_t row0,
+                                                 int64_t col0, int lane) {
+    const int r1 = lane & 31;
+    const int h1 = 8 * (lane >> 5);
+    const int r2 = lane & 15;
+    const int c2 = 16 * ((lane >> 4) & 1) + 8 * (lane >> 5);
+    uint16_t* C = reinterpret_cast<uint16_t*>(a.c);
+    uint16_t* Dp = reinterpret_cast<uint16_t*>(a.aux);
+    const uint16_t* Gp = reinterpret_cast<const uint16_t*>(a.zin);
+    const uint16_t* Up = reinterpret_cast<const uint16_t*>(a.zin2);
+    u32x4_t gb[2][2], ub[2][2];              // [tile parity][piece p]
+    auto load = [&](int t, int buf) {
+        const int i = t / TN, j = t % TN;
+#pragma unroll
+        for (int p = 0; p < 2; ++p) {
+            gb[buf][p] = load_bf16x8<FAST>(Gp, a.ldzin, a.M, a.N, row0 + 32 * i + r1, col0 + 32 * j + 16 * p + h1);
+            ub[buf][p] = load_bf16x8<FAST>(Up, a.ldzin2, a.M, a.N, row0 + 32 * i + r1, col0 + 32 * j + 16 * p + h1);
+        }
+    };
+    load(0, 0);
+#pragma unroll
+    for (int t = 0; t < TM * TN; ++t) {
+        const int i = t / TN, j = t % TN;
+        if (t + 1 < TM * TN) load(t + 1, (t + 1) & 1);
+        const f32x16& v = acc[i][j];
+        uint32_t o[2][4], h[2][4];
+#pragma unroll
+        for (int p = 0; p < 2; ++p) {
+#pragma unroll
+            for (int q = 0; q < 4; ++q) o[p][q] = pack_bf16x2(v[8 * p + 2 * q], v[8 * p + 2 * q + 1]);
+            swap_halves(o[p][0], o[p][2]);
+            swap_halves(o[p][1], o[p][3]);
+            const u32x4_t g = gb[t & 1][p], u = ub[t & 1][p];
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const float y0 = __uint_as_float(o[p][q] << 16);
+                const float y1 = __uint_as_float(o[p][q] & 0xffff0000u);
+                h[p][q] = pack_bf16x2(y0 * __uint_as_float(g[q] << 16), y1 * __uint_as_float(g[q] & 0xffff0000u));
+                o[p][q] = pack_bf16x2(y0 * __uint_as_float(u[q] << 16), y1 * __uint_as_float(u[q] & 0xffff0000u));
+            }
+        }
+        const int64_t gx = row0 + 32 * i + r2;
+        const int64_t gn = col0 + 32 * j + c2;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            swap_rows16(o[0][q], o[1][q]);
+            swap_rows16(h[0][q], h[1][q]);
+        }
+        store_bf16x8<FAST>(C, a.ldc, a.M, a.N, gx, gn, o[0]);
+        store_bf16x8<FAST>(C, a.ldc, a.M, a.N, gx + 16, gn, o[1]);
+        store_bf16x8<FAST>(Dp, a.ldaux, a.M, a.N, gx, gn, h[0]);
+        store_bf16x8<FAST>(Dp, a.ldaux, a.M, a.N, gx + 16, gn, h[1]);
     }
 }
 
@@ -611,16 +685,23 @@ __device__ __forceinline__ void epilogue_t_act(const GemmArgs& a, const f32x16 (
     } else {
         fast = fast && al(a.c, a.ldc, 8);
     }
-    if constexpr (EPI == EPI_Z_H || EPI == EPI_DZ) fast = fast && (a.aux == nullptr || al(a.aux, a.ldaux, 8));
-    if constexpr (EPI == EPI_DZ) fast = fast && al(a.zin, a.ldzin, 8);
-    if (fast) epilogue_t_impl<EPI, ACT, true>(a, acc, row0, col0, lane, split);
-    else epilogue_t_impl<EPI, ACT, false>(a, acc, row0, col0, lane, split);
+    if constexpr (EPI == EPI_Z_H || EPI == EPI_DZ || EPI == EPI_GATE || EPI == EPI_DGATE)
+        fast = fast && (a.aux == nullptr || al(a.aux, a.ldaux, 8));
+    if constexpr (EPI == EPI_DZ || EPI == EPI_GATE || EPI == EPI_DGATE) fast = fast && al(a.zin, a.ldzin, 8);
+    if constexpr (EPI == EPI_DGATE) fast = fast && al(a.zin2, a.ldzin2, 8);
+    if constexpr (EPI == EPI_DGATE) {
+        if (fast) epilogue_t_dgate<true>(a, acc, row0, col0, lane);
+        else epilogue_t_dgate<false>(a, acc, row0, col0, lane);
+    } else {
+        if (fast) epilogue_t_impl<EPI, ACT, true>(a, acc, row0, col0, lane, split);
+        else epilogue_t_impl<EPI, ACT, false>(a, acc, row0, col0, lane, split);
+    }
 }
 
 template <int EPI, int TM, int TN>
 __device__ __forceinline__ void epilogue_block_t(const GemmArgs& a, const f32x16 (&acc)[TM][TN], int64_t row0,
                                                  int64_t col0, int lane, int split) {
-    if constexpr (EPI == EPI_STORE || EPI == EPI_STORE_F32) {
+    if constexpr (EPI == EPI_STORE || EPI == EPI_STORE_F32 || EPI == EPI_GATE || EPI == EPI_DGATE) {
         epilogue_t_act<EPI, 0>(a, acc, row0, col0, lane, split);
     } else {
         if (a.act == 0) epilogue_t_act<EPI, 0>(a, acc, row0, col0, lane, split);

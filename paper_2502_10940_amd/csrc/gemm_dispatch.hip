@@ -19,6 +19,7 @@ namespace {
 // process-wide tuning options (cola_set_option)
 std::atomic<int> g_force_stream{0};
 std::atomic<int> g_wgrad_pair{1};
+std::atomic<int> g_fuse_gate{1};
 }  // namespace
 
 int set_option(int option, int value) {
@@ -26,6 +27,7 @@ int set_option(int option, int value) {
     switch (option) {
         case OPT_STREAM_ONLY: g_force_stream.store(value); return 0;
         case OPT_WGRAD_PAIR: g_wgrad_pair.store(value); return 0;
+        case OPT_FUSE_GATE: g_fuse_gate.store(value); return 0;
         default: return -1;
     }
 }
@@ -34,6 +36,7 @@ int get_option(int option) {
     switch (option) {
         case OPT_STREAM_ONLY: return g_force_stream.load();
         case OPT_WGRAD_PAIR: return g_wgrad_pair.load();
+        case OPT_FUSE_GATE: return g_fuse_gate.load();
         default: return -1;
     }
 }
@@ -52,6 +55,8 @@ int gemm_family(int64_t M, int64_t N, int tag) {
     if (g_force_stream.load(std::memory_order_relaxed)) return FAM_STREAM;
     return bf16_wide_ok(M, N) ? (int)FAM_PP : (int)FAM_STREAM;
 }
+
+bool pp_takes(const GemmArgs& a) { return gemm_family(a.M, a.N, a.tag) == FAM_PP && pp_operands_ok(a); }
 
 hipError_t launch_gemm_bf16_pair(const GemmArgs& a0, const GemmArgs& a1, hipStream_t s) {
     const bool pp = gemm_family(a0.M, a0.N, a0.tag) == FAM_PP && gemm_family(a1.M, a1.N, a1.tag) == FAM_PP &&

@@ -594,6 +594,8 @@ hipError_t launch_gemm_pp(const GemmArgs& a, hipStream_t s) {
         case TAG_INFER_H: return launch_p<KMAJ, KMAJ, EPI_H, TAG_INFER_H>(a, s);
         case TAG_FWD_Y: return launch_p<KMAJ, KMAJ, EPI_STORE, TAG_FWD_Y>(a, s);
         case TAG_FWD_YP: return launch_p<KMAJ, KMAJ, EPI_Z_H, TAG_FWD_YP>(a, s);
+        case TAG_FWD_YG: return launch_p<KMAJ, KMAJ, EPI_GATE, TAG_FWD_YG>(a, s);
+        case TAG_BWD_DXG: return launch_p<KMAJ, MNMAJ, EPI_DGATE, TAG_BWD_DXG>(a, s);
         case TAG_BWD_DZ: return launch_p<KMAJ, MNMAJ, EPI_DZ, TAG_BWD_DZ>(a, s);
         case TAG_BWD_DX: return launch_p<KMAJ, MNMAJ, EPI_STORE, TAG_BWD_DX>(a, s);
         case TAG_BWD_DA: return launch_p<MNMAJ, MNMAJ, EPI_STORE_F32, TAG_BWD_DA>(a, s);

@@ -19,6 +19,9 @@ enum Epilogue : int {
     EPI_Z_H = 2,       // c = Z = round(acc); aux = H = round(sigma(Z))
     EPI_DZ = 3,        // c = dZ = round(acc * sigma'(Z)), Z read from zin; aux = H if non-NULL
     EPI_H = 4,         // c = H = round(sigma(round(acc))): H of EPI_Z_H without storing Z (inference)
+    // the gated MLP of the decoder block (ping-pong family only):
+    EPI_GATE = 5,      // c = u = round(acc); aux = m = round(g u), g read from zin
+    EPI_DGATE = 6,     // with dm = round(acc): c = round(dm u), aux = round(dm g); g from zin, u from zin2
 };
 
 // Which step of the layer a GEMM is (same numbering as the kernel classes of
@@ -26,7 +29,9 @@ enum Epilogue : int {
 enum Tag : int {
     TAG_FWD_Z = 0, TAG_FWD_Y = 1, TAG_BWD_DZ = 2, TAG_BWD_DX = 3, TAG_BWD_DA = 4,
     TAG_BWD_DB = 5, TAG_DENSE_FWD = 7, TAG_DENSE_DX = 8, TAG_DENSE_DW = 9, TAG_INFER_H = 11,
-    TAG_FWD_YP = 12     // K2 of the both-sigma variant: EPI_Z_H storing P and sigma_out(P)
+    TAG_FWD_YP = 12,    // K2 of the both-sigma variant: EPI_Z_H storing P and sigma_out(P)
+    TAG_FWD_YG = 13,    // K2 of the up projection with the gated product (EPI_GATE)
+    TAG_BWD_DXG = 14    // K4 of the down projection with the gated product's backward (EPI_DGATE)
 };
 
 struct GemmArgs {
@@ -35,7 +40,8 @@ struct GemmArgs {
     const void* q; int64_t ldq; int q_layout;    // right operand Q (C = P Q^T)
     void* c; int64_t ldc;                        // output
     void* aux; int64_t ldaux;                    // second output (H) or NULL
-    const void* zin; int64_t ldzin;              // Z read by EPI_DZ
+    const void* zin; int64_t ldzin;              // Z read by EPI_DZ, g by EPI_GATE / EPI_DGATE
+    const void* zin2; int64_t ldzin2;            // u read by EPI_DGATE
     int epi;
     int tag;                                     // Tag
     int act;                                     // 0 identity, 1 SiLU
@@ -63,11 +69,14 @@ enum Family : int { FAM_STREAM = 1, FAM_PP = 4 };
 // output dimensions exceed 128, else STREAM; the option OPT_STREAM_ONLY
 // sends every product to STREAM.
 int gemm_family(int64_t M, int64_t N, int tag);
+// Whether the PP family runs this GEMM (family and operand alignment): the
+// gated epilogues exist only there.
+bool pp_takes(const GemmArgs& a);
 
 // Process-wide tuning options (the public cola_set_option): the values of
 // cola_option in include/cola.h.  set_option returns 0, or -1 for an unknown
 // option or a value other than 0 / 1.
-enum Option : int { OPT_STREAM_ONLY = 0, OPT_WGRAD_PAIR = 1 };
+enum Option : int { OPT_STREAM_ONLY = 0, OPT_WGRAD_PAIR = 1, OPT_FUSE_GATE = 2 };
 int set_option(int option, int value);
 int get_option(int option);
 

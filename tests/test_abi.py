@@ -423,6 +423,7 @@ def test_tuning_options():
     L = cola.lib()
     assert cola.get_option(cola.OPT_STREAM_ONLY) == 0
     assert cola.get_option(cola.OPT_WGRAD_PAIR) == 1
+    assert cola.get_option(cola.OPT_FUSE_GATE) == 1
     assert L.cola_get_option(7) == -1
     assert L.cola_set_option(7, 0) == cola.ERR_INVALID_ARG
     assert L.cola_set_option(cola.OPT_WGRAD_PAIR, 2) == cola.ERR_INVALID_ARG

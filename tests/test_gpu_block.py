@@ -116,6 +116,34 @@ def test_block_cola_m_bitwise_equals_cola_and_is_deterministic(case):
         assert np.array_equal(ra[k], ra2[k]), k
 
 
+@pytest.mark.parametrize("recompute", [False, True], ids=["cola", "colam"])
+@pytest.mark.parametrize("case", [CASES[1], CASES[3]], ids=[CASES[1][0], CASES[3][0]])
+def test_block_gate_fusion_is_bitwise_the_elementwise_path(case, recompute):
+    """The gated product m = gate * up and its backward in the GEMM epilogues
+    (the default where the ping-pong family takes the up and down products)
+    against the separate elementwise kernels (COLA_OPT_FUSE_GATE = 0): same
+    roundings, so every output and saved tensor is bitwise the same."""
+    name, n_seq, L, d, ffn, heads, r, act = case
+    ins = I.block_inputs(9, n_seq, L, d, ffn, r)
+    assert cola.get_option(cola.OPT_FUSE_GATE) == 1
+    fused = BlockRun(ins, n_seq, L, d, ffn, heads, r, act, recompute).run()
+    rf = fused.raw()
+    cola.set_option(cola.OPT_FUSE_GATE, 0)
+    try:
+        plain = BlockRun(ins, n_seq, L, d, ffn, heads, r, act, recompute).run()
+    finally:
+        cola.set_option(cola.OPT_FUSE_GATE, 1)
+    rp = plain.raw()
+    for k in rf:
+        assert np.array_equal(rf[k], rp[k]), k
+    # logical widths: the pad columns of a pitch are never written
+    widths = {"x1": d, "Z_gu": 2 * r, "gate": ffn, "up": ffn, "m": ffn}
+    slots = ("x1", "Z_gu") if recompute else ("x1", "Z_gu", "gate", "up", "m")
+    for slot in slots:
+        a, b = fused.slot(slot, widths[slot]), plain.slot(slot, widths[slot])
+        assert torch.equal(a.view(torch.int16), b.view(torch.int16)), slot
+
+
 def test_block_empty_batch():
     d = cola.block_desc(0, 16, 128, 96, 2, 16)
     ins = I.block_inputs(3, 1, 16, 128, 96, 16)
