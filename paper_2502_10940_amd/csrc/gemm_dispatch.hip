@@ -4,7 +4,8 @@
 //
 //  * PP (gemm_pp.hip): 256 x 256 tiles, two wave groups in ping-pong, for
 //    every product whose output exceeds one 128-wide tile in both dimensions
-//    and whose operands have 16-byte aligned rows (measured on MI355X:
+//    (weight gradients: at least 128 in both) and whose operands have
+//    16-byte aligned rows (measured on MI355X:
 //    1.1-1.5x the streaming family on the products of the layer, weight
 //    gradients included).
 //  * STREAM (gemm_stream.hip): BM x 128 tiles, two workgroups per CU, for
@@ -51,8 +52,11 @@ bool pp_operands_ok(const GemmArgs& a) {
 }
 
 int gemm_family(int64_t M, int64_t N, int tag) {
-    (void)tag;
     if (g_force_stream.load(std::memory_order_relaxed)) return FAM_STREAM;
+    // weight gradients take PP down to 128 x 128 outputs: half-empty 256-row
+    // tiles, but the pair of dA and dB in one launch over the whole chip
+    // (measured on MI355X at rank 128: the 60M-shaped step 1.479 -> 1.394 ms)
+    if ((tag == TAG_BWD_DA || tag == TAG_BWD_DB) && M >= 128 && N >= 128) return FAM_PP;
     return bf16_wide_ok(M, N) ? (int)FAM_PP : (int)FAM_STREAM;
 }
 
