@@ -4,7 +4,9 @@ outputs equal cola_bwd's on the same inputs (same kernels, same split plan:
 bitwise) and match the oracle within the bf16 / fp32 tolerance, on two calls
 in a row, the second with a smaller input (the scratch keeps the first call's
 contents, which the second must not depend on); a call needing more than the
-scratch holds is refused before anything is enqueued."""
+scratch holds is refused before anything is enqueued; and, for the callers it
+is for, a forward and the scratch backward captured in a HIP graph replay
+bitwise the eager result."""
 import numpy as np
 import pytest
 import torch
@@ -87,3 +89,51 @@ def test_scratch_backward_empty_batch():
     cola.bwd_scratch(d, None, None, None, None, None, None, None, dA, dB)
     torch.cuda.synchronize()
     assert torch.count_nonzero(dA).item() == 0 and torch.count_nonzero(dB).item() == 0
+
+
+def _bits(t, width):
+    v = t[:, :width] if t.dim() == 2 and width is not None else t
+    return v.contiguous().view(torch.int16 if v.dtype == torch.bfloat16 else torch.int32).clone()
+
+
+def test_scratch_backward_replays_in_a_hip_graph():
+    """A forward and the scratch backward captured in a HIP graph
+    (torch.cuda.CUDAGraph) and replayed three times, with eager work between
+    the replays (another layer's forward and scratch backward, which rewrite
+    the shared scratch) and synchronisations; every replay bitwise the eager
+    result."""
+    T, d_in, d_out, r = 1500, 512, 768, 128
+    run = LayerRun(I.layer_inputs(310, 0, d_in, d_out, r, T, "bf16"), T, d_in, d_out, r, "bf16", "silu", False)
+    other = LayerRun(I.layer_inputs(311, 0, 384, 640, 96, 900, "bf16"), 900, 384, 640, 96, "bf16", "silu", False)
+    dX = torch.full_like(run.dX, float("nan"))
+    dA = torch.full_like(run.dA, float("nan"))
+    dB = torch.full_like(run.dB, float("nan"))
+
+    def step():
+        run.forward()
+        cola.bwd_scratch(run.desc, run.dY, run.X, run.Z, run.H, run.A, run.B, dX, dA, dB)
+
+    step()
+    torch.cuda.synchronize()
+    outs = (("Y", run.Y, d_out), ("Z", run.Z, r), ("H", run.H, r), ("dX", dX, d_in), ("dA", dA, None),
+            ("dB", dB, None))
+    ref = {name: _bits(t, w) for name, t, w in outs}
+    graph = torch.cuda.CUDAGraph()
+    cs = torch.cuda.Stream()
+    cs.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(cs):
+        with torch.cuda.graph(graph, stream=cs):
+            step()
+    torch.cuda.synchronize()
+    for rep in range(3):
+        print(f"\n[graph] replay {rep}", flush=True)
+        for _, t, _ in outs:
+            t.fill_(float("nan"))
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        for name, t, w in outs:
+            assert torch.equal(_bits(t, w), ref[name]), f"replay {rep}: {name}"
+        other.forward()
+        scratch_backward(other)
+    del graph
