@@ -35,13 +35,15 @@
 //    dS = P (dP - D), dV^T += dO^T P, dK^T += Q^T dS over the query blocks
 //    from the diagonal on) and dq of query block w (dQ^T += K^T dS^T over the
 //    key blocks up to the diagonal): nqb + 1 blocks of work on every wave.
+//    Both write their output blocks through a per-wave LDS stage so that a
+//    store instruction covers 16 rows x 64 contiguous bytes.
 //  * staged kernels: forward, backward dq (which also forms D) and backward
 //    dk, dv, one workgroup of 4 waves per (sequence, head, 128 queries or
 //    keys), 64 rows staged in LDS per barrier pair (the forward loads the
 //    next stage during the current one), the same block arithmetic.
-// Only blocks on the diagonal or holding rows past the sequence end are
-// masked.  Every LDS tile is row-major; transposed operands come from the
-// transposing reads.
+// The whole-sequence kernels evaluate the causal mask only on blocks on the
+// diagonal or holding rows past the sequence end.  Every LDS tile is
+// row-major; transposed operands come from the transposing reads.
 // No atomics: each output element is written by one lane, in a fixed order
 // of summation (bitwise reproducible).
 #include <math.h>
@@ -675,7 +677,6 @@ __global__ __launch_bounds__(NW * 64) void attn_bwd_dkdv_kernel(AttnArgs a) {
 // sequence end, are masked.
 // ---------------------------------------------------------------------------
 constexpr int LMAX = 256;
-
 
 // Rows 0 .. L-1 of one head (zeros from L to the next multiple of 32) into a
 // row-major LDS tile, NB chunk pairs (elements i, i + HD/2) per thread of NTHR:
