@@ -157,15 +157,9 @@ def test_block_empty_batch():
         assert torch.count_nonzero(g).item() == 0, k
 
 
-def test_block_1b_fullsize_sampled_sequences():
-    """The LLaMA-1B-shaped block (T = 128 x 256, d = 2048, ffn = 5461, 32 heads,
-    r = 512): CoLA and CoLA-M bitwise equal over every output; x2, dx0 and the
-    saved x1 of three whole sequences against the oracle run on those
-    sequences alone (the weight gradients sum over every sequence and are
-    checked at the small shapes)."""
-    n_seq, L, d, ffn, heads, r = 128, 256, 2048, 5461, 32, 512
+def _fullsize_sampled(n_seq, L, d, ffn, heads, r, seed, seqs):
     print(f"\n[block fullsize] n_seq={n_seq} L={L} d={d} ffn={ffn} heads={heads} r={r}", flush=True)
-    ins = I.block_inputs(41, n_seq, L, d, ffn, r)
+    ins = I.block_inputs(seed, n_seq, L, d, ffn, r)
     a = BlockRun(ins, n_seq, L, d, ffn, heads, r, "silu", False).run()
     res_a = a.results()
     ra = a.raw()
@@ -180,7 +174,8 @@ def test_block_1b_fullsize_sampled_sequences():
     assert np.array_equal(x1a, b.slot("x1").view(torch.int16).cpu().numpy())
     x1 = b.slot("x1").float().cpu().numpy().astype(np.float64)
     del b
-    for s in (0, 63, 127):
+    torch.cuda.empty_cache()
+    for s in seqs:
         rows = slice(s * L, (s + 1) * L)
         sub = {k: I.Tensor(v.store[rows] if k in ("x0", "dx2") else v.store, "bf16") for k, v in ins.items()}
         ref, saved = oracle_block(sub, 1, L, d, ffn, heads, r, "silu", False)
@@ -188,3 +183,20 @@ def test_block_1b_fullsize_sampled_sequences():
             e = relerr(res_a[k][rows], ref[k])
             assert e <= TOL, f"sequence {s} {k}: {e:.3e}"
         assert relerr(x1[rows], saved["x1"]) <= TOL
+
+
+def test_block_7b_fullsize_sampled_sequences():
+    """The LLaMA-7B-shaped block (T = 64 x 256, d = 4096, ffn = 11008, 32 heads
+    of 128, r = 1024: the staged attention kernels at full size), as the 1B
+    test below: CoLA and CoLA-M bitwise equal over every output, x2, dx0 and
+    x1 of two whole sequences against the oracle run on them alone."""
+    _fullsize_sampled(64, 256, 4096, 11008, 32, 1024, 43, (0, 63))
+
+
+def test_block_1b_fullsize_sampled_sequences():
+    """The LLaMA-1B-shaped block (T = 128 x 256, d = 2048, ffn = 5461, 32 heads,
+    r = 512): CoLA and CoLA-M bitwise equal over every output; x2, dx0 and the
+    saved x1 of three whole sequences against the oracle run on those
+    sequences alone (the weight gradients sum over every sequence and are
+    checked at the small shapes)."""
+    _fullsize_sampled(128, 256, 2048, 5461, 32, 512, 41, (0, 63, 127))
