@@ -3,10 +3,11 @@ C ABI) against the fp64 block oracle (oracle/block.py) on the same seeded
 inputs: the block output x2, the input gradient dx0, all thirteen parameter
 gradients and the saved residual and pre-activations, element by element over
 whole tensors, in CoLA and in CoLA-M, within the bf16 tolerance; CoLA-M
-bitwise equal to CoLA; bitwise run-to-run determinism; the empty batch.  At
-the LLaMA-1B block shape the full-size run is checked on sampled whole
-sequences (attention mixes tokens only within a sequence, so the oracle runs
-those sequences alone) and CoLA-M against CoLA bitwise over everything."""
+bitwise equal to CoLA; bitwise run-to-run determinism; the empty batch; the
+fused gated product bitwise the elementwise one.  At the LLaMA-1B and 7B
+block shapes the full-size run is checked on sampled whole sequences
+(attention mixes tokens only within a sequence, so the oracle runs those
+sequences alone) and CoLA-M against CoLA bitwise over everything."""
 import numpy as np
 import pytest
 import torch
