@@ -72,6 +72,9 @@ def parse():
 
 
 COPY_BYTES = 1 << 30
+# the workload of the headline line (LLaMA-1B-shaped block); its counter readings sit at the
+# top level of profiles/traffic.json
+HEADLINE_WORKLOAD = 4
 KERNEL_TAGS = {0: "fwd_z_sigma", 1: "fwd_y", 2: "bwd_dz", 3: "bwd_dx", 4: "bwd_da", 5: "bwd_db",
                7: "dense_fwd", 8: "dense_dx", 9: "dense_dw"}
 
@@ -104,11 +107,13 @@ def _pmc_rows(path, counter):
     return rows
 
 
-def traffic_summary(fetch_csv, write_csv, copy_fetch_csv, copy_write_csv):
+def traffic_summary(fetch_csv, write_csv, copy_fetch_csv, copy_write_csv, workload=4):
     """HBM bytes per launch for each GEMM kernel class, from rocprofv3 --pmc
     FETCH_SIZE and WRITE_SIZE (KiB per dispatch), each scaled by the ratio of
     the known bytes of a plain 1 GiB copy to what the same counter reads for
-    that copy."""
+    that copy.  The headline workload's classes sit at the top level of
+    profiles/traffic.json, another workload's under "workload_<n>"; the other
+    sections of the file are kept."""
     import hashlib
     import re
 
@@ -138,7 +143,7 @@ def traffic_summary(fetch_csv, write_csv, copy_fetch_csv, copy_write_csv):
             cls = "bwd_da_db" if "pair_kernel" in name else KERNEL_TAGS.get(int(m.group(1)))
             per.setdefault(cls, {}).setdefault(key, []).append(v * 1024.0 * scale)
     h = kernel_source_hash()
-    out = {"_note": "HBM bytes per launch from rocprofv3 FETCH_SIZE + WRITE_SIZE, scaled by a "
+    sec = {"_note": "HBM bytes per launch from rocprofv3 FETCH_SIZE + WRITE_SIZE, scaled by a "
                     "1 GiB copy (fetch factor %.4f, write factor %.4f; a read-only 1 GiB pass gives fetch "
                     "factor %s)" % (ff, fw, "%.4f" % ff_ro if ff_ro else "n/a"),
            "_fetch_factor": ff, "_write_factor": fw, "_fetch_factor_read_only": ff_ro}
@@ -147,14 +152,25 @@ def traffic_summary(fetch_csv, write_csv, copy_fetch_csv, copy_write_csv):
         w = d.get("write", [])
         if not f or not w:
             continue
-        out[cls] = {"bytes_per_launch": sum(f) / len(f) + sum(w) / len(w),
+        sec[cls] = {"bytes_per_launch": sum(f) / len(f) + sum(w) / len(w),
                     "fetch_bytes_per_launch": sum(f) / len(f),
                     "write_bytes_per_launch": sum(w) / len(w),
                     "launches": len(f), "source_sha256_16": h}
     path = os.path.join(ROOT, "profiles", "traffic.json")
+    out = {}
+    if os.path.exists(path):
+        try:
+            out = json.load(open(path))
+        except (OSError, ValueError):
+            out = {}
+    if workload == HEADLINE_WORKLOAD:
+        out = {k: v for k, v in out.items() if k.startswith("workload_")}
+        out.update(sec)
+    else:
+        out["workload_%d" % workload] = sec
     with open(path, "w") as fh:
         json.dump(out, fh, indent=1, sort_keys=True)
-    print(json.dumps(out), flush=True)
+    print(json.dumps(sec), flush=True)
 
 
 def algo_flops_cola(T, d_in, d_out, r):
@@ -374,7 +390,7 @@ def kernel_source_hash():
     return h.hexdigest()[:16]
 
 
-def load_traffic(kernel):
+def load_traffic(kernel, workload=4):
     """HBM bytes per launch measured by rocprofv3 counters (profiles/traffic.json),
     or None when absent or taken on a different kernel source."""
     path = os.path.join(ROOT, "profiles", "traffic.json")
@@ -384,6 +400,8 @@ def load_traffic(kernel):
         rec = json.load(open(path))
     except (OSError, ValueError):
         return None
+    if workload != HEADLINE_WORKLOAD:
+        rec = rec.get("workload_%d" % workload, {})
     ent = rec.get(kernel)
     if not ent:
         return None
@@ -616,6 +634,7 @@ def workload_record(cfg, args):
     kern = events_pass(cola, h.step("cola_1s") if main_mode == "cola" else h.step(main_mode), 3)
     if kern:
         dom, rec["roofline"] = roofline_of(kern, peak)
+        rec["roofline"]["traffic"] = load_traffic(dom, cfg)
     rec["setup_s"] = round(setup, 1)
     del h
     torch.cuda.empty_cache()
@@ -736,7 +755,7 @@ def per_projection(args):
 def main():
     args = parse()
     if args.traffic_from:
-        traffic_summary(*args.traffic_from)
+        traffic_summary(*args.traffic_from, workload=args.workload)
         return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (got --gpus {args.gpus}); this build has no "

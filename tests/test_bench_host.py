@@ -142,3 +142,37 @@ def test_bench_flops_equal_oracle_mac_count(shape):
     oracle.dense_fwd(X, W)
     oracle.dense_bwd(X, W, dY)
     assert bench.algo_flops_dense(T, d_in, d_out) == 2 * oracle.macs()
+
+
+def test_traffic_summary_keeps_workload_sections(tmp_path, monkeypatch):
+    """Counter readings of another workload go to their own section of
+    traffic.json; a later headline summary replaces only the top level."""
+    (tmp_path / "profiles").mkdir()
+    monkeypatch.setattr(bench, "ROOT", str(tmp_path))
+    monkeypatch.setattr(bench, "kernel_source_hash", lambda: "0123456789abcdef")
+    gib_kib = bench.COPY_BYTES / 1024.0
+    pair = "void gemm_pp_pair_kernel<64, 1, 1, 1, 4>(GemmArgs, GemmArgs, long) [clone .kd]"
+    copy = "void at::native::elementwise_kernel<128, 4>(int, copy_functor) [clone .kd]"
+    cf, cw = tmp_path / "cf.csv", tmp_path / "cw.csv"
+    write_pmc(cf, "FETCH_SIZE", [(copy, 0.8 * gib_kib)])
+    write_pmc(cw, "WRITE_SIZE", [(copy, gib_kib)])
+    for wl, kib in ((2, 10.0), (4, 100.0), (3, 30.0)):
+        f, w = tmp_path / f"f{wl}.csv", tmp_path / f"w{wl}.csv"
+        write_pmc(f, "FETCH_SIZE", [(pair, kib)])
+        write_pmc(w, "WRITE_SIZE", [(pair, 1.0)])
+        bench.traffic_summary(str(f), str(w), str(cf), str(cw), workload=wl)
+    out = json.load(open(tmp_path / "profiles" / "traffic.json"))
+    assert out["bwd_da_db"]["fetch_bytes_per_launch"] == pytest.approx(100.0 * 1024 * 1.25)
+    assert out["workload_2"]["bwd_da_db"]["fetch_bytes_per_launch"] == pytest.approx(10.0 * 1024 * 1.25)
+    assert out["workload_3"]["bwd_da_db"]["fetch_bytes_per_launch"] == pytest.approx(30.0 * 1024 * 1.25)
+    assert bench.load_traffic("bwd_da_db", 2) == pytest.approx(10.0 * 1024 * 1.25 + 1024)
+    assert bench.load_traffic("bwd_da_db") == pytest.approx(100.0 * 1024 * 1.25 + 1024)
+    assert bench.load_traffic("bwd_da_db", 5) is None
+    # a new headline reading keeps the other workloads' sections
+    f, w = tmp_path / "f4b.csv", tmp_path / "w4b.csv"
+    write_pmc(f, "FETCH_SIZE", [(pair, 50.0)])
+    write_pmc(w, "WRITE_SIZE", [(pair, 1.0)])
+    bench.traffic_summary(str(f), str(w), str(cf), str(cw))
+    out = json.load(open(tmp_path / "profiles" / "traffic.json"))
+    assert out["bwd_da_db"]["fetch_bytes_per_launch"] == pytest.approx(50.0 * 1024 * 1.25)
+    assert set(k for k in out if k.startswith("workload_")) == {"workload_2", "workload_3"}
