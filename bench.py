@@ -62,6 +62,8 @@ def parse():
                     help="per-projection kernel-class durations of the workload (event-timed, one stream) and exit")
     ap.add_argument("--library-baseline", action="store_true",
                     help="time hipBLASLt (torch.matmul) on the workload's GEMM shapes and exit")
+    ap.add_argument("--hbm-ceilings", action="store_true",
+                    help="time plain read / write / copy / add passes over 1 GiB and exit")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run only a plain 1 GiB device copy (3 times), for scaling HBM counters")
     ap.add_argument("--traffic-from", nargs=4, metavar=("FETCH_CSV", "WRITE_CSV", "COPY_FETCH_CSV",
@@ -95,6 +97,42 @@ def copy_calibration():
         f.sum()
     torch.cuda.synchronize()
     print(json.dumps({"copy_calibration_bytes": COPY_BYTES, "repeats": 3, "read_only_pass": "sum"}), flush=True)
+
+
+def hbm_ceilings(nbytes=COPY_BYTES, reps=10):
+    """What this machine's HBM sustains for plain streaming patterns over nbytes
+    buffers (torch's own kernels, the median of `reps` event-timed launches
+    after two warm-up ones): a read-only pass (row sums), a write-only pass (a
+    fill), a copy (one read and one write stream) and two reads with one
+    write (an add): the practical ceilings for kernels that read and write,
+    beside the nominal 8 TB/s."""
+    import torch
+    n = nbytes // 4
+    a = torch.ones(n, dtype=torch.float32, device="cuda:0")
+    b = torch.ones(n, dtype=torch.float32, device="cuda:0")
+    c = torch.empty(n, dtype=torch.float32, device="cuda:0")
+    # read-only: row sums over 65536 rows of 16 KB (a single full reduction
+    # keeps too few loads in flight: 3.9 against 6.1 TB/s, measured)
+    pats = {"read": (lambda: a.view(65536, -1).sum(1), 1), "write": (lambda: c.fill_(2.0), 1),
+            "copy": (lambda: c.copy_(a), 2), "read2_write1": (lambda: torch.add(a, b, out=c), 3)}
+    out = {"buffer_bytes": nbytes}
+    for name, (fn, streams) in pats.items():
+        for _ in range(2):
+            fn()
+        times = []
+        for _ in range(reps):
+            s = torch.cuda.Event(enable_timing=True)
+            e = torch.cuda.Event(enable_timing=True)
+            s.record()
+            fn()
+            e.record()
+            torch.cuda.synchronize()
+            times.append(s.elapsed_time(e))
+        ms = sorted(times)[len(times) // 2]
+        out[name + "_gbs"] = round(streams * nbytes / (ms * 1e6), 1)
+    del a, b, c
+    torch.cuda.empty_cache()
+    return out
 
 
 def _pmc_rows(path, counter):
@@ -768,6 +806,9 @@ def main():
     if args.copy_calibration:
         copy_calibration()
         return
+    if args.hbm_ceilings:
+        print(json.dumps({"hbm_ceilings": hbm_ceilings()}), flush=True)
+        return
     cola.lib()
     if args.library_baseline:
         library_baseline(args)
@@ -850,6 +891,9 @@ def main():
         "tokens_per_s": round(T / (ms / 1e3), 1),
         "sclk_mhz": sampler.median(),
     }
+    if dtype == "bf16" and not args.only:
+        # the box's streaming ceilings, for the HBM-bound records below
+        out["hbm_ceilings"] = hbm_ceilings()
     if args.workload == 4 and main_mode == "cola":
         # the target: 60 % of the bf16 dense MFMA peak on this block; how far
         # the step is from it, as a time ratio and in ms
@@ -907,7 +951,27 @@ def main():
         out["block"] = block_record(args.workload, args)
     if not args.no_workloads and args.only is None:
         out["workloads"] = {str(c): workload_record(c, args) for c in (1, 2, 3, 5) if c != args.workload}
+        box_relative(out["workloads"], out.get("hbm_ceilings"))
     print(json.dumps(out), flush=True)
+
+
+def box_relative(records, ceilings):
+    """HBM-bound dominant kernels of the workload records against what this
+    box's HBM sustains for a read-only pass and for a copy (hbm_ceilings), beside
+    their fraction of the nominal 8 TB/s: achieved GB/s of the algorithmic
+    bytes, and of the measured traffic where the counters are stored."""
+    if not ceilings:
+        return
+    for rec in records.values():
+        rl = rec.get("roofline")
+        if not rl or rl.get("bound") != "hbm":
+            continue
+        meas = rl.get("traffic")
+        gbs = {"algorithmic": rl["achieved"]}
+        if meas:
+            gbs["measured_traffic"] = round(meas / (rl["avg_us"] * 1e3), 1)
+        rl["vs_box"] = {k: {"gbs": v, "of_read_only": round(v / ceilings["read_gbs"], 3),
+                            "of_copy": round(v / ceilings["copy_gbs"], 3)} for k, v in gbs.items()}
 
 
 if __name__ == "__main__":

@@ -176,3 +176,17 @@ def test_traffic_summary_keeps_workload_sections(tmp_path, monkeypatch):
     out = json.load(open(tmp_path / "profiles" / "traffic.json"))
     assert out["bwd_da_db"]["fetch_bytes_per_launch"] == pytest.approx(50.0 * 1024 * 1.25)
     assert set(k for k in out if k.startswith("workload_")) == {"workload_2", "workload_3"}
+
+
+def test_box_relative_only_for_hbm_bound_records():
+    recs = {"2": {"roofline": {"bound": "hbm", "achieved": 4000.0, "avg_us": 50.0, "traffic": 250e6}},
+            "5": {"roofline": {"bound": "mfma", "achieved": 1200.0, "avg_us": 300.0}},
+            "1": {}}
+    bench.box_relative(recs, {"read_gbs": 6000.0, "copy_gbs": 5000.0})
+    v = recs["2"]["roofline"]["vs_box"]
+    assert v["algorithmic"] == {"gbs": 4000.0, "of_read_only": pytest.approx(0.667, abs=1e-3),
+                                "of_copy": 0.8}
+    assert v["measured_traffic"]["gbs"] == pytest.approx(5000.0)
+    assert v["measured_traffic"]["of_copy"] == 1.0
+    assert "vs_box" not in recs["5"]["roofline"]
+    bench.box_relative(recs, None)      # no ceilings measured: nothing added, no error
