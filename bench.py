@@ -599,6 +599,21 @@ class SclkSampler:
         return v[len(v) // 2]
 
 
+# shader clock (MHz) at which the nominal MFMA peaks are quoted
+NOMINAL_SCLK_MHZ = 2400.0
+
+
+def at_clock(roofline, sclk_mhz):
+    """Beside the fraction of the nominal peak (quoted at 2.4 GHz), an
+    MFMA-bound kernel's fraction of the peak at the shader clock sampled during
+    the run (the clock falls to 1.4-2.1 GHz under sustained load on MI355X)."""
+    if roofline.get("bound") != "mfma" or not sclk_mhz:
+        return
+    p = roofline["peak"] * sclk_mhz / NOMINAL_SCLK_MHZ
+    roofline["peak_at_sclk"] = round(p, 1)
+    roofline["frac_at_sclk"] = round(roofline["achieved"] / p, 4)
+
+
 def roofline_of(kernels, peak):
     """The dominant kernel class (largest total time) against its roofline:
     MFMA-bound when its algorithmic intensity is above the ridge point, else
@@ -673,6 +688,7 @@ def workload_record(cfg, args):
     if kern:
         dom, rec["roofline"] = roofline_of(kern, peak)
         rec["roofline"]["traffic"] = load_traffic(dom, cfg)
+        at_clock(rec["roofline"], rec["sclk_mhz"])
     rec["setup_s"] = round(setup, 1)
     del h
     torch.cuda.empty_cache()
@@ -939,6 +955,7 @@ def main():
     if kernels:
         dom, out["roofline"] = roofline_of(kernels, peak)
         out["roofline"]["traffic"] = load_traffic(dom)
+        at_clock(out["roofline"], out["sclk_mhz"])
         out["kernels"] = {k: {kk: (round(vv, 3) if isinstance(vv, float) else vv)
                               for kk, vv in v.items()} for k, v in kernels.items()}
     if not args.no_cpu_baseline and main_mode != "dense":

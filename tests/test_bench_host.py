@@ -190,3 +190,16 @@ def test_box_relative_only_for_hbm_bound_records():
     assert v["measured_traffic"]["of_copy"] == 1.0
     assert "vs_box" not in recs["5"]["roofline"]
     bench.box_relative(recs, None)      # no ceilings measured: nothing added, no error
+
+
+def test_roofline_at_sampled_clock():
+    r = {"bound": "mfma", "achieved": 1000.0, "peak": 2516.6}
+    bench.at_clock(r, 1800)
+    assert r["peak_at_sclk"] == pytest.approx(2516.6 * 0.75, abs=0.1)
+    assert r["frac_at_sclk"] == pytest.approx(1000.0 / (2516.6 * 0.75), abs=1e-4)
+    h = {"bound": "hbm", "achieved": 4000.0, "peak": 8000.0}
+    bench.at_clock(h, 1800)
+    assert "frac_at_sclk" not in h
+    m = {"bound": "mfma", "achieved": 1000.0, "peak": 2516.6}
+    bench.at_clock(m, None)
+    assert "frac_at_sclk" not in m
