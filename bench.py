@@ -549,14 +549,41 @@ class Harness:
 
 
 class SclkSampler:
-    """The GPU's current shader clock (MHz), sampled from the driver's sysfs
-    DPM table while a measurement runs; None where the table is not readable."""
+    """The GPU's current shader clock (MHz) and board power (W), sampled from
+    the driver's sysfs DPM table and power sensor while a measurement runs;
+    None where they are not readable."""
 
     def __init__(self):
         import glob
         self.files = sorted(glob.glob("/sys/class/drm/card*/device/pp_dpm_sclk"))
+        self.pfiles = sorted(glob.glob("/sys/class/drm/card*/device/hwmon/hwmon*/power1_input"))
         self.vals = []
+        self.pvals = []
         self._stop = None
+
+    @staticmethod
+    def _microwatts(path):
+        try:
+            with open(path) as fh:
+                return int(fh.read().strip())
+        except (OSError, ValueError):
+            return None
+
+    def read_power(self):
+        """Board power in W (the sum over the cards the sensors list), or None."""
+        vals = [self._microwatts(f) for f in self.pfiles]
+        vals = [v for v in vals if v is not None]
+        return sum(vals) / 1e6 if vals else None
+
+    def power(self):
+        """Median and maximum of the sampled board power and the power cap (W)."""
+        if not self.pvals:
+            return None
+        v = sorted(self.pvals)
+        caps = [self._microwatts(f.replace("power1_input", "power1_cap")) for f in self.pfiles]
+        caps = [c for c in caps if c]
+        return {"median": round(v[len(v) // 2], 1), "max": round(v[-1], 1),
+                "cap": round(sum(caps) / 1e6, 1) if caps else None, "samples": len(v)}
 
     def read(self):
         import re
@@ -582,6 +609,9 @@ class SclkSampler:
                 v = self.read()
                 if v is not None:
                     self.vals.append(v)
+                w = self.read_power()
+                if w is not None:
+                    self.pvals.append(w)
                 self._stop.wait(0.01)
 
         self._t = threading.Thread(target=loop, daemon=True)
@@ -678,6 +708,7 @@ def workload_record(cfg, args):
                                   "pct_of_peak": round(100.0 * fl / (ms * 1e9) / peak, 2),
                                   "tokens_per_s": round(h.T / (ms / 1e3), 1)}
     rec["sclk_mhz"] = sc.median()
+    rec["power_w"] = sc.power()
     if "dense" in rec["modes"]:
         for mode in modes:
             if mode != "dense":
@@ -740,6 +771,7 @@ def block_record(cfg, args):
             rec["modes"][m] = {"ms_per_step": round(ms, 4), "tokens_per_s": round(T / (ms / 1e3), 1),
                                "tflops": round((lin + attn) / (ms * 1e9), 2)}
     rec["sclk_mhz"] = sc.median()
+    rec["power_w"] = sc.power()
     # CoLA-M's activation memory against CoLA's, the caller's x0 counted in both
     rec["cola_m_memory_ratio"] = round((saved_b["cola_m"] + 2 * T * d) / (saved_b["cola"] + 2 * T * d), 4)
     rec["cola_m_overhead"] = round(rec["modes"]["cola_m"]["ms_per_step"] / rec["modes"]["cola"]["ms_per_step"] - 1,
@@ -906,6 +938,7 @@ def main():
         "pct_of_bf16_mfma_peak": round(100.0 * value / peak, 2),
         "tokens_per_s": round(T / (ms / 1e3), 1),
         "sclk_mhz": sampler.median(),
+        "power_w": sampler.power(),
     }
     if dtype == "bf16" and not args.only:
         # the box's streaming ceilings, for the HBM-bound records below

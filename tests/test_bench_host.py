@@ -203,3 +203,20 @@ def test_roofline_at_sampled_clock():
     m = {"bound": "mfma", "achieved": 1000.0, "peak": 2516.6}
     bench.at_clock(m, None)
     assert "frac_at_sclk" not in m
+
+
+def test_power_sampler_reads_sensor_files(tmp_path):
+    """Board power from hwmon power1_input (microwatts), summed over cards;
+    median, maximum and the cap from power1_cap."""
+    d = tmp_path / "hwmon0"
+    d.mkdir()
+    (d / "power1_input").write_text("1200000000\n")
+    (d / "power1_cap").write_text("1400000000\n")
+    s = bench.SclkSampler()
+    s.files, s.pfiles = [], [str(d / "power1_input")]
+    assert s.read_power() == pytest.approx(1200.0)
+    assert s.power() is None
+    s.pvals = [1100.0, 1300.0, 1200.0]
+    assert s.power() == {"median": 1200.0, "max": 1300.0, "cap": 1400.0, "samples": 3}
+    s.pfiles = [str(tmp_path / "missing")]
+    assert s.read_power() is None
