@@ -7,7 +7,9 @@ columns of dB for one rank index in every 256-wide block -- and the GPU must
 match them within the bf16 tolerance.  Unsampled outputs are checked for
 finiteness.  Every workload runs in CoLA and in CoLA-M mode.  The dense
 baseline runs at the 1B-shaped gate and down shapes the same way (rows of Y
-and dX, rows of dW)."""
+and dX, rows of dW).  The sampled rows of Z, H, Y and dX are also held to the
+reference that applies the path's bf16 storage policy (within 1e-3, Z and H
+bitwise on at least 99.9 % of their elements)."""
 import numpy as np
 import pytest
 import torch
@@ -17,6 +19,7 @@ from paper_2502_10940_amd import cola
 from paper_2502_10940_amd import inputs as I
 
 from layer_runner import NAN_BITS, LayerRun, empty, relerr, to_device
+from test_gpu_rounding import MIN_EQUAL, TOL as ROUNDED_TOL, rounded_layer
 
 pytestmark = pytest.mark.gpu
 
@@ -89,6 +92,15 @@ def test_fullsize_sampled(cfg, proj, recompute):
     for k, g in got.items():
         e = relerr(g, ref[k])
         assert e <= TOL, f"{k}: {e:.3e}"
+    # the same rows under the bf16 storage policy (tests/test_gpu_rounding.py):
+    # within 1e-3, Z and H bitwise on almost every element
+    rr = rounded_layer(X[rows], A, B, dY[rows], "silu")
+    for k, g in got.items():
+        e = relerr(g, rr[k])
+        assert e <= ROUNDED_TOL, f"{k} against the rounding-policy reference: {e:.3e}"
+        if k in ("Z", "H"):
+            same = float(np.mean(g == rr[k]))
+            assert same >= MIN_EQUAL, f"{k}: {same:.5f} bitwise equal"
     ref_dA, ref_dB = oracle.cola_wgrad_cols(X, A, B, dY, ranks, "silu")
     assert relerr(got_dA, ref_dA) <= TOL
     assert relerr(got_dB, ref_dB) <= TOL

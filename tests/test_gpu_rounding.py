@@ -36,6 +36,12 @@ def round_bf16(x):
 
 def reference(ins, act):
     X, A, B, dY = (ins[k].f64 for k in ("X", "A", "B", "dY"))
+    return rounded_layer(X, A, B, dY, act)
+
+
+def rounded_layer(X, A, B, dY, act):
+    """The layer under the storage policy for the tokens (rows) of X and dY
+    given; dA and dB are those tokens' contributions."""
     Z = round_bf16(oracle.dense_fwd(X, A))
     H_exact, _ = oracle.cola_up_from_z(Z, B, act)
     H = round_bf16(H_exact)
