@@ -1,4 +1,5 @@
-"""A seeded sweep of layer shapes around the kernels' decision points.
+"""Seeded sweeps of shapes around the kernels' decision points: single
+layers, grouped projections and the dense layer.
 
 Each of T, d_in, d_out and r is drawn from one of three bands -- below one
 32-wide MFMA tile, around the 128 / 256 tile edges (where the launcher
@@ -124,3 +125,105 @@ def test_shape_sweep(case, _device):
             if k in ("Z", "H"):
                 differ = int(np.sum(g != rr[k]))
                 assert differ <= 2 + 0.001 * g.size, f"{k}: {differ} of {g.size} elements differ"
+
+
+# ---- grouped projections (one X, several CoLA layers) and the dense layer ----
+
+def group_draws(seed=SEED + 1, n=24):
+    """(T, d_in, ranks, widths, dtype, act) with 1-4 projections."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    out = []
+    while len(out) < n:
+        T = _dim(rng, 300, 2000)
+        d_in = _dim(rng, 300, 1200)
+        k = int(rng.integers(1, 5))
+        ranks = [_dim(rng, 260, 400) for _ in range(k)]
+        widths = [_dim(rng, 300, 1200) for _ in range(k)]
+        if sum(T * r * (d_in + w) for r, w in zip(ranks, widths)) > MAX_WORK:
+            continue
+        dtype = "f32" if rng.random() < 0.2 else "bf16"
+        act = ("silu", "gelu", "identity")[int(rng.choice(3, p=[0.6, 0.25, 0.15]))]
+        out.append((T, d_in, ranks, widths, dtype, act, bool(rng.random() < 0.5)))
+    return out
+
+
+def dense_draws(seed=SEED + 2, n=24):
+    """(T, d_in, d_out, dtype, padded)."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    out = []
+    while len(out) < n:
+        T, d_in, d_out = _dim(rng, 300, 3000), _dim(rng, 300, 1500), _dim(rng, 300, 1500)
+        if T * d_in * d_out > MAX_WORK:
+            continue
+        out.append((T, d_in, d_out, "f32" if rng.random() < 0.2 else "bf16", bool(rng.random() < 0.5)))
+    return out
+
+
+GROUP_CASES = group_draws()
+DENSE_CASES = dense_draws()
+
+
+def test_group_and_dense_draws():
+    """Deterministic, within budget, and reaching one to four projections
+    (one to the limit of eight the ABI takes) and both dtypes (no GPU)."""
+    assert group_draws() == GROUP_CASES and dense_draws() == DENSE_CASES
+    assert {len(c[2]) for c in GROUP_CASES} == {1, 2, 3, 4}
+    assert {c[4] for c in GROUP_CASES} == {"bf16", "f32"} and {c[3] for c in DENSE_CASES} == {"bf16", "f32"}
+    assert {c[4] for c in DENSE_CASES} == {False, True}
+    assert all(T * di * do <= MAX_WORK for T, di, do, *_ in DENSE_CASES)
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("case", range(len(GROUP_CASES)),
+                         ids=[f"T{c[0]}-in{c[1]}-r{'_'.join(map(str, c[2]))}-out{'_'.join(map(str, c[3]))}-{c[4]}"
+                              f"-{c[5]}-{'colam' if c[6] else 'cola'}" for c in GROUP_CASES])
+def test_group_shape_sweep(case, _device):
+    from test_gpu_group import GroupRun, group_inputs, oracle_group
+    T, d_in, ranks, widths, dtype, act, recompute = GROUP_CASES[case]
+    print(f"\n[group sweep] case {case}: T={T} d_in={d_in} r={ranks} d_out={widths} {dtype} {act} "
+          f"recompute={recompute}", flush=True)
+    X, As, Bs, dYs = group_inputs(600 + case, T, d_in, ranks, widths, dtype)
+    ref = oracle_group(X, As, Bs, dYs, act)
+    got = GroupRun(X, As, Bs, dYs, T, d_in, ranks, widths, dtype, act, recompute).run().results()
+    for k, g in got.items():
+        gl = g if isinstance(g, list) else [g]
+        rl = ref[k] if isinstance(ref[k], list) else [ref[k]]
+        for p, (gp, rp) in enumerate(zip(gl, rl)):
+            assert np.all(np.isfinite(gp)), f"{k}[{p}]: non-finite values"
+            e = relerr(gp, rp)
+            assert e <= TOL[dtype], f"{k}[{p}]: {e:.3e} against the oracle"
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("case", range(len(DENSE_CASES)),
+                         ids=[f"T{c[0]}-{c[1]}x{c[2]}-{c[3]}-{'pad' if c[4] else 'tight'}" for c in DENSE_CASES])
+def test_dense_shape_sweep(case, _device):
+    from layer_runner import NAN_BITS, empty, to_device
+    T, d_in, d_out, dtype, padded = DENSE_CASES[case]
+    print(f"\n[dense sweep] case {case}: T={T} {d_in}->{d_out} {dtype} padded={padded}", flush=True)
+    ins = I.layer_inputs(700 + case, 0, d_in, d_out, 1, T, dtype, with_dense=True)
+    ldx = I.padded_ld(d_in, dtype) if padded else d_in
+    ldy = I.padded_ld(d_out, dtype) if padded else d_out
+    d = cola.dense_desc(T, d_in, d_out, dtype, ldx, ldy)
+    Xd = to_device(ins["X"].store, dtype, ldx)
+    Wd = to_device(ins["W"].store, dtype)
+    dYd = to_device(ins["dY"].store, dtype, ldy)
+    Y = empty(T, ldy, dtype, NAN_BITS[dtype])
+    dX = empty(T, ldx, dtype, NAN_BITS[dtype])
+    dW = torch.full((d_out, d_in), float("nan"), dtype=torch.float32, device=Xd.device)
+    ws = torch.empty(max(1, cola.dense_workspace_bytes(d, 0), cola.dense_workspace_bytes(d, 1)),
+                     dtype=torch.uint8, device=Xd.device)
+    cola.dense_fwd(d, Xd, Wd, Y, ws)
+    cola.dense_bwd(d, dYd, Xd, Wd, dX, dW, ws)
+    torch.cuda.synchronize()
+    for t, w in ((Y, d_out), (dX, d_in)):
+        if t.shape[1] > w:
+            assert torch.isnan(t[:, w:].float()).all(), "pad columns written"
+    X, W, dY = ins["X"].f64, ins["W"].f64, ins["dY"].f64
+    ref_Y = oracle.dense_fwd(X, W)
+    ref_dX, ref_dW = oracle.dense_bwd(X, W, dY)
+    for name, g, ref in (("Y", Y[:, :d_out], ref_Y), ("dX", dX[:, :d_in], ref_dX), ("dW", dW, ref_dW)):
+        a = g.double().cpu().numpy()
+        assert np.all(np.isfinite(a)), f"{name}: non-finite values"
+        e = relerr(a, ref)
+        assert e <= TOL[dtype], f"{name}: {e:.3e} against the oracle"
