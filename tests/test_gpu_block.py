@@ -2,7 +2,9 @@
 C ABI) against the fp64 block oracle (oracle/block.py) on the same seeded
 inputs: the block output x2, the input gradient dx0, all thirteen parameter
 gradients and the saved residual and pre-activations, element by element over
-whole tensors, in CoLA and in CoLA-M, within the bf16 tolerance; CoLA-M
+whole tensors, in CoLA and in CoLA-M, within the bf16 tolerance, and the
+block output and gradients also against the reference that applies the
+path's bf16 storage policy (tests/block_rounding.py) within 7.5e-3; CoLA-M
 bitwise equal to CoLA; bitwise run-to-run determinism; the empty batch; the
 fused gated product bitwise the elementwise one.  At the LLaMA-1B and 7B
 block shapes the full-size run is checked on sampled whole sequences
@@ -17,10 +19,15 @@ from paper_2502_10940_amd import cola
 from paper_2502_10940_amd import inputs as I
 
 from block_runner import BlockRun
+from block_rounding import rounded_block
+from test_gpu_rounding import round_bf16
 
 pytestmark = pytest.mark.gpu
 
 TOL = 1e-2
+# against the reference that applies the path's bf16 storage policy
+# (tests/block_rounding.py): two valid bf16 evaluations of the block
+ROUNDED_TOL = 7.5e-3
 
 # (name, n_seq, seq_len, d, ffn, heads, r, act)
 CASES = [
@@ -71,8 +78,15 @@ def test_block_against_oracle(case, recompute):
     run = BlockRun(ins, n_seq, L, d, ffn, heads, r, act, recompute).run()
     got = run.results()
     ref, saved = oracle_block(ins, n_seq, L, d, ffn, heads, r, act, recompute)
+    rx2, rdx0, rg = rounded_block(OB.Cfg(n_seq, L, d, ffn, heads, r, act=act), {k: v.f64 for k, v in ins.items()},
+                                  ins["x0"].f64, ins["dx2"].f64, round_bf16)
+    rr = {"x2": rx2, "dx0": rdx0, **{"d" + k: v for k, v in rg.items()}}
+    worst = sorted(((relerr(got[k], rr[k]), k) for k in ref if ref[k].any()), reverse=True)[:3]
+    print("against the storage-policy reference: " + " ".join(f"{k}={e:.2e}" for e, k in worst), flush=True)
     for k in ref:
         assert np.isfinite(got[k]).all(), k
+        if ref[k].any():
+            assert relerr(got[k], rr[k]) <= ROUNDED_TOL, f"{k}: {relerr(got[k], rr[k]):.3e} (storage policy)"
         if not ref[k].any():
             # identically zero by the method's structure: with one token per
             # sequence the softmax is constant, so q and k get no gradient;
