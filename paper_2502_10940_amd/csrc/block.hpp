@@ -85,10 +85,11 @@ hipError_t launch_up_projection(int64_t T, int64_t d_out, int64_t r, const void*
 // stores dg = dm u and du = dm g instead (g, u, dg, du with pitch ld); each
 // sets *fused to whether the fused epilogue ran (the ping-pong family takes
 // the product and the fusion option is on), else the caller forms the
-// products with the elementwise kernels.
+// products with the elementwise kernels.  keep_u false: a fused forward
+// stores m only, leaving the last projection's Y unwritten.
 int group_fwd_gated(const cola_group_desc* desc, const void* X, const void* A_all, const void* const* B,
                     void* const* Y, void* Z_all, void* H_all, void* ws, size_t ws_bytes, cola_stream_t stream,
-                    const void* g, int64_t ld, void* m, bool* fused);
+                    const void* g, int64_t ld, void* m, bool* fused, bool keep_u);
 int layer_bwd_gated(const cola_desc* desc, const void* dY, const void* X, const void* Z, const void* H,
                     const void* A, const void* B, void* dX, float* dA, float* dB, void* ws, size_t ws_bytes,
                     cola_stream_t stream, const void* g, const void* u, int64_t ld, void* dg, void* du,

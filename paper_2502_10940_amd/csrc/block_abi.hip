@@ -386,8 +386,10 @@ int cola_block_fwd(const cola_block_desc* desc, const cola_block_weights* w, con
             const void* B2[2] = {w->B_g, w->B_u};
             void* Y2[2] = {gt, u};
             bool fused = false;
+            // CoLA-M reads up again only after recomputing it, so the
+            // fused epilogue stores m alone there
             st = group_fwd_gated(&g, bn, w->A_gu, B2, Y2, SV(COLA_BLK_Z_GU), b.m ? nullptr : SV(COLA_BLK_H_GU), sub,
-                                 W.sub_bytes, stream, gt, b.ldf, m, &fused);
+                                 W.sub_bytes, stream, gt, b.ldf, m, &fused, !b.m);
             if (st != COLA_OK) return st;
             if (!fused && (st = ew(c, EW_MUL, b.ffn, gt, b.ldf, u, b.ldf, nullptr, 0, m, b.ldf, nullptr, 0)) != COLA_OK)
                 return st;

@@ -409,6 +409,7 @@ struct Gate {
     void* out;       // m (forward) or dg (backward)
     void* out2;      // du (backward)
     bool* fused;
+    bool keep_u;     // forward: the fused epilogue also stores u (else only m)
 };
 
 bool gate_fusion_on() { return get_option(OPT_FUSE_GATE) == 1; }
@@ -1117,7 +1118,9 @@ int group_forward(const GDims& g, int act, const void* X, const void* A_all, con
             *gate->fused = g.bf16 && gate_fusion_on() && g.ldy[q] == gate->ld && pp_takes(kg);
             if (*gate->fused) {
                 k2 = kg;
-                b2 = es * ((double)g.T * g.r[q] + (double)g.d_out[q] * g.r[q] + 3.0 * g.T * g.d_out[q]);
+                if (!gate->keep_u) k2.c = nullptr;
+                b2 = es * ((double)g.T * g.r[q] + (double)g.d_out[q] * g.r[q] +
+                           (gate->keep_u ? 3.0 : 2.0) * g.T * g.d_out[q]);
             }
         }
         e = timed(COLA_KC_FWD_Y, gemm_flops(g.T, g.d_out[q], g.r[q]), b2, s, [&] { return gemm(k2, g.bf16, s); });
@@ -1305,10 +1308,10 @@ namespace cola {
 
 int group_fwd_gated(const cola_group_desc* desc, const void* X, const void* A_all, const void* const* B,
                     void* const* Y, void* Z_all, void* H_all, void* ws, size_t ws_bytes, cola_stream_t stream,
-                    const void* g, int64_t ld, void* m, bool* fused) {
+                    const void* g, int64_t ld, void* m, bool* fused, bool keep_u) {
     if (!fused) return COLA_ERR_INVALID_ARG;
     *fused = false;
-    const Gate gate{g, nullptr, ld, m, nullptr, fused};
+    const Gate gate{g, nullptr, ld, m, nullptr, fused, keep_u};
     return guarded([&]() -> int {
         return group_fwd_checked(desc, X, A_all, B, Y, Z_all, H_all, ws, ws_bytes, stream, &gate);
     });
@@ -1320,7 +1323,7 @@ int layer_bwd_gated(const cola_desc* desc, const void* dY, const void* X, const 
                     bool* fused) {
     if (!fused) return COLA_ERR_INVALID_ARG;
     *fused = false;
-    const Gate gate{g, u, ld, dg, du, fused};
+    const Gate gate{g, u, ld, dg, du, fused, true};
     return guarded([&]() -> int {
         return bwd_checked(desc, dY, X, Z, H, A, B, dX, dA, dB, ws, ws_bytes, stream, &gate);
     });

@@ -591,11 +591,14 @@ __device__ __forceinline__ void epilogue_t_impl(const GemmArgs& a, const f32x16 
                         }
                     }
                 }
-                // exchange 2, then one store per piece
+                // exchange 2, then one store per piece (EPI_GATE without a
+                // first output stores only m)
+                if (EPI != EPI_GATE || C != nullptr) {
 #pragma unroll
-                for (int q = 0; q < 4; ++q) swap_rows16(o[0][q], o[1][q]);
-                store_bf16x8<FAST>(C, a.ldc, a.M, a.N, gx, gn, o[0]);
-                store_bf16x8<FAST>(C, a.ldc, a.M, a.N, gx + 16, gn, o[1]);
+                    for (int q = 0; q < 4; ++q) swap_rows16(o[0][q], o[1][q]);
+                    store_bf16x8<FAST>(C, a.ldc, a.M, a.N, gx, gn, o[0]);
+                    store_bf16x8<FAST>(C, a.ldc, a.M, a.N, gx + 16, gn, o[1]);
+                }
                 if constexpr (EPI == EPI_Z_H || EPI == EPI_DZ || EPI == EPI_GATE) {
                     if (Hp) {
 #pragma unroll
@@ -683,7 +686,7 @@ __device__ __forceinline__ void epilogue_t_act(const GemmArgs& a, const f32x16 (
         const float* c = reinterpret_cast<const float*>(a.c) + (int64_t)split * a.split_stride;
         fast = fast && (reinterpret_cast<uintptr_t>(c) & 15u) == 0 && a.ldc % 4 == 0;
     } else {
-        fast = fast && al(a.c, a.ldc, 8);
+        fast = fast && ((EPI == EPI_GATE && a.c == nullptr) || al(a.c, a.ldc, 8));
     }
     if constexpr (EPI == EPI_Z_H || EPI == EPI_DZ || EPI == EPI_GATE || EPI == EPI_DGATE)
         fast = fast && (a.aux == nullptr || al(a.aux, a.ldaux, 8));

@@ -20,7 +20,7 @@ enum Epilogue : int {
     EPI_DZ = 3,        // c = dZ = round(acc * sigma'(Z)), Z read from zin; aux = H if non-NULL
     EPI_H = 4,         // c = H = round(sigma(round(acc))): H of EPI_Z_H without storing Z (inference)
     // the gated MLP of the decoder block (ping-pong family only):
-    EPI_GATE = 5,      // c = u = round(acc); aux = m = round(g u), g read from zin
+    EPI_GATE = 5,      // c = u = round(acc) (not stored when c is NULL); aux = m = round(g u), g read from zin
     EPI_DGATE = 6,     // with dm = round(acc): c = round(dm u), aux = round(dm g); g from zin, u from zin2
 };
 
