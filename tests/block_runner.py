@@ -8,7 +8,6 @@ import numpy as np
 import torch
 
 from paper_2502_10940_amd import cola
-from paper_2502_10940_amd import inputs as I
 
 DEV = "cuda:0"
 

@@ -4,8 +4,6 @@ off-by-one mask, a recompute from the wrong saved tensor) must fail at least
 one pin.  Mistakes are planted in a temporary copy on the CPU; the real
 oracle is untouched."""
 import importlib.util
-import os
-import sys
 
 import pytest
 

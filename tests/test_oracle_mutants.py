@@ -2,7 +2,6 @@
 each (a dropped term, a wrong sign, a wrong operand, an off-by-one) must fail
 at least one pin.  Mistakes are planted in a temporary copy of the oracle's
 source on the CPU; the real oracle is untouched."""
-import os
 import subprocess
 
 import pytest
