@@ -843,8 +843,8 @@ def main():
         traffic_summary(*args.traffic_from, workload=args.workload)
         return
     if args.gpus != 1:
-        print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the library runs on a single GPU and has no "
-              "multi-GPU path", file=sys.stderr)
+        print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the library runs on a single GPU "
+              "and has no multi-GPU path", file=sys.stderr)
         sys.exit(2)
     import torch
     from paper_2502_10940_amd import cola
