@@ -72,3 +72,41 @@ def test_two_streams_bitwise_equal_serial():
         assert run.padding_untouched(), f"layer {i}: pad columns written"
         for k in exp:
             assert np.array_equal(got[k], exp[k]), f"layer {i} {LAYERS[i]}: {k} differs from the serial run"
+
+
+@pytest.mark.parametrize("fill", [0x00, 0xFF], ids=["zeros", "ones"])
+def test_workspace_contents_do_not_matter(fill):
+    """The workspace is scratch: whatever it holds before a call (zeros, or
+    all bits set, which reads as NaN in bf16 and fp32) the outputs are
+    bitwise those of a fresh run, so no kernel reads workspace it has not
+    written (split partials, packed weights, CoLA-M's H)."""
+    reference = make_runs()
+    for run in reference:
+        run.run()
+    runs = make_runs()
+    for run in runs:
+        run.ws.fill_(fill)
+    torch.cuda.synchronize()
+    for i, (run, ref) in enumerate(zip(runs, reference)):
+        run.run()
+        got, exp = run.raw(), ref.raw()
+        for k in exp:
+            assert np.array_equal(got[k], exp[k]), f"layer {i} {LAYERS[i]}: {k} depends on the workspace contents"
+
+
+@pytest.mark.parametrize("recompute", [False, True], ids=["cola", "colam"])
+def test_block_workspace_and_saved_contents_do_not_matter(recompute):
+    """The decoder block's workspace and saved buffer start with all bits
+    set: the forward writes every saved tensor it keeps and the backward
+    reads nothing of the workspace it has not written."""
+    from block_runner import BlockRun
+    shape = (2, 100, 256, 270, 4, 64)
+    ins = I.block_inputs(33, shape[0], shape[1], shape[2], shape[3], shape[5])
+    ref = BlockRun(ins, *shape, "silu", recompute).run().raw()
+    run = BlockRun(ins, *shape, "silu", recompute)
+    run.ws.fill_(0xFF)
+    run.saved.fill_(0xFF)
+    torch.cuda.synchronize()
+    got = run.run().raw()
+    for k in ref:
+        assert np.array_equal(got[k], ref[k]), f"{k} depends on the workspace or saved contents"
