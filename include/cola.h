@@ -71,10 +71,15 @@ typedef enum { COLA_F32 = 0, COLA_BF16 = 1 } cola_dtype;
  * paper names GeLU for its BERT runs without saying which form). */
 typedef enum { COLA_ACT_IDENTITY = 0, COLA_ACT_SILU = 1, COLA_ACT_GELU = 2 } cola_act;
 
+/* Largest row pitch, in elements, of any activation or weight (and so of
+ * any width): 2^22.  Wider descriptors are refused with COLA_ERR_BAD_SHAPE. */
+#define COLA_MAX_PITCH (1LL << 22)
+
 typedef enum {
     COLA_OK = 0,
     COLA_ERR_INVALID_ARG = 1,      /* NULL desc/pointer, bad enum, H vs recompute mismatch */
-    COLA_ERR_BAD_SHAPE = 2,        /* d_in, d_out or r < 1, T < 0, ld < width, size overflow */
+    COLA_ERR_BAD_SHAPE = 2,        /* d_in, d_out or r < 1, T < 0, ld < width, a row pitch above
+                                      COLA_MAX_PITCH, size overflow */
     COLA_ERR_WORKSPACE = 3,        /* ws_bytes below the size cola_workspace_bytes() returns */
     COLA_ERR_HIP = 4,              /* a launch failed; cola_strerror() returns HIP's text */
     COLA_ERR_UNSUPPORTED = 5,      /* combination not compiled in */
@@ -296,6 +301,7 @@ int dense_bwd(const dense_desc* desc, const void* dY, const void* X, const void*
  * contiguous (overwritten), in the shapes of cola_block_weights.  The layout
  * of `saved` is the library's (cola_block_saved_slot gives each tensor's
  * offset and pitch).  bf16 only; head_dim 64 or 128; d and r multiples of 8;
+ * 3r and ffn, rounded up to multiples of 64, at most COLA_MAX_PITCH;
  * x0, x2, dx2, dx0, g1, g2, saved and ws 16-byte aligned (else
  * COLA_ERR_INVALID_ARG); n_seq and heads at most 65535.
  * Ownership, streams and errors as for cola_fwd; T = 0 enqueues nothing in

@@ -67,6 +67,7 @@ int check_block(const cola_block_desc* dsc, Blk* out) {
     if ((double)b.T * (double)(b.ffn > b.d ? b.ffn : b.d) > 4.0e15) return COLA_ERR_BAD_SHAPE;
     if (b.T > (int64_t(1) << 31)) return COLA_ERR_BAD_SHAPE;
     b.ld3 = lp64(3 * b.r); b.ld2 = lp64(2 * b.r); b.ld1 = lp64(b.r); b.ldf = lp64(b.ffn);
+    if (b.ld3 > kMaxPitch || b.ldf > kMaxPitch) return COLA_ERR_BAD_SHAPE;
     *out = b;
     return COLA_OK;
 }

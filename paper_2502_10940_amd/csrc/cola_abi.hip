@@ -115,6 +115,7 @@ hipError_t timed(int kc, double flops, double bytes, hipStream_t s, F&& launch) 
 // shapes and plans
 // ---------------------------------------------------------------------------
 constexpr int64_t kMaxDim = int64_t(1) << 40;   // keeps every byte count far from overflow
+static_assert(COLA_MAX_PITCH == kMaxPitch, "the public pitch limit is the kernels' limit");
 
 struct Dims {
     int64_t T, d_in, d_out, r, ldx, ldy, ldz;
@@ -138,7 +139,7 @@ int check_desc(const cola_desc* d, Dims* out) {
     x.ldy = d->ldy ? d->ldy : d->d_out;
     x.ldz = d->ldz ? d->ldz : d->r;
     if (x.ldx < x.d_in || x.ldy < x.d_out || x.ldz < x.r) return COLA_ERR_BAD_SHAPE;
-    if (x.ldx > kMaxDim || x.ldy > kMaxDim || x.ldz > kMaxDim) return COLA_ERR_BAD_SHAPE;
+    if (x.ldx > kMaxPitch || x.ldy > kMaxPitch || x.ldz > kMaxPitch) return COLA_ERR_BAD_SHAPE;
     // element counts of the largest operands must stay below 2^62
     const double big = (double)x.T * (double)(x.ldx > x.ldy ? x.ldx : x.ldy);
     if (big > 4.0e18 || (double)x.r * (double)(x.d_in > x.d_out ? x.d_in : x.d_out) > 4.0e18)
@@ -952,7 +953,7 @@ int check_group(const cola_group_desc* d, GDims* out) {
     }
     if (g.R > kMaxDim) return COLA_ERR_BAD_SHAPE;
     g.ldz = d->ldz ? d->ldz : g.R;
-    if (g.ldz < g.R || g.ldz > kMaxDim) return COLA_ERR_BAD_SHAPE;
+    if (g.ldz < g.R || g.ldz > kMaxPitch) return COLA_ERR_BAD_SHAPE;
     if ((double)g.T * (double)g.ldz > 4.0e18 || (double)g.R * (double)g.d_in > 4.0e18) return COLA_ERR_BAD_SHAPE;
     *out = g;
     return COLA_OK;

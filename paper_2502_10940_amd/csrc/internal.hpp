@@ -102,6 +102,12 @@ hipError_t launch_fill_zero(float* out, int64_t n, hipStream_t s);
 hipError_t launch_outer_grad(bool bf16, const void* dy, int64_t lddy, const void* p, int64_t ldp, void* out,
                              int64_t ldo, int64_t T, int64_t n, int act, hipStream_t s);
 
+// Largest row pitch (elements) of any operand: the 256 x 256 family reads a
+// K tile of a k-contiguous operand through a buffer descriptor whose range is
+// 2^31 bytes from the tile's first row, and 255 rows of this pitch fit it.
+// Descriptors with wider pitches are refused (COLA_ERR_BAD_SHAPE).
+constexpr int64_t kMaxPitch = int64_t(1) << 22;
+
 // K tile of the bf16 kernel: split-K chunks are multiples of it.
 constexpr int BF16_BK = 64;
 // K tile of the fp32 kernel.

@@ -94,6 +94,28 @@ def test_invalid_descriptors():
     assert fwd_status(d) == cola.ERR_BAD_SHAPE
 
 
+def test_row_pitch_limit():
+    """Row pitches up to COLA_MAX_PITCH (2^22 elements, what the 256 x 256
+    family's buffer descriptors reach) are taken; wider ones, and widths
+    beyond it, are refused before anything is enqueued."""
+    maxp = 1 << 22
+    hdr = open(os.path.join(ROOT, "include", "cola.h")).read()
+    assert "#define COLA_MAX_PITCH (1LL << 22)" in hdr
+    for ld in (dict(ldx=maxp), dict(ldy=maxp), dict(ldz=maxp)):
+        assert cola.workspace_bytes(cola.desc(16, 32, 32, 8, **ld), 1) > 0
+    for ld in (dict(ldx=maxp + 1), dict(ldy=maxp + 8), dict(ldz=maxp + 64)):
+        d = cola.desc(16, 32, 32, 8, **ld)
+        assert fwd_status(d) == cola.ERR_BAD_SHAPE
+        assert bwd_status(d) == cola.ERR_BAD_SHAPE
+        assert cola.workspace_bytes(d, 0) == 0 and cola.workspace_bytes(d, 1) == 0
+    assert cola.workspace_bytes(cola.desc(16, maxp + 8, 32, 8), 1) == 0
+    assert cola.group_workspace_bytes(cola.group_desc(16, 32, [8, 8], [32, 32], ldz=maxp + 64), 1) == 0
+    assert cola.group_workspace_bytes(cola.group_desc(16, 32, [8, 8], [32, 32], ldz=maxp), 1) > 0
+    assert cola.dense_workspace_bytes(cola.dense_desc(16, 32, 32, "bf16", maxp + 8, 32), 1) == 0
+    assert cola.block_saved_bytes(cola.block_desc(2, 64, 128, maxp + 1, 2, 8)) == 0
+    assert cola.block_saved_bytes(cola.block_desc(2, 64, 128, maxp - 64, 2, 8)) > 0
+
+
 def test_h_must_match_recompute():
     d = cola.desc(16, 32, 32, 8, recompute=False)
     assert fwd_status(d, H=None) == cola.ERR_INVALID_ARG
