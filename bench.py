@@ -38,15 +38,15 @@ HBM_PEAK_GBS = 8000.0
 
 def parse():
     ap = argparse.ArgumentParser()
-    ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--gpus", type=int, default=1, help="GPUs (one only: the library runs on a single GPU)")
+    ap.add_argument("--steps", type=int, default=20, help="timed steps of the headline pass")
+    ap.add_argument("--warmup", type=int, default=5, help="untimed steps before them")
     ap.add_argument("--workload", type=int, default=4, help="1..5 (default 4: LLaMA-1B-shaped block)")
-    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-cpu-baseline", action="store_true", help="skip timing the fp64 oracle on the host")
     ap.add_argument("--streams", type=int, default=2,
                     help="HIP streams the independent projections (or groups) of every step are spread over")
-    ap.add_argument("--no-dense", action="store_true")
-    ap.add_argument("--no-cola-m", action="store_true")
+    ap.add_argument("--no-dense", action="store_true", help="skip the dense-layer baseline")
+    ap.add_argument("--no-cola-m", action="store_true", help="skip the CoLA-M mode")
     ap.add_argument("--cpu-tokens", type=int, default=8192,
                     help="tokens per projection in the oracle's CPU sample")
     ap.add_argument("--no-fused", action="store_true",
@@ -56,7 +56,7 @@ def parse():
     ap.add_argument("--no-block", action="store_true", help="skip the decoder-block record")
     ap.add_argument("--no-workloads", action="store_true", help="skip the records of the other workloads")
     ap.add_argument("--sub-steps", type=int, default=50, help="timed steps of the block and workload records")
-    ap.add_argument("--sub-warmup", type=int, default=10)
+    ap.add_argument("--sub-warmup", type=int, default=10, help="untimed steps before them")
     ap.add_argument("--per-projection", action="store_true",
                     help="per-projection kernel-class durations of the workload (event-timed, one stream) and exit")
     ap.add_argument("--library-baseline", action="store_true",
