@@ -7,8 +7,9 @@ switches between the streaming and the 256 x 256 families and where the
 ragged-edge paths start), and several tiles wide -- together with the storage
 dtype, the activation, CoLA or CoLA-M, and tight or cache-line row pitches
 (tight pitches with odd widths take the guarded, unaligned paths).  Every
-draw runs forward and backward through the C ABI and is compared with the
-fp64 oracle (1e-2 bf16, 1e-5 fp32); bf16 draws are also held to the
+draw runs forward and backward through the C ABI (and the inference
+forward, whose Y must be the training forward's bit for bit) and is
+compared with the fp64 oracle (1e-2 bf16, 1e-5 fp32); bf16 draws are also held to the
 reference that applies the path's bf16 storage policy (1e-3, Z and H equal
 bit for bit except for the rare element next to a rounding boundary).  Pad
 columns must keep their NaN fill.  The draws are fixed by the seed, so a
@@ -107,6 +108,17 @@ def test_shape_sweep(case, _device):
                    ldx=pitch(d_in), ldy=pitch(d_out), ldz=pitch(r)).run()
     got = run.outputs()
     assert run.padding_untouched()
+    # the inference forward (K1 keeps only H) gives the training forward's Y bit for bit
+    from layer_runner import DEV, NAN_BITS, empty
+    di = cola.desc(T, d_in, d_out, r, dtype, act, False, pitch(d_in), pitch(d_out), pitch(r))
+    Yi = empty(T, pitch(d_out), dtype, NAN_BITS[dtype])
+    cola.infer(di, run.X, run.A, run.B, Yi,
+               torch.empty(max(1, cola.workspace_bytes(di, 2)), dtype=torch.uint8, device=DEV))
+    torch.cuda.synchronize()
+    bits = (lambda t: t.view(torch.int16)) if dtype == "bf16" else (lambda t: t.view(torch.int32))
+    assert torch.equal(bits(Yi[:, :d_out].contiguous()), bits(run.Y[:, :d_out].contiguous())), "inference Y"
+    if pitch(d_out) > d_out:
+        assert torch.isnan(Yi[:, d_out:].float()).all(), "inference wrote pad columns"
 
     X, A, B, dY = (ins[k].f64 for k in ("X", "A", "B", "dY"))
     Z, H, Y = oracle.cola_fwd(X, A, B, act)
