@@ -8,8 +8,10 @@ ragged-edge paths start), and several tiles wide -- together with the storage
 dtype, the activation, CoLA or CoLA-M, and tight or cache-line row pitches
 (tight pitches with odd widths take the guarded, unaligned paths).  Every
 draw runs forward and backward through the C ABI (and the inference
-forward, whose Y must be the training forward's bit for bit) and is
-compared with the fp64 oracle (1e-2 bf16, 1e-5 fp32); bf16 draws are also held to the
+forward, whose Y must be the training forward's bit for bit, and the other
+of CoLA / CoLA-M, whose outputs must be the same bits, dB within fp32
+rounding when the caller's H rows are not 16-byte aligned) and is compared
+with the fp64 oracle (1e-2 bf16, 1e-5 fp32); bf16 draws are also held to the
 reference that applies the path's bf16 storage policy (1e-3, Z and H equal
 bit for bit except for the rare element next to a rounding boundary).  Pad
 columns must keep their NaN fill.  The draws are fixed by the seed, so a
@@ -119,6 +121,21 @@ def test_shape_sweep(case, _device):
     assert torch.equal(bits(Yi[:, :d_out].contiguous()), bits(run.Y[:, :d_out].contiguous())), "inference Y"
     if pitch(d_out) > d_out:
         assert torch.isnan(Yi[:, d_out:].float()).all(), "inference wrote pad columns"
+    # the other mode (CoLA-M recomputes H) gives the same bits.  One
+    # exception: CoLA's dB reads H from the caller's rows, CoLA-M's from its
+    # own 16-byte aligned workspace; when the caller's rows are not aligned
+    # the two take different (each fixed) summation orders, so dB agrees to
+    # fp32 rounding only.
+    other_run = LayerRun(ins, T, d_in, d_out, r, dtype, act, not recompute,
+                         ldx=pitch(d_in), ldy=pitch(d_out), ldz=pitch(r)).run()
+    other, mine = other_run.raw(), run.raw()
+    h_aligned = (pitch(r) * (2 if dtype == "bf16" else 4)) % 16 == 0
+    for k in mine:
+        if k == "dB" and not h_aligned:
+            e = relerr(run.outputs()["dB"], other_run.outputs()["dB"])
+            assert e <= 1e-6, f"dB: CoLA and CoLA-M differ by {e:.3e}"
+        else:
+            assert np.array_equal(mine[k], other[k]), f"{k}: CoLA and CoLA-M differ"
 
     X, A, B, dY = (ins[k].f64 for k in ("X", "A", "B", "dY"))
     Z, H, Y = oracle.cola_fwd(X, A, B, act)
