@@ -811,6 +811,28 @@ def library_baseline(args):
     print(json.dumps(out), flush=True)
 
 
+def vendor_dense_step_ms(workload, reps=20, warmup=5):
+    """The dense layer's step on hipBLASLt (torch.matmul, bf16 in, fp32
+    accumulate): the median time of each of its GEMM shapes (Y = X W^T,
+    dX = dY W, dW = dY^T X per projection), summed over the step.  Context for
+    the speedup, which the bench line quotes against the dense layer on this
+    library's own kernels."""
+    import torch
+    from paper_2502_10940_amd import inputs as I
+    T = I.WORKLOADS[workload]["T"]
+    count = {}
+    for _, _, d_in, d_out in I.projections(workload):
+        for mnk in ((T, d_out, d_in), (T, d_in, d_out), (d_out, d_in, T)):
+            count[mnk] = count.get(mnk, 0) + 1
+    total = 0.0
+    for (M, N, K), n in sorted(count.items()):
+        a = torch.randn(M, K, device="cuda:0", dtype=torch.bfloat16)
+        b = torch.randn(K, N, device="cuda:0", dtype=torch.bfloat16)
+        total += n * timed_steps_median(lambda: torch.matmul(a, b), reps, warmup)
+        del a, b
+    return total
+
+
 def per_projection(args):
     """Kernel-class durations per projection: after 3 warm-up steps, each
     projection's forward and backward 5 times with an event pair around every
@@ -968,6 +990,13 @@ def main():
             out["speedup_vs_dense"] = round(res["dense"] / res["cola"], 3)
         if "cola_m" in res:
             out["cola_m"]["speedup_vs_dense"] = round(res["dense"] / res["cola_m"], 3)
+        if dtype == "bf16" and "cola" in res and not args.only:
+            # the same dense step on the vendor library, as context
+            vms = vendor_dense_step_ms(args.workload)
+            out["dense_hipblaslt"] = {"ms_per_step": round(vms, 4),
+                                      "tflops": round(flops_dense / (vms * 1e9), 2),
+                                      "speedup_cola_vs_it": round(vms / res["cola"], 3),
+                                      "how": "sum of per-shape medians of torch.matmul, 20 launches each"}
     if "fused" in res:
         # same algorithmic flops; q, k, v read one X and gate, up another
         out["fused_block"] = {"ms_per_step": round(res["fused"], 4),
